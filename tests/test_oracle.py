@@ -1,0 +1,368 @@
+"""Pins of the CPU oracle against facts the paper and the mathematics fix.
+
+None of these re-types the oracle's own formula: they use closed forms,
+hand-worked fixtures, the paper's printed budgets, invariants and brute-force
+enumeration on tiny inputs.
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2605_20600_amd import synth, workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+rng = np.random.default_rng(1234)
+
+
+# ---------------------------------------------------------------- Eq. (1)
+def test_attention_weights_sum_to_one():
+    L, d = 37, 16
+    q, K = rng.normal(size=d), rng.normal(size=(L, d))
+    o = oracle.attention(q, K, np.ones((L, d)))
+    assert np.allclose(o, 1.0, atol=1e-12, rtol=0)
+
+
+def test_attention_one_hot_and_uniform():
+    L, d = 9, 8
+    V = rng.normal(size=(L, d))
+    K = np.zeros((L, d))
+    q = np.zeros(d)
+    q[0] = 100.0
+    K[4, 0] = 100.0                      # logit 10000/sqrt(8) against 0
+    assert np.array_equal(oracle.attention(q, K, V), V[4])
+    o = oracle.attention(np.zeros(d), rng.normal(size=(L, d)), V)   # q = 0
+    assert np.allclose(o, V.mean(axis=0), atol=1e-14, rtol=0)
+
+
+def test_attention_two_token_closed_form_checks_scaling():
+    # logits differ by ln(3) only if the dot product is divided by sqrt(d):
+    # weights 3/4 and 1/4
+    d = 16
+    q = np.zeros(d)
+    q[1] = 1.0
+    K = np.zeros((2, d))
+    K[0, 1] = math.sqrt(d) * math.log(3.0)
+    V = np.zeros((2, d))
+    V[0, 0], V[1, 2] = 1.0, 1.0
+    o = oracle.attention(q, K, V)
+    assert abs(o[0] - 0.75) < 1e-14 and abs(o[2] - 0.25) < 1e-14 and o[1] == 0.0
+
+
+def test_attention_permutation_and_shift_invariance():
+    L, d = 23, 32
+    q, K, V = rng.normal(size=d), rng.normal(size=(L, d)), rng.normal(size=(L, d))
+    o = oracle.attention(q, K, V)
+    p = rng.permutation(L)
+    assert np.allclose(oracle.attention(q, K[p], V[p]), o, atol=1e-13, rtol=0)
+    u = rng.normal(size=d)                       # same logit offset for all keys
+    assert np.allclose(oracle.attention(q, K + u, V), o, atol=1e-12, rtol=0)
+
+
+# ------------------------------------------------------ Sec. 4 Step 2 grouping
+@pytest.mark.parametrize("L,tau", [(7, 0.9), (13, 0.9), (101, 0.85), (428, 0.95)])
+def test_grouping_uniform_attention(L, tau):
+    # q = 0: every weight is 1/L, so S(n) = n/L and n* = ceil(tau*L)
+    assert (tau * L) != int(tau * L)
+    g = oracle.group_head(np.zeros(8), rng.normal(size=(L, 8)), tau, 5)
+    assert g["n_star"] == math.ceil(tau * L)
+
+
+@pytest.mark.parametrize("delta", [0, 1, 5, 30])
+def test_grouping_one_hot_at_distance(delta):
+    L, d = 64, 8
+    K = np.zeros((L, d))
+    q = np.zeros(d)
+    q[3] = 30.0
+    K[L - 1 - delta, 3] = 30.0               # dominant key delta tokens back
+    g = oracle.group_head(q, K, 0.9, 10)
+    assert g["n_star"] == delta + 1
+    assert g["is_local"] == (1 if delta + 1 < 10 else 0)
+
+
+@pytest.mark.parametrize("r,L", [(0.8, 60), (0.95, 200), (0.5, 40)])
+def test_grouping_geometric_closed_form(r, L):
+    # the weight of the token i steps back is proportional to r^i, so
+    # S(n) = (1 - r^n) / (1 - r^L), n* = ceil(ln(1 - tau (1 - r^L)) / ln r);
+    # a forward (oldest-first) accumulation or a missing 1/sqrt(d) would differ
+    d, tau = 4, 0.9
+    q = np.zeros(d)
+    q[0] = math.sqrt(d)
+    K = np.zeros((L, d))
+    for j in range(L):
+        K[j, 0] = (L - 1 - j) * math.log(r)
+    x = math.log(1.0 - tau * (1.0 - r ** L)) / math.log(r)
+    assert abs(x - round(x)) > 1e-6
+    g = oracle.group_head(q, K, tau, 7)
+    assert g["n_star"] == math.ceil(x)
+    w = 6                                     # S(W_loc - 1) for W_loc = 7
+    assert abs(g["mass_window"] - (1 - r ** w) / (1 - r ** L)) < 1e-12
+
+
+def test_grouping_brute_force_tiny():
+    # enumerate every n on tiny caches with an independent numpy softmax
+    for trial in range(40):
+        L, d = int(rng.integers(1, 12)), 4
+        q, K = rng.normal(size=d) * 2, rng.normal(size=(L, d)) * 2
+        tau, wl = float(rng.uniform(0.3, 1.0)), int(rng.integers(1, 14))
+        s = K @ q / math.sqrt(d)
+        a = np.exp(s - s.max())
+        a /= a.sum()
+        mass = [a[L - n:].sum() for n in range(1, L + 1)]
+        ok = [n for n in range(1, L + 1) if mass[n - 1] >= tau - 1e-12]
+        g = oracle.group_head(q, K, tau, wl)
+        if any(abs(m - tau) < 1e-9 for m in mass):
+            continue                          # constructed near-tie, skip
+        assert g["n_star"] == ok[0]
+        assert g["is_local"] == int(ok[0] < wl)
+
+
+def test_planted_heads_are_labelled():
+    # synthetic analogue of the local/global attention maps: heads with a
+    # strong 2-D positional term are local, heads without one are global
+    for wl, slices in ((W.TINY, [(0, 0)]), (W.LUMINA768, [(0, 0), (31, 7)])):
+        t_g = wl.group_threshold - 1
+        for (layer, b) in slices:
+            amp = synth.amplitudes(wl)[layer, b]
+            for h in range(wl.heads):
+                q, k, v, kc, vc = synth.head_inputs(wl, layer, b, h)
+                g = oracle.group_head(q[t_g], torch.cat([kc, k[: t_g + 1]]), wl.tau,
+                                      wl.local_window)
+                assert g["is_local"] == int(amp[h] == 3.0), (wl.name, layer, b, h)
+                assert abs(g["mass_window"] - wl.tau) > 0.05     # clear margin
+
+
+# --------------------------------------------------------------- budgets
+def _golden_rows(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                yield [c.strip() for c in line.split("|")]
+
+
+def test_budgets_match_paper_table():
+    for N, rho, B in _golden_rows("budgets_tab_efficient.txt"):
+        num, den = map(int, rho.split("/"))
+        got = oracle.budgets(oracle.BUDGET_PAPER, [0, 1], int(N), 24, 48, (num, den))
+        assert got[0] == int(B)
+        assert got[1] == min(48, int(N))
+
+
+def test_budgets_whole_rows_for_workloads():
+    for wl in (W.LUMINA768.with_(rho=(1, 4)), W.LUMINA768.with_(rho=(1, 6)), W.LUMINA768,
+               W.JANUS7B.with_(budget_mode=W.BUDGET_PAPER)):
+        b = oracle.budgets(W.BUDGET_PAPER, [0], wl.num_visual, wl.row_len, wl.recent_len, wl.rho)
+        assert b[0] % wl.row_len == 0
+
+
+def test_budgets_total_mode_conserves_layer_total():
+    wl = W.JANUS7B
+    for trial in range(50):
+        labels = rng.integers(0, 2, size=wl.heads)
+        b = oracle.budgets(W.BUDGET_TOTAL, labels, wl.num_visual, wl.row_len, wl.recent_len, wl.rho)
+        total = (wl.num_visual * wl.rho[0] // wl.rho[1]) * wl.heads
+        assert b.sum() <= total
+        assert np.all(b[labels == 1] == wl.recent_len)
+        g = b[labels == 0]
+        if g.size:
+            assert np.all(g == g[0]) and g[0] % wl.row_len == 0
+            assert total - b.sum() < g.size * wl.row_len     # whole rows, floor
+            assert g[0] >= wl.recent_len
+
+
+def test_budgets_override_and_errors():
+    assert list(oracle.budgets(W.BUDGET_OVERRIDE, [1, 0], 100, 10, 20, override=[5, 100])) == [5, 100]
+    with pytest.raises(ValueError):
+        oracle.budgets(W.BUDGET_OVERRIDE, [1, 0], 100, 10, 20, override=[0, 5])
+    with pytest.raises(ValueError):
+        oracle.budgets(W.BUDGET_OVERRIDE, [1, 0], 100, 10, 20, override=[5, 101])
+
+
+# ------------------------------------------------------------ Eqs. (2)-(6)
+def test_ste_worked_example():
+    for keys, budget, u, rs, local, kept in _golden_rows("ste_worked_example.txt"):
+        kv = np.array([float(x) for x in keys.split()]).reshape(-1, 1)
+        num, den = map(int, rs.split("/"))
+        got, _ = oracle.update(list(range(10)), kv, np.ones(1), int(budget), local == "1", 2,
+                               (num, den), int(u))
+        assert list(got) == [int(x) for x in kept.split()], (keys, budget, u, rs, local)
+
+
+def _scores(Kvis, qsum, ret):
+    return np.array([sum(qsum[i] * Kvis[p, i] for i in range(Kvis.shape[1])) for p in ret])
+
+
+def test_ste_brute_force_subsets():
+    # per part, the kept set maximises the summed score (the appendix objective
+    # with a modular information function) at the part's quota
+    for trial in range(60):
+        d, w = 3, int(rng.integers(1, 4))
+        n = int(rng.integers(w + 1, w + 13))
+        ret = sorted(rng.choice(200, size=n, replace=False).tolist())
+        Kvis = rng.normal(size=(200, d))
+        qsum = rng.normal(size=d)
+        budget = int(rng.integers(1, n + 2))
+        u = int(rng.integers(0, 4))
+        rs = (int(rng.integers(0, 5)), 4)
+        got, _ = oracle.update(ret, Kvis, qsum, budget, False, w, rs, u)
+        w_eff = min(w, budget)
+        T = max(0, n - w_eff)
+        hist, recent = ret[:T], ret[T:]
+        M = max(0, T - (budget - w_eff))
+        n_long = T * rs[0] // rs[1]
+        m_long = (M + (u & 1)) // 2
+        m_near = M - m_long
+        if m_long > n_long:
+            m_near, m_long = m_near + m_long - n_long, n_long
+        if m_near > T - n_long:
+            m_long, m_near = m_long + m_near - (T - n_long), T - n_long
+        s = dict(zip(hist, _scores(Kvis, qsum, hist)))
+        expect = []
+        for part, m in ((hist[:n_long], m_long), (hist[n_long:], m_near)):
+            best = max(itertools.combinations(part, len(part) - m),
+                       key=lambda c: sum(s[p] for p in c))
+            expect += list(best)
+        assert list(got) == sorted(expect + recent)
+        assert len(got) == min(n, budget) if n > w_eff else len(got) == n
+
+
+def test_ste_matches_literal_eq6_ranking():
+    # Eq. (6) literally: the mean over the past-P queries of q_p k_j / sqrt(d);
+    # the oracle ranks by the sum of the queries dotted with k_j
+    d, P = 16, 7
+    for trial in range(20):
+        n, w = 40, 4
+        ret = list(range(n))
+        Kvis = rng.normal(size=(n, d))
+        Q = rng.normal(size=(P, d))
+        literal = (Q @ Kvis.T / math.sqrt(d)).mean(axis=0)
+        budget = 20
+        got, _ = oracle.update(ret, Kvis, Q.sum(axis=0), budget, False, w, (1, 2), 0)
+        T = n - w
+        M = T - (budget - w)
+        half = T // 2
+        m_long, m_near = M // 2, M - M // 2
+        ev_long = np.argsort(literal[:half], kind="stable")[:m_long]
+        ev_near = half + np.argsort(literal[half:T], kind="stable")[:m_near]
+        expect = sorted(set(ret) - set(ev_long.tolist()) - set(ev_near.tolist()))
+        assert list(got) == expect
+
+
+def test_ste_global_topk_special_case():
+    # r_s = 0 or 1 turns STE into one bottom-M over the whole history
+    for rs in ((0, 1), (1, 1)):
+        for trial in range(10):
+            n, w, d = 60, 5, 8
+            Kvis = rng.normal(size=(n, d))
+            qsum = rng.normal(size=d)
+            got, _ = oracle.update(list(range(n)), Kvis, qsum, 30, False, w, rs, trial)
+            sc = _scores(Kvis, qsum, list(range(n - w)))
+            drop = set(np.argsort(sc, kind="stable")[: (n - w) - (30 - w)].tolist())
+            assert list(got) == [p for p in range(n) if p not in drop]
+
+
+# --------------------------------------------- whole generation of one head
+def _inputs(wl, layer=0, b=0, h=0):
+    return synth.head_inputs(wl, layer, b, h)
+
+
+def test_full_budget_equals_full_attention():
+    wl = W.TINY
+    q, k, v, kc, vc = _inputs(wl, h=2)
+    N = wl.num_visual
+    out, _, st = oracle.run_head(q, k, v, kc, vc, wl.group_threshold - 1, wl.period, False,
+                                 N, wl.recent_len)
+    assert st["evicted"] == 0
+    for t in (0, 5, 63, 64, 200, N - 1):
+        K = torch.cat([kc, k[: t + 1]])
+        V = torch.cat([vc, v[: t + 1]])
+        assert np.array_equal(out[t], oracle.attention(q[t], K, V))
+
+
+def test_retained_set_invariants():
+    wl = W.TINY
+    t_g, P, w, N = wl.group_threshold - 1, wl.period, wl.recent_len, wl.num_visual
+    steps = list(range(N))
+    for h, local, budget in ((0, True, 32), (2, False, 128), (3, False, 40), (1, True, 20)):
+        q, k, v, kc, vc = _inputs(wl, h=h)
+        _, snaps, st = oracle.run_head(q, k, v, kc, vc, t_g, P, local, budget, w,
+                                       want_out=False, snap_steps=steps)
+        prev = None
+        for t in steps:
+            kept = np.flatnonzero(snaps[t])
+            assert kept.max() == t                                 # newest is kept
+            if t < t_g:
+                assert len(kept) == t + 1                          # no compression yet
+            else:
+                since = (t - t_g) % P
+                assert len(kept) == min(budget, t - since + 1) + since
+                w_eff = min(w, budget)
+                assert set(range(t - w_eff + 1, t + 1)) <= set(kept)   # recent window
+                if local:                                          # sliding window
+                    assert list(kept) == list(range(t - len(kept) + 1, t + 1))
+            if prev is not None:
+                assert set(kept) <= set(prev) | {t}                # evicted never return
+            prev = kept
+        assert st["updates"] == (N - 1 - t_g) // P + 1
+
+
+def test_ste_update_parts_quota():
+    # at each update of a global head, |evicted in long part| = M_long
+    wl = W.TINY
+    q, k, v, kc, vc = _inputs(wl, h=2)
+    t_g, P, w, B = wl.group_threshold - 1, wl.period, wl.recent_len, 100
+    upd = [t for t in range(wl.num_visual) if t >= t_g and (t - t_g) % P == 0]
+    _, snaps, _ = oracle.run_head(q, k, v, kc, vc, t_g, P, False, B, w, want_out=False,
+                                  snap_steps=[u - 1 for u in upd] + upd)
+    for i, t in enumerate(upd):
+        before = set(np.flatnonzero(snaps[i]).tolist()) | {t}
+        after = set(np.flatnonzero(snaps[len(upd) + i]).tolist())
+        hist = sorted(before)[: len(before) - w]
+        T = len(hist)
+        M = max(0, T - (B - w))
+        n_long = T // 2
+        u = (t - t_g) // P
+        m_long = min((M + (u & 1)) // 2, n_long)
+        ev = set(hist) - after
+        assert len(ev) == M
+        assert len(ev & set(hist[:n_long])) == m_long + max(0, (M - m_long) - (T - n_long))
+
+
+def test_oracle_generator_is_seeded():
+    a = synth.head_inputs(W.TINY, 0, 0, 1)
+    b = synth.head_inputs(W.TINY, 0, 0, 1)
+    c = synth.head_inputs(W.TINY, 0, 0, 1, seed=7)
+    assert all(torch.equal(x, y) for x, y in zip(a, b))
+    assert not torch.equal(a[1], c[1])
+
+
+@pytest.mark.parametrize("L,tau,n", [(4, 0.75, 3), (8, 0.5, 4), (16, 0.9375, 15)])
+def test_grouping_threshold_is_reached_when_mass_equals_tau(L, tau, n):
+    # q = 0 gives weights 1/L exactly (L a power of two), so S(n) hits tau
+    # exactly; reading: the accumulation stops once the mass reaches tau
+    g = oracle.group_head(np.zeros(4), rng.normal(size=(L, 4)), tau, n + 1)
+    assert g["n_star"] == n and g["is_local"] == 1
+
+
+def test_ste_query_window_is_the_last_P_queries():
+    # Only one query is non-zero.  Inside the window [t-P+1, t] it decides the
+    # ranking; just outside (step t-P) it must not: then every score is 0 and
+    # the ties evict the oldest tokens of each part.
+    N, C, d, t_g, P, w, B = 40, 2, 4, 19, 5, 4, 10
+    k = rng.normal(size=(N, d))
+    v = rng.normal(size=(N, d))
+    kc, vc = rng.normal(size=(C, d)), rng.normal(size=(C, d))
+    oldest_first = {5, 6, 7, 13, 14, 15, 16, 17, 18, 19}
+    for step, inside in ((t_g - P, False), (t_g - P + 1, True), (t_g, True)):
+        q = np.zeros((N, d))
+        q[step] = 50.0 * rng.normal(size=d)
+        _, snaps, _ = oracle.run_head(q, k, v, kc, vc, t_g, P, False, B, w,
+                                      want_out=False, snap_steps=[t_g])
+        kept = set(np.flatnonzero(snaps[0]).tolist())
+        assert len(kept) == B
+        assert (kept == oldest_first) == (not inside), step
