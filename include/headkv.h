@@ -1,0 +1,174 @@
+/*
+ * headkv.h -- C ABI of the head-aware compressed-KV decode path for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The library keeps, per layer, a KV cache whose retained length differs per
+ * (batch row, head), and runs four operations of HeadKV (arXiv 2605.20600) on
+ * it with hand-written HIP kernels:
+ *
+ *   headkv_score_heads       head grouping (Sec. 4, Step 2)
+ *   headkv_assign_budgets    per-head budgets (Sec. 5.1, Implementation Details)
+ *                            and the one-time move into per-head segments
+ *   headkv_append_and_evict  cache append (Sec. 3, KV Cache) and the periodic
+ *                            update (Sec. 4, Step 3 and Efficient Cache Update):
+ *                            sliding window for local heads (Eq. 3), Stratified
+ *                            Token Eviction for global heads (Eqs. 4-6)
+ *   headkv_decode_attn       single-query attention, Eq. (1), over the
+ *                            conditional prefix and the retained tokens
+ *
+ * Conventions shared by every entry point:
+ *   - Status: every call returns HEADKV_OK (0) or a negative error code and
+ *     never aborts; headkv_last_error() returns a message for the calling
+ *     thread.  Arguments and the call order are validated before any HIP call.
+ *   - Memory: the caller allocates every device buffer (sizes from headkv_plan
+ *     and headkv_assign_budgets) and keeps it alive while the handle uses it.
+ *     The library calls no hipMalloc.  Device buffers must be 256-byte aligned.
+ *   - Streams: `stream` is a hipStream_t (NULL = the default stream).  Calls
+ *     are asynchronous on it, except headkv_assign_budgets, which waits for the
+ *     stream once to read the budgets back.
+ *   - Layouts: bf16 values are passed as uint16_t bit patterns.  Per-step
+ *     vectors are [batch][heads][head_dim] row-major; per-head arrays are
+ *     [batch][heads].
+ *   - Threads: a handle is not thread-safe; use one handle per stream.
+ *   - Call order per layer: headkv_prefill once, then for every visual step t
+ *     (t = 0, 1, ... consecutively): headkv_append_and_evict(t); at the
+ *     grouping step t_g = group_threshold - 1 also headkv_score_heads and
+ *     headkv_assign_budgets; then headkv_decode_attn.  Calls out of this order
+ *     return HEADKV_ERR_STATE.
+ */
+#ifndef HEADKV_H
+#define HEADKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t headkv_status;
+
+#define HEADKV_OK 0
+#define HEADKV_ERR_INVALID_ARG (-1) /* bad pointer, size, value or alignment */
+#define HEADKV_ERR_CAPACITY (-2)    /* a caller buffer is too small */
+#define HEADKV_ERR_STATE (-3)       /* call out of the documented order */
+#define HEADKV_ERR_HIP (-4)         /* a HIP runtime call or launch failed */
+#define HEADKV_ERR_UNSUPPORTED (-5) /* a shape this build does not handle */
+
+/* Budget modes (Sec. 5.1, Implementation Details: global heads keep rho*N
+ * tokens, local heads a small set of neighbouring tokens). */
+#define HEADKV_BUDGET_PAPER 0    /* local: recent_len, global: floor(rho*N) */
+#define HEADKV_BUDGET_OVERRIDE 1 /* caller budgets per head, 1..N */
+#define HEADKV_BUDGET_TOTAL 2    /* layer keeps floor(rho*N)*heads in total:
+                                    local heads recent_len, global heads an
+                                    equal share in whole rows, >= recent_len */
+
+/* Limits of this build. */
+#define HEADKV_MAX_VISUAL 16384  /* num_visual */
+#define HEADKV_MAX_PREFIX 2048   /* prefix_len */
+#define HEADKV_MAX_CAPACITY 4608 /* visual tokens one head can hold */
+
+typedef struct headkv_config {
+    int32_t batch;           /* B >= 1 */
+    int32_t num_layers;      /* >= 1 */
+    int32_t num_heads;       /* H >= 1; key/value heads = query heads */
+    int32_t head_dim;        /* d: 64 or 128 */
+    int32_t prefix_len;      /* C: conditional tokens, never evicted (Eq. 2) */
+    int32_t row_len;         /* R: tokens per image row, row-end token included */
+    int32_t num_visual;      /* N: visual tokens of one image */
+    int32_t recent_len;      /* w: recent window (Eq. 2), two rows in the paper */
+    int32_t local_window;    /* W_loc: a head is local iff n* < W_loc */
+    int32_t period;          /* P: update every P steps (Efficient Cache Update) */
+    int32_t group_threshold; /* thr in 1..N: heads are grouped when thr visual
+                                tokens are cached, i.e. at step thr - 1 */
+    int32_t budget_mode;     /* HEADKV_BUDGET_* */
+    int32_t rho_num, rho_den;/* rho = rho_num / rho_den in (0, 1] */
+    int32_t rs_num, rs_den;  /* r_s = rs_num / rs_den in [0, 1] (Eq. 5) */
+    double tau;              /* grouping mass threshold in (0, 1], 0.9 */
+} headkv_config;
+
+typedef struct headkv_ctx* headkv_t;
+
+/* Sizes of the caller-owned device buffers.
+ *   dense_kv_bytes: per layer, the cache before grouping (every head holds
+ *                   its prefix and up to group_threshold visual tokens);
+ *   meta_bytes:     per layer, lengths, positions tables, labels, budgets,
+ *                   query sums and the work list;
+ *   workspace_bytes: one buffer shared by all layers (split-K partials). */
+headkv_status headkv_plan(const headkv_config* cfg, size_t* dense_kv_bytes,
+                          size_t* meta_bytes, size_t* workspace_bytes);
+
+/* Creates a host handle.  dense_kv, meta: host arrays of num_layers device
+ * pointers; workspace: one device pointer.  No device work is done. */
+headkv_status headkv_create(const headkv_config* cfg, void* const* dense_kv,
+                            void* const* meta, void* workspace, headkv_t* out);
+
+void headkv_destroy(headkv_t h);
+
+/* Step 1, cache prefilling (Sec. 4): stores the conditional keys and values
+ * k_c, v_c ([B][H][C][d] bf16, device; NULL allowed when C = 0) as the first
+ * C cache entries of every head of `layer`, and resets the layer's state. */
+headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c,
+                             const uint16_t* v_c, void* stream);
+
+/* Cache append K <- [K, k_t], V <- [V, v_t] (Sec. 3, KV Cache) for visual
+ * step `step` of `layer`; q, k, v: [B][H][d] bf16, device.  q_t is added to
+ * the head's sum of the past-P queries (Eq. 6).  When the layer is grouped and
+ * (step - t_g) is a positive multiple of P, the periodic update follows
+ * (Eqs. 2-6): each local head keeps its newest `budget` visual tokens; each
+ * global head keeps its recent window and evicts from its history the
+ * lowest-scored tokens of the long-range and near-range parts, M/2 each.
+ * Steps must be consecutive from 0.  A step past t_g before grouping is
+ * HEADKV_ERR_STATE. */
+headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step,
+                                      const uint16_t* q, const uint16_t* k,
+                                      const uint16_t* v, void* stream);
+
+/* Head grouping (Sec. 4, Step 2), at step t_g after its append: for each
+ * (b, h) the current query q ([B][H][d] bf16, device) attends over the whole
+ * key cache (prefix and visual tokens 0..t_g) in fp64; the attention mass is
+ * accumulated backward from the newest token; n* is the smallest count whose
+ * mass reaches tau, and the head is local iff n* < local_window.
+ * Writes n_star ([B][H] int32, device) and is_local ([B][H] uint8, device,
+ * 1 = local). */
+headkv_status headkv_score_heads(headkv_t h, int32_t layer, const uint16_t* q,
+                                 int32_t* n_star, uint8_t* is_local, void* stream);
+
+/* Budgets (Sec. 5.1) and the move into per-head segments, at step t_g after
+ * score_heads.  is_local: [B][H] uint8 labels (device; usually the array
+ * score_heads wrote; all zero gives the uniform-budget LineAR layout).
+ * budget_override: [B][H] int32 (device) for HEADKV_BUDGET_OVERRIDE, else
+ * NULL.  budgets: [B][H] int32 output (device), visual tokens per head, the
+ * recent window included and the prefix not counted.
+ * Each head then needs prefix_len + min(budget + period, N) slots; the total,
+ * with alignment, is written to *ragged_bytes_needed.  If ragged_kv is NULL
+ * or ragged_bytes is smaller, the call returns HEADKV_ERR_CAPACITY after
+ * setting *ragged_bytes_needed and changes no state: allocate and call again.
+ * Otherwise the first update runs (Eqs. 2-6), the retained tokens are copied
+ * into ragged_kv (device, caller-owned from now on), and the dense buffer of
+ * this layer is no longer used.  Waits for `stream` once. */
+headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is_local,
+                                    const int32_t* budget_override, int32_t* budgets,
+                                    void* ragged_kv, size_t ragged_bytes,
+                                    size_t* ragged_bytes_needed, void* stream);
+
+/* Decode attention, Eq. (1), of the current step for every (b, h) of
+ * `layer`: o = softmax(q K^T / sqrt(d)) V over the prefix and the head's
+ * retained visual tokens (the current token included).  q: [B][H][d] bf16,
+ * out: [B][H][d] fp32, both device.  bf16 storage, fp32 accumulation. */
+headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q,
+                                 float* out, void* stream);
+
+/* Parity export: mask[b][h][p] = 1 iff visual position p is retained
+ * ([B][H][N] uint8, device) and count[b][h] = number retained ([B][H] int32,
+ * device). */
+headkv_status headkv_export_retained(headkv_t h, int32_t layer, uint8_t* mask,
+                                     int32_t* count, void* stream);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* headkv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -178,3 +178,27 @@ def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
         res["snaps"][h] = snaps
         res["stats"][h] = st
     return res
+
+
+def group_layer(wl, layer: int, seed: Optional[int] = None) -> Dict[str, np.ndarray]:
+    """Grouping and budgets for every (b, h) of one layer: arrays [B][H]."""
+    from paper_2605_20600_amd import synth
+    kw = {} if seed is None else {"seed": seed}
+    t_g = wl.group_threshold - 1
+    q, k, _ = synth.visual_qkv(wl, layer, 0, t_g + 1, "cpu", **kw)       # [T][B][H][d]
+    kc, _ = synth.prefix_kv(wl, layer, "cpu", **kw)                     # [B][H][C][d]
+    B, H = wl.batch, wl.heads
+    out = {k_: np.zeros((B, H), dt) for k_, dt in (("labels", np.int32), ("n_star", np.int32),
+                                                   ("margin", np.float64),
+                                                   ("mass_window", np.float64),
+                                                   ("budgets", np.int32))}
+    ov = synth.budget_override(wl)
+    for b in range(B):
+        for h in range(H):
+            K = torch.cat([kc[b, h], k[:, b, h]], dim=0)
+            g = group_head(q[t_g, b, h], K, wl.tau, wl.local_window)
+            out["labels"][b, h], out["n_star"][b, h] = g["is_local"], g["n_star"]
+            out["margin"][b, h], out["mass_window"][b, h] = g["margin"], g["mass_window"]
+        out["budgets"][b] = budgets(wl.budget_mode, out["labels"][b], wl.num_visual, wl.row_len,
+                                    wl.recent_len, wl.rho, None if ov is None else ov[layer, b])
+    return out

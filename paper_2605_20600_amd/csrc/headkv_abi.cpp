@@ -1,0 +1,389 @@
+// Host runtime and C ABI of the head-aware compressed-KV decode path.
+//
+// The handle mirrors, per layer, what the device state must be (step, phase,
+// every head's length, budget and capacity) so that every call is validated
+// before anything is launched, grids are sized without reading the device
+// back, and the only device-to-host wait is the one in assign_budgets, where
+// the budgets decide the layout of the per-head segments.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/headkv.h"
+#include "layout.h"
+
+using namespace headkv;
+
+namespace {
+
+thread_local std::string g_err;
+
+headkv_status fail(headkv_status code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+headkv_status ok() { return HEADKV_OK; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
+
+struct Layer {
+    void* dense = nullptr;
+    void* meta = nullptr;
+    void* ragged = nullptr;
+    bool prefilled = false;
+    bool grouped = false;
+    int last_step = -1;
+    int n_items = 0;               // decode work items after grouping
+    std::vector<int> n, budget, cap;
+};
+
+}  // namespace
+
+struct headkv_ctx {
+    headkv_config cfg;
+    Shape shape;
+    MetaLayout ml;
+    int t_g = 0;
+    int dense_cap = 0;             // visual slots per head before grouping
+    int dense_cph = 0;             // decode chunks per head before grouping
+    int64_t dense_seg = 0;         // bytes per head segment before grouping
+    int max_chunks = 0;            // decode chunks of the largest possible head
+    size_t ws_bytes = 0;
+    void* ws = nullptr;
+    std::vector<Layer> layers;
+};
+
+namespace {
+
+headkv_status validate_config(const headkv_config* c) {
+    if (!c) return fail(HEADKV_ERR_INVALID_ARG, "config is NULL");
+    if (c->batch < 1 || c->num_layers < 1 || c->num_heads < 1)
+        return fail(HEADKV_ERR_INVALID_ARG, "batch, num_layers and num_heads must be >= 1");
+    if (c->num_heads > 1024) return fail(HEADKV_ERR_UNSUPPORTED, "num_heads > 1024");
+    if ((long long)c->batch * c->num_heads > (1 << 24))
+        return fail(HEADKV_ERR_UNSUPPORTED, "batch * num_heads > 2^24");
+    if (c->head_dim != 64 && c->head_dim != 128)
+        return fail(HEADKV_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+    if (c->prefix_len < 0 || c->prefix_len > HEADKV_MAX_PREFIX)
+        return fail(HEADKV_ERR_INVALID_ARG, "prefix_len out of [0, HEADKV_MAX_PREFIX]");
+    if (c->num_visual < 1 || c->num_visual > HEADKV_MAX_VISUAL)
+        return fail(HEADKV_ERR_INVALID_ARG, "num_visual out of [1, HEADKV_MAX_VISUAL]");
+    if (c->row_len < 1 || c->row_len > c->num_visual)
+        return fail(HEADKV_ERR_INVALID_ARG, "row_len out of [1, num_visual]");
+    if (c->recent_len < 1 || c->local_window < 1 || c->period < 1)
+        return fail(HEADKV_ERR_INVALID_ARG, "recent_len, local_window and period must be >= 1");
+    if (c->group_threshold < 1 || c->group_threshold > c->num_visual)
+        return fail(HEADKV_ERR_INVALID_ARG, "group_threshold out of [1, num_visual]");
+    if (c->group_threshold > HEADKV_MAX_CAPACITY)
+        return fail(HEADKV_ERR_UNSUPPORTED, "group_threshold > HEADKV_MAX_CAPACITY");
+    if (c->budget_mode < HEADKV_BUDGET_PAPER || c->budget_mode > HEADKV_BUDGET_TOTAL)
+        return fail(HEADKV_ERR_INVALID_ARG, "unknown budget_mode");
+    if (c->rho_num < 1 || c->rho_den < 1 || c->rho_num > c->rho_den)
+        return fail(HEADKV_ERR_INVALID_ARG, "rho must be in (0, 1]");
+    if (c->rs_num < 0 || c->rs_den < 1 || c->rs_num > c->rs_den)
+        return fail(HEADKV_ERR_INVALID_ARG, "r_s must be in [0, 1]");
+    if (!(c->tau > 0.0 && c->tau <= 1.0)) return fail(HEADKV_ERR_INVALID_ARG, "tau must be in (0, 1]");
+    return ok();
+}
+
+struct Plan {
+    int BH, dense_cap, dense_cph, max_chunks, max_items;
+    int64_t dense_seg;
+    size_t dense_bytes, ws_bytes;
+    MetaLayout ml;
+};
+
+Plan make_plan(const headkv_config& c) {
+    Plan p;
+    p.BH = c.batch * c.num_heads;
+    p.dense_cap = c.group_threshold;
+    p.dense_seg = (int64_t)segment_bytes(c.prefix_len, p.dense_cap, c.head_dim);
+    p.dense_bytes = (size_t)p.dense_seg * p.BH;
+    p.dense_cph = ceil_div(c.prefix_len + p.dense_cap, kChunk);
+    const int cap_max = std::min(c.num_visual, HEADKV_MAX_CAPACITY);
+    p.max_chunks = ceil_div(c.prefix_len + cap_max, kChunk);
+    // ragged work list: every head's chunks, padded to equal XCD bins
+    p.max_items = p.BH * std::max(p.max_chunks, p.dense_cph) + kXcds * (p.max_chunks + 1);
+    p.ml.compute(p.BH, c.head_dim, p.max_items);
+    const size_t partials = (size_t)p.BH * std::max(p.max_chunks, p.dense_cph);
+    p.ws_bytes = align_up(partials * (c.head_dim + 2) * sizeof(float), 256);
+    return p;
+}
+
+headkv_status check_layer(headkv_t h, int32_t layer) {
+    if (!h) return fail(HEADKV_ERR_INVALID_ARG, "handle is NULL");
+    if (layer < 0 || layer >= h->cfg.num_layers) return fail(HEADKV_ERR_INVALID_ARG, "layer out of range");
+    return ok();
+}
+
+headkv_status hip_status(int e, const char* what) {
+    if (e != 0) return fail(HEADKV_ERR_HIP, std::string(what) + ": " + hipGetErrorString((hipError_t)e));
+    return ok();
+}
+
+LayerDev dev_of(headkv_t h, const Layer& L) {
+    return make_layer_dev(L.grouped ? L.ragged : L.dense, L.meta, h->ml);
+}
+
+}  // namespace
+
+extern "C" {
+
+headkv_status headkv_plan(const headkv_config* cfg, size_t* dense_kv_bytes, size_t* meta_bytes,
+                          size_t* workspace_bytes) {
+    headkv_status st = validate_config(cfg);
+    if (st) return st;
+    if (!dense_kv_bytes || !meta_bytes || !workspace_bytes)
+        return fail(HEADKV_ERR_INVALID_ARG, "output pointer is NULL");
+    Plan p = make_plan(*cfg);
+    *dense_kv_bytes = p.dense_bytes;
+    *meta_bytes = p.ml.total;
+    *workspace_bytes = p.ws_bytes;
+    return ok();
+}
+
+headkv_status headkv_create(const headkv_config* cfg, void* const* dense_kv, void* const* meta,
+                            void* workspace, headkv_t* out) {
+    headkv_status st = validate_config(cfg);
+    if (st) return st;
+    if (!dense_kv || !meta || !workspace || !out) return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer");
+    if (!aligned(workspace, 256)) return fail(HEADKV_ERR_INVALID_ARG, "workspace not 256-byte aligned");
+    for (int l = 0; l < cfg->num_layers; ++l) {
+        if (!dense_kv[l] || !meta[l]) return fail(HEADKV_ERR_INVALID_ARG, "NULL layer buffer");
+        if (!aligned(dense_kv[l], 256) || !aligned(meta[l], 256))
+            return fail(HEADKV_ERR_INVALID_ARG, "layer buffer not 256-byte aligned");
+    }
+    headkv_ctx* h = new (std::nothrow) headkv_ctx();
+    if (!h) return fail(HEADKV_ERR_INVALID_ARG, "out of host memory");
+    Plan p = make_plan(*cfg);
+    h->cfg = *cfg;
+    h->shape = Shape{p.BH, cfg->batch, cfg->num_heads, cfg->head_dim, cfg->prefix_len, cfg->num_visual};
+    h->ml = p.ml;
+    h->t_g = cfg->group_threshold - 1;
+    h->dense_cap = p.dense_cap;
+    h->dense_cph = p.dense_cph;
+    h->dense_seg = p.dense_seg;
+    h->max_chunks = p.max_chunks;
+    h->ws_bytes = p.ws_bytes;
+    h->ws = workspace;
+    h->layers.resize(cfg->num_layers);
+    for (int l = 0; l < cfg->num_layers; ++l) {
+        h->layers[l].dense = dense_kv[l];
+        h->layers[l].meta = meta[l];
+    }
+    *out = h;
+    return ok();
+}
+
+void headkv_destroy(headkv_t h) { delete h; }
+
+headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c, const uint16_t* v_c,
+                             void* stream) {
+    headkv_status st = check_layer(h, layer);
+    if (st) return st;
+    const headkv_config& c = h->cfg;
+    if (c.prefix_len > 0 && (!k_c || !v_c)) return fail(HEADKV_ERR_INVALID_ARG, "k_c / v_c is NULL");
+    if (c.prefix_len > 0 && (!aligned(k_c, 16) || !aligned(v_c, 16)))
+        return fail(HEADKV_ERR_INVALID_ARG, "k_c / v_c not 16-byte aligned");
+    Layer& L = h->layers[layer];
+    L.grouped = false;
+    L.prefilled = false;
+    L.ragged = nullptr;
+    L.last_step = -1;
+    L.n.assign(h->shape.BH, 0);
+    L.cap.assign(h->shape.BH, h->dense_cap);
+    L.budget.assign(h->shape.BH, 0);
+    st = hip_status(launch_prefill(dev_of(h, L), h->shape, k_c, v_c, h->dense_seg, h->dense_cap,
+                                   h->dense_cph, stream),
+                    "prefill launch");
+    if (st) return st;
+    L.prefilled = true;
+    return ok();
+}
+
+headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
+                                      const uint16_t* k, const uint16_t* v, void* stream) {
+    headkv_status st = check_layer(h, layer);
+    if (st) return st;
+    if (!q || !k || !v) return fail(HEADKV_ERR_INVALID_ARG, "q / k / v is NULL");
+    Layer& L = h->layers[layer];
+    const headkv_config& c = h->cfg;
+    if (!L.prefilled) return fail(HEADKV_ERR_STATE, "append before prefill");
+    if (step != L.last_step + 1) return fail(HEADKV_ERR_STATE, "steps must be consecutive from 0");
+    if (step >= c.num_visual) return fail(HEADKV_ERR_INVALID_ARG, "step >= num_visual");
+    if (!L.grouped && step > h->t_g)
+        return fail(HEADKV_ERR_STATE, "heads must be grouped at step group_threshold - 1");
+    for (int i = 0; i < h->shape.BH; ++i)
+        if (L.n[i] >= L.cap[i]) return fail(HEADKV_ERR_CAPACITY, "head capacity exhausted");
+    // window of the past-P queries that the next update scores against (Eq. 6)
+    const int P = c.period;
+    const int first = std::max(0, h->t_g - P + 1);
+    const int accumulate = step >= first ? 1 : 0;
+    const int reset = (step == first) || (step > h->t_g && (step - h->t_g - 1) % P == 0);
+    LayerDev D = dev_of(h, L);
+    st = hip_status(launch_append(D, h->shape, q, k, v, step, accumulate, reset, stream), "append launch");
+    if (st) return st;
+    for (int i = 0; i < h->shape.BH; ++i) L.n[i] += 1;
+    L.last_step = step;
+    if (L.grouped && step > h->t_g && (step - h->t_g) % P == 0) {
+        const int u = (step - h->t_g) / P;
+        st = hip_status(launch_update(D, h->shape, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
+                                      c.rs_den, u, stream),
+                        "update launch");
+        if (st) return st;
+        for (int i = 0; i < h->shape.BH; ++i) L.n[i] = std::min(L.n[i], L.budget[i]);
+    }
+    return ok();
+}
+
+headkv_status headkv_score_heads(headkv_t h, int32_t layer, const uint16_t* q, int32_t* n_star,
+                                 uint8_t* is_local, void* stream) {
+    headkv_status st = check_layer(h, layer);
+    if (st) return st;
+    if (!q || !n_star || !is_local) return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer");
+    Layer& L = h->layers[layer];
+    if (!L.prefilled || L.grouped || L.last_step != h->t_g)
+        return fail(HEADKV_ERR_STATE, "score_heads runs once, right after the append of step group_threshold - 1");
+    const headkv_config& c = h->cfg;
+    const int len = c.prefix_len + h->t_g + 1;
+    return hip_status(launch_score(dev_of(h, L), h->shape, q, n_star, is_local, len,
+                                   std::sqrt((double)c.head_dim), c.tau, c.local_window, stream),
+                      "score launch");
+}
+
+headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is_local,
+                                    const int32_t* budget_override, int32_t* budgets,
+                                    void* ragged_kv, size_t ragged_bytes,
+                                    size_t* ragged_bytes_needed, void* stream) {
+    headkv_status st = check_layer(h, layer);
+    if (st) return st;
+    if (!is_local || !budgets || !ragged_bytes_needed) return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer");
+    const headkv_config& c = h->cfg;
+    if (c.budget_mode == HEADKV_BUDGET_OVERRIDE && !budget_override)
+        return fail(HEADKV_ERR_INVALID_ARG, "budget_override is NULL in override mode");
+    if (ragged_kv && !aligned(ragged_kv, 256)) return fail(HEADKV_ERR_INVALID_ARG, "ragged_kv not 256-byte aligned");
+    Layer& L = h->layers[layer];
+    if (!L.prefilled || L.grouped || L.last_step != h->t_g)
+        return fail(HEADKV_ERR_STATE, "assign_budgets runs once, at step group_threshold - 1");
+    const int BH = h->shape.BH;
+    hipStream_t s = (hipStream_t)stream;
+    LayerDev Dold = dev_of(h, L);
+    st = hip_status(launch_budgets(Dold, h->shape, is_local, budget_override, budgets, c.budget_mode,
+                                   c.row_len, c.recent_len, c.rho_num, c.rho_den, stream),
+                    "budget launch");
+    if (st) return st;
+    std::vector<int32_t> bud(BH);
+    st = hip_status(hipMemcpyAsync(bud.data(), budgets, sizeof(int32_t) * BH, hipMemcpyDeviceToHost, s),
+                    "budget read-back");
+    if (st) return st;
+    st = hip_status(hipStreamSynchronize(s), "stream wait");
+    if (st) return st;
+    // segments: prefix + min(budget + P, N) slots each, in head order
+    std::vector<int64_t> off(BH);
+    std::vector<int32_t> cap(BH), base(BH);
+    size_t total = 0;
+    int chunks_total = 0;
+    for (int i = 0; i < BH; ++i) {
+        if (bud[i] < 1 || bud[i] > c.num_visual)
+            return fail(HEADKV_ERR_INVALID_ARG, "a budget is outside [1, num_visual]");
+        cap[i] = std::min(bud[i] + c.period, c.num_visual);
+        if (cap[i] > HEADKV_MAX_CAPACITY)
+            return fail(HEADKV_ERR_UNSUPPORTED, "budget + period exceeds HEADKV_MAX_CAPACITY");
+        off[i] = (int64_t)total;
+        total += segment_bytes(c.prefix_len, cap[i], c.head_dim);
+        base[i] = chunks_total;
+        chunks_total += ceil_div(c.prefix_len + cap[i], kChunk);
+    }
+    *ragged_bytes_needed = total;
+    if (!ragged_kv || ragged_bytes < total)
+        return fail(HEADKV_ERR_CAPACITY, "ragged_kv is NULL or smaller than *ragged_bytes_needed");
+    // decode work list: heads spread over the XCD bins by chunk count (largest
+    // first onto the lightest bin); block i runs on XCD i % 8, so all chunks of
+    // a head meet in one L2 for the merge
+    std::vector<int> order(BH);
+    for (int i = 0; i < BH; ++i) order[i] = i;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cap[a] > cap[b]; });
+    std::vector<std::vector<int32_t>> bins(kXcds);
+    std::vector<long long> load(kXcds, 0);
+    for (int i : order) {
+        const int nc = ceil_div(c.prefix_len + cap[i], kChunk);
+        const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
+        for (int ch = 0; ch < nc; ++ch) {
+            bins[x].push_back(i);
+            bins[x].push_back(ch);
+        }
+        load[x] += nc;
+    }
+    size_t longest = 0;
+    for (auto& b : bins) longest = std::max(longest, b.size() / 2);
+    const int n_items = (int)longest * kXcds;
+    if (n_items > h->ml.max_items) return fail(HEADKV_ERR_UNSUPPORTED, "work list exceeds its planned size");
+    std::vector<int32_t> work((size_t)n_items * 2, -1);
+    for (int x = 0; x < kXcds; ++x)
+        for (size_t k = 0; k < bins[x].size() / 2; ++k) {
+            work[2 * (k * kXcds + x)] = bins[x][2 * k];
+            work[2 * (k * kXcds + x) + 1] = bins[x][2 * k + 1];
+        }
+    // tables of the new layout (the host vectors outlive the copies: the stream
+    // is waited for below on every path)
+    char* mb = static_cast<char*>(L.meta);
+    st = hip_status(hipMemcpyAsync(mb + h->ml.seg_off, off.data(), sizeof(int64_t) * BH, hipMemcpyHostToDevice, s), "table upload");
+    if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.cap, cap.data(), sizeof(int32_t) * BH, hipMemcpyHostToDevice, s), "table upload");
+    if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.chunk_base, base.data(), sizeof(int32_t) * BH, hipMemcpyHostToDevice, s), "table upload");
+    if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.work, work.data(), sizeof(int32_t) * work.size(), hipMemcpyHostToDevice, s), "table upload");
+    // first update, fused with the move from the dense buffer into the segments
+    if (!st) {
+        LayerDev Dnew = make_layer_dev(ragged_kv, L.meta, h->ml);
+        st = hip_status(launch_update(Dnew, h->shape, static_cast<const char*>(L.dense), 1, h->dense_seg,
+                                      h->dense_cap, c.recent_len, c.rs_num, c.rs_den, 0, stream),
+                        "relayout launch");
+    }
+    headkv_status st_wait = hip_status(hipStreamSynchronize(s), "stream wait");
+    if (st) return st;
+    if (st_wait) return st_wait;
+    L.ragged = ragged_kv;
+    L.grouped = true;
+    L.n_items = n_items;
+    L.budget.assign(bud.begin(), bud.end());
+    L.cap.assign(cap.begin(), cap.end());
+    for (int i = 0; i < BH; ++i) L.n[i] = std::min(L.n[i], L.budget[i]);
+    return ok();
+}
+
+headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, float* out,
+                                 void* stream) {
+    headkv_status st = check_layer(h, layer);
+    if (st) return st;
+    if (!q || !out) return fail(HEADKV_ERR_INVALID_ARG, "q / out is NULL");
+    Layer& L = h->layers[layer];
+    if (!L.prefilled || L.last_step < 0) return fail(HEADKV_ERR_STATE, "decode_attn before the first append");
+    if (!L.grouped && L.last_step == h->t_g)
+        return fail(HEADKV_ERR_STATE, "assign_budgets must run before attention at step group_threshold - 1");
+    const int uniform = L.grouped ? 0 : ceil_div(h->cfg.prefix_len + L.last_step + 1, kChunk);
+    return hip_status(launch_decode(dev_of(h, L), h->shape, q, out, static_cast<float*>(h->ws), uniform,
+                                    L.n_items, stream),
+                      "decode launch");
+}
+
+headkv_status headkv_export_retained(headkv_t h, int32_t layer, uint8_t* mask, int32_t* count,
+                                     void* stream) {
+    headkv_status st = check_layer(h, layer);
+    if (st) return st;
+    if (!mask || !count) return fail(HEADKV_ERR_INVALID_ARG, "mask / count is NULL");
+    Layer& L = h->layers[layer];
+    if (!L.prefilled) return fail(HEADKV_ERR_STATE, "export before prefill");
+    return hip_status(launch_export(dev_of(h, L), h->shape, mask, count, stream), "export launch");
+}
+
+const char* headkv_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

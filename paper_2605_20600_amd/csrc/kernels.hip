@@ -1,0 +1,656 @@
+// HIP kernels of the head-aware compressed-KV decode path, written for gfx950
+// (CDNA4: 64-lane wavefronts, 160 KB LDS per CU, 8 XCDs).
+//
+//   k_prefill  Step 1 cache prefilling (Sec. 4): conditional keys/values into
+//              rows 0..C-1 of every head, layer state reset.
+//   k_append   cache append (Sec. 3, KV Cache) + running sum of the queries of
+//              the current update window (Eq. 6 is linear in the queries).
+//   k_score    head grouping (Sec. 4, Step 2), fp64.
+//   k_budgets  per-head budgets (Sec. 5.1, Implementation Details).
+//   k_update   periodic update (Eqs. 2-6): sliding window (Eq. 3) or
+//              Stratified Token Eviction (Eqs. 4-6), fused with the
+//              compaction of the head's slots or, at the grouping step, with
+//              the move into the head's own segment.
+//   k_decode   decode attention, Eq. (1), split over 64-token chunks with an
+//              online softmax per chunk and a last-block merge per head.
+//   k_export   retained-position masks for parity checks.
+//
+// Everything that decides an index (grouping mass, eviction scores) is
+// computed in fp64 with one fixed summation order and no fused multiply-add,
+// so the decisions do not depend on thread scheduling.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/headkv.h"
+#include "layout.h"
+
+namespace headkv {
+namespace {
+
+template <int NW>
+struct alignas(NW * 4) Words {
+    uint32_t w[NW];
+};
+
+__device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+__device__ __forceinline__ double bf_f64(uint16_t b) {
+    return (double)__uint_as_float((uint32_t)b << 16);
+}
+
+// Sum over the 16 lanes of a DPP row: quad swaps, then half-row and row
+// mirrors; every lane of the row ends with the full sum.
+__device__ __forceinline__ float row16_sum(float v) {
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
+    return v;
+}
+
+// Exclusive prefix sum over a 256-thread block; *total receives the sum.
+// Every thread of the block must call it.
+__device__ int block_exclusive_scan(int x, int* total) {
+    __shared__ int wsum[kBlock / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int inc = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(inc, o);
+        if (lane >= o) inc += y;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int off = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kBlock / 64; ++w) {
+        off += w < wave ? wsum[w] : 0;
+        tot += wsum[w];
+    }
+    __syncthreads();
+    *total = tot;
+    return off + inc - x;
+}
+
+struct SegPtrs {
+    uint16_t* K;
+    uint16_t* V;
+    int32_t* pos;
+};
+
+__device__ __forceinline__ SegPtrs seg_ptrs(char* seg, int C, int cap, int d) {
+    SegPtrs p;
+    p.K = reinterpret_cast<uint16_t*>(seg);
+    p.V = p.K + (size_t)(C + cap) * d;
+    p.pos = reinterpret_cast<int32_t*>(p.V + (size_t)(C + cap) * d);
+    return p;
+}
+
+// ------------------------------------------------------------------ prefill
+__global__ __launch_bounds__(kBlock) void k_prefill(LayerDev L, int C, int d, const uint16_t* kc,
+                                                    const uint16_t* vc, int64_t seg_bytes,
+                                                    int dense_cap, int cph) {
+    const int h = blockIdx.x, tid = threadIdx.x;
+    if (tid == 0) {
+        L.seg_off[h] = (int64_t)h * seg_bytes;
+        L.cap[h] = dense_cap;
+        L.n[h] = 0;
+        L.budget[h] = 0;
+        L.nstar[h] = 0;
+        L.label[h] = 0;
+        L.counter[h] = 0;
+        L.chunk_base[h] = h * cph;
+    }
+    for (int i = tid; i < d; i += kBlock) L.qsum[(size_t)h * d + i] = 0.0;
+    if (C == 0) return;
+    SegPtrs s = seg_ptrs(L.kv + (int64_t)h * seg_bytes, C, dense_cap, d);
+    const int n16 = C * d / 8;
+    const uint4* ks = reinterpret_cast<const uint4*>(kc + (size_t)h * C * d);
+    const uint4* vs = reinterpret_cast<const uint4*>(vc + (size_t)h * C * d);
+    uint4* kd = reinterpret_cast<uint4*>(s.K);
+    uint4* vd = reinterpret_cast<uint4*>(s.V);
+    for (int i = tid; i < n16; i += kBlock) {
+        kd[i] = ks[i];
+        vd[i] = vs[i];
+    }
+}
+
+// ------------------------------------------------------------------- append
+__global__ void k_append(LayerDev L, int C, int d, const uint16_t* q, const uint16_t* k,
+                         const uint16_t* v, int step, int accumulate, int reset) {
+#pragma clang fp contract(off)
+    const int h = blockIdx.x, i = threadIdx.x;
+    const int n = L.n[h];
+    SegPtrs s = seg_ptrs(L.kv + L.seg_off[h], C, L.cap[h], d);
+    const size_t row = (size_t)(C + n) * d;
+    s.K[row + i] = k[(size_t)h * d + i];
+    s.V[row + i] = v[(size_t)h * d + i];
+    if (accumulate) {
+        double* qs = L.qsum + (size_t)h * d + i;
+        *qs = (reset ? 0.0 : *qs) + bf_f64(q[(size_t)h * d + i]);
+    }
+    __syncthreads();
+    if (i == 0) {
+        s.pos[n] = step;
+        L.n[h] = n + 1;
+    }
+}
+
+// ------------------------------------------------------------ head grouping
+__global__ __launch_bounds__(kBlock) void k_score(LayerDev L, int d, const uint16_t* q,
+                                                  int32_t* n_star, uint8_t* is_local, int len,
+                                                  double sqrt_d, double tau, int local_window) {
+#pragma clang fp contract(off)
+    extern __shared__ double a[];  // [len]
+    __shared__ double qd[128];
+    __shared__ double red[kBlock / 64];
+    __shared__ double zsh;
+    const int h = blockIdx.x, tid = threadIdx.x;
+    for (int i = tid; i < d; i += kBlock) qd[i] = bf_f64(q[(size_t)h * d + i]);
+    __syncthreads();
+    const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + L.seg_off[h]);
+    // logits q.k_j / sqrt(d), dims summed in order
+    double m = -INFINITY;
+    for (int j = tid; j < len; j += kBlock) {
+        const uint16_t* kr = K + (size_t)j * d;
+        double acc = 0.0;
+        for (int i = 0; i < d; i += 8) {
+            const Words<4> u = *reinterpret_cast<const Words<4>*>(kr + i);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                acc = acc + qd[i + 2 * e] * (double)bf_lo(u.w[e]);
+                acc = acc + qd[i + 2 * e + 1] * (double)bf_hi(u.w[e]);
+            }
+        }
+        a[j] = acc / sqrt_d;
+        m = fmax(m, a[j]);
+    }
+    for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+    if ((tid & 63) == 0) red[tid >> 6] = m;
+    __syncthreads();
+    m = fmax(fmax(red[0], red[1]), fmax(red[2], red[3]));
+    for (int j = tid; j < len; j += kBlock) a[j] = exp(a[j] - m);
+    __syncthreads();
+    if (tid == 0) {  // normaliser, summed over the cache in order
+        double z = 0.0;
+        for (int j = 0; j < len; ++j) z += a[j];
+        zsh = z;
+    }
+    __syncthreads();
+    const double z = zsh;
+    for (int j = tid; j < len; j += kBlock) a[j] = a[j] / z;
+    __syncthreads();
+    if (tid == 0) {  // mass accumulated backward from the newest token
+        double S = 0.0;
+        int ns = len;
+        for (int nn = 1; nn <= len; ++nn) {
+            S += a[len - nn];
+            if (S >= tau) {
+                ns = nn;
+                break;
+            }
+        }
+        const int loc = ns < local_window ? 1 : 0;
+        n_star[h] = ns;
+        is_local[h] = (uint8_t)loc;
+        L.nstar[h] = ns;
+        L.label[h] = loc;
+    }
+}
+
+// ------------------------------------------------------------------ budgets
+__global__ void k_budgets(LayerDev L, int H, int N, const uint8_t* is_local,
+                          const int32_t* override_b, int32_t* budgets, int mode, int row_len,
+                          int recent_len, int rho_num, int rho_den) {
+    __shared__ int n_local;
+    const int b = blockIdx.x, h = threadIdx.x, idx = b * H + h;
+    if (h == 0) n_local = 0;
+    __syncthreads();
+    const int loc = is_local[idx] ? 1 : 0;
+    if (loc) atomicAdd(&n_local, 1);
+    __syncthreads();
+    const long long rhoN = (long long)N * rho_num / rho_den;
+    const int b_local = recent_len < N ? recent_len : N;
+    int B;
+    if (mode == HEADKV_BUDGET_OVERRIDE) {
+        B = override_b[idx];
+    } else if (mode == HEADKV_BUDGET_PAPER) {
+        B = loc ? b_local : (int)(rhoN < 1 ? 1 : rhoN);
+    } else {
+        const int n_global = H - n_local;
+        const long long rest = rhoN * H - (long long)n_local * b_local;
+        const long long per = (n_global > 0 && rest > 0) ? rest / n_global : 0;
+        long long bg = per / row_len * row_len;
+        if (bg < b_local) bg = b_local;
+        if (bg > N) bg = N;
+        B = loc ? b_local : (int)bg;
+    }
+    budgets[idx] = B;
+    L.budget[idx] = B;
+    L.label[idx] = loc;
+}
+
+// ------------------------------------------------------------------- update
+template <int D>
+__global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, const char* src_kv,
+                                                   int relayout, int64_t dense_seg_bytes,
+                                                   int dense_cap, int recent_len, int rs_num,
+                                                   int rs_den, int u) {
+#pragma clang fp contract(off)
+    constexpr int kMaxCap = HEADKV_MAX_CAPACITY;
+    constexpr int kWords = HEADKV_MAX_VISUAL / 32;
+    constexpr int kRow16 = D / 8;  // 16-byte pieces per K or V row
+    __shared__ uint32_t bm[kWords];
+    __shared__ int32_t wpre[kWords];
+    __shared__ uint16_t order[kMaxCap];  // slot of rank r (ranks by position)
+    __shared__ uint8_t evict[kMaxCap];   // by slot
+    __shared__ double sig[kMaxCap];      // score by rank; reused as int lists
+    __shared__ double qs[D];
+    const int h = blockIdx.x, tid = threadIdx.x;
+    const int n = L.n[h];
+    const int B = L.budget[h];
+    const int local = L.label[h];
+    // Eq. (2): history = retained tokens older than the recent window
+    const int w_eff = recent_len < B ? recent_len : B;
+    const int T = n > w_eff ? n - w_eff : 0;
+    const int keep = B - w_eff;
+    const int M = T > keep ? T - keep : 0;
+    if (!relayout && M == 0) return;
+
+    const int src_cap = relayout ? dense_cap : L.cap[h];
+    char* src_seg = relayout ? const_cast<char*>(src_kv) + (int64_t)h * dense_seg_bytes
+                             : L.kv + L.seg_off[h];
+    SegPtrs S = seg_ptrs(src_seg, C, src_cap, D);
+
+    // rank every occupied slot by its position: bitmap + prefix popcount
+    const int nw = (N + 31) >> 5;
+    for (int i = tid; i < nw; i += kBlock) bm[i] = 0u;
+    for (int i = tid; i < n; i += kBlock) evict[i] = 0;
+    __syncthreads();
+    for (int s = tid; s < n; s += kBlock) {
+        const int p = S.pos[s];
+        atomicOr(&bm[p >> 5], 1u << (p & 31));
+    }
+    __syncthreads();
+    {
+        const int w0 = 2 * tid;
+        const int c0 = w0 < nw ? __popc(bm[w0]) : 0;
+        const int c1 = w0 + 1 < nw ? __popc(bm[w0 + 1]) : 0;
+        int tot;
+        const int ex = block_exclusive_scan(c0 + c1, &tot);
+        if (w0 < nw) wpre[w0] = ex;
+        if (w0 + 1 < nw) wpre[w0 + 1] = ex + c0;
+    }
+    __syncthreads();
+    for (int s = tid; s < n; s += kBlock) {
+        const int p = S.pos[s];
+        const int r = wpre[p >> 5] + __popc(bm[p >> 5] & ((1u << (p & 31)) - 1u));
+        order[r] = (uint16_t)s;
+    }
+    __syncthreads();
+
+    if (M > 0) {
+        if (local) {
+            // Eq. (3): sliding window, the M oldest leave
+            for (int r = tid; r < M; r += kBlock) evict[order[r]] = 1;
+        } else {
+            // Eq. (5): long-range part = the oldest floor(T r_s) history tokens
+            const int n_long = (int)((long long)T * rs_num / rs_den);
+            const int n_near = T - n_long;
+            int m_long = (M + (u & 1)) >> 1;
+            int m_near = M - m_long;
+            if (m_long > n_long) {
+                m_near += m_long - n_long;
+                m_long = n_long;
+            }
+            if (m_near > n_near) {
+                m_long += m_near - n_near;
+                m_near = n_near;
+            }
+            // Eq. (6): mean raw logit of the past-P queries; the positive factor
+            // 1/(P sqrt(d)) is dropped, the order is that of (sum q) . k
+            for (int i = tid; i < D; i += kBlock) qs[i] = L.qsum[(size_t)h * D + i];
+            __syncthreads();
+            for (int r = tid; r < T; r += kBlock) {
+                const uint16_t* kr = S.K + (size_t)(C + order[r]) * D;
+                double acc = 0.0;
+                for (int i = 0; i < D; i += 8) {
+                    const Words<4> w4 = *reinterpret_cast<const Words<4>*>(kr + i);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        acc = acc + qs[i + 2 * e] * (double)bf_lo(w4.w[e]);
+                        acc = acc + qs[i + 2 * e + 1] * (double)bf_hi(w4.w[e]);
+                    }
+                }
+                sig[r] = acc;
+            }
+            __syncthreads();
+            // per part, evict the m lowest by (score, position)
+            for (int r = tid; r < T; r += kBlock) {
+                const bool lp = r < n_long;
+                const int lo = lp ? 0 : n_long, hi = lp ? n_long : T;
+                const int mq = lp ? m_long : m_near;
+                if (mq == 0) continue;
+                bool ev = true;
+                if (mq < hi - lo) {
+                    const double sr = sig[r];
+                    int cnt = 0;
+                    for (int r2 = lo; r2 < hi && cnt < mq; ++r2) {
+                        const double s2 = sig[r2];
+                        cnt += (s2 < sr) || (s2 == sr && r2 < r);
+                    }
+                    ev = cnt < mq;
+                }
+                if (ev) evict[order[r]] = 1;
+            }
+        }
+    }
+    __syncthreads();
+    const int n_new = n - M;
+    int32_t* list_a = reinterpret_cast<int32_t*>(sig);
+    int32_t* list_b = list_a + kMaxCap;
+
+    if (relayout) {
+        // prefix rows, then kept slots in position order, into the new segment
+        SegPtrs Dd = seg_ptrs(L.kv + L.seg_off[h], C, L.cap[h], D);
+        const uint4* sk = reinterpret_cast<const uint4*>(S.K);
+        const uint4* sv = reinterpret_cast<const uint4*>(S.V);
+        uint4* dk = reinterpret_cast<uint4*>(Dd.K);
+        uint4* dv = reinterpret_cast<uint4*>(Dd.V);
+        for (int i = tid; i < C * kRow16; i += kBlock) {
+            dk[i] = sk[i];
+            dv[i] = sv[i];
+        }
+        int base = 0;
+        for (int r0 = 0; r0 < n; r0 += kBlock) {
+            const int r = r0 + tid;
+            const int kf = (r < n && !evict[order[r]]) ? 1 : 0;
+            int tot;
+            const int ex = block_exclusive_scan(kf, &tot);
+            if (kf) {
+                list_a[base + ex] = order[r];
+                Dd.pos[base + ex] = S.pos[order[r]];
+            }
+            base += tot;
+        }
+        __syncthreads();
+        for (int i = tid; i < n_new * kRow16; i += kBlock) {
+            const int j = i / kRow16, c = i - j * kRow16;
+            const size_t src = (size_t)(C + list_a[j]) * kRow16 + c;
+            const size_t dst = (size_t)(C + j) * kRow16 + c;
+            dk[dst] = sk[src];
+            dv[dst] = sv[src];
+        }
+    } else {
+        // in place: evicted slots below n_new are refilled from kept slots at or
+        // above n_new; the two sets are disjoint, so no copy reads a written row
+        int nh = 0, nf = 0;
+        for (int s0 = 0; s0 < n; s0 += kBlock) {
+            const int s = s0 + tid;
+            const int hf = (s < n_new && evict[s]) ? 1 : 0;
+            const int ff = (s >= n_new && s < n && !evict[s]) ? 1 : 0;
+            int th, tf;
+            const int eh = block_exclusive_scan(hf, &th);
+            const int ef = block_exclusive_scan(ff, &tf);
+            if (hf) list_a[nh + eh] = s;
+            if (ff) list_b[nf + ef] = s;
+            nh += th;
+            nf += tf;
+        }
+        __syncthreads();
+        uint4* k4 = reinterpret_cast<uint4*>(S.K);
+        uint4* v4 = reinterpret_cast<uint4*>(S.V);
+        for (int i = tid; i < nh * kRow16; i += kBlock) {
+            const int j = i / kRow16, c = i - j * kRow16;
+            const size_t dst = (size_t)(C + list_a[j]) * kRow16 + c;
+            const size_t src = (size_t)(C + list_b[j]) * kRow16 + c;
+            k4[dst] = k4[src];
+            v4[dst] = v4[src];
+        }
+        for (int j = tid; j < nh; j += kBlock) S.pos[list_a[j]] = S.pos[list_b[j]];
+    }
+    if (tid == 0) L.n[h] = n_new;
+}
+
+// ------------------------------------------------------------------- decode
+// One block = 4 wavefronts = one 64-token chunk of one head.  Each 16-lane
+// row of a wavefront holds one token at a time (d/16 elements per lane, one
+// 8- or 16-byte load per lane), so a K or V row is read by one coalesced row
+// of lanes; the q.k partial dot is summed over the row with DPP.
+template <int D>
+__global__ __launch_bounds__(kBlock) void k_decode(LayerDev L, int C, const uint16_t* __restrict__ q,
+                                                   float* __restrict__ out,
+                                                   float* __restrict__ part, float qscale,
+                                                   int uniform_active) {
+    constexpr int VPL = D / 16;   // bf16 elements per lane
+    constexpr int NW = VPL / 2;   // 32-bit words per lane
+    using Vec = Words<NW>;
+    int h, c;
+    if (uniform_active > 0) {
+        h = blockIdx.x / uniform_active;
+        c = blockIdx.x - h * uniform_active;
+    } else {
+        h = L.work[2 * blockIdx.x];
+        c = L.work[2 * blockIdx.x + 1];
+        if (h < 0) return;
+    }
+    const int n = L.n[h];
+    const int cap = L.cap[h];
+    const int len = C + n;
+    const int active = (len + kChunk - 1) / kChunk;
+    if (c >= active) return;
+    const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + L.seg_off[h]);
+    const uint16_t* V = K + (size_t)(C + cap) * D;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int row = lane >> 4, col = lane & 15;
+
+    float qf[VPL];
+    {
+        const Vec u = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
+#pragma unroll
+        for (int e = 0; e < NW; ++e) {
+            qf[2 * e] = bf_lo(u.w[e]) * qscale;
+            qf[2 * e + 1] = bf_hi(u.w[e]) * qscale;
+        }
+    }
+    const int t0 = c * kChunk + wave * 16 + row;
+    Vec kr[4], vr[4];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int tok = t0 + it * 4;
+        if (tok < len) {
+            kr[it] = *reinterpret_cast<const Vec*>(K + (size_t)tok * D + col * VPL);
+            vr[it] = *reinterpret_cast<const Vec*>(V + (size_t)tok * D + col * VPL);
+        } else {
+#pragma unroll
+            for (int e = 0; e < NW; ++e) kr[it].w[e] = vr[it].w[e] = 0u;
+        }
+    }
+    float s[4];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        float dp = 0.f;
+#pragma unroll
+        for (int e = 0; e < NW; ++e) {
+            dp += qf[2 * e] * bf_lo(kr[it].w[e]);
+            dp += qf[2 * e + 1] * bf_hi(kr[it].w[e]);
+        }
+        dp = row16_sum(dp);
+        s[it] = (t0 + it * 4 < len) ? dp : -INFINITY;
+    }
+    float m = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+    float l = 0.f;
+    float acc[VPL];
+#pragma unroll
+    for (int e = 0; e < VPL; ++e) acc[e] = 0.f;
+    if (m != -INFINITY) {
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+            const float p = __builtin_amdgcn_exp2f(s[it] - m);
+            l += p;
+#pragma unroll
+            for (int e = 0; e < NW; ++e) {
+                acc[2 * e] += p * bf_lo(vr[it].w[e]);
+                acc[2 * e + 1] += p * bf_hi(vr[it].w[e]);
+            }
+        }
+    }
+    // merge the four rows of the wavefront
+#pragma unroll
+    for (int off = 16; off <= 32; off <<= 1) {
+        const float mo = __shfl_xor(m, off);
+        const float lo = __shfl_xor(l, off);
+        const float mn = fmaxf(m, mo);
+        const float fa = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mn);
+        const float fb = (mo == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mo - mn);
+        l = l * fa + lo * fb;
+#pragma unroll
+        for (int e = 0; e < VPL; ++e) {
+            const float ao = __shfl_xor(acc[e], off);
+            acc[e] = acc[e] * fa + ao * fb;
+        }
+        m = mn;
+    }
+    __shared__ float sm[4], sl[4];
+    __shared__ float sacc[4][D];
+    if (row == 0) {
+#pragma unroll
+        for (int e = 0; e < VPL; ++e) sacc[wave][col * VPL + e] = acc[e];
+        if (col == 0) {
+            sm[wave] = m;
+            sl[wave] = l;
+        }
+    }
+    __syncthreads();
+    float o_acc = 0.f, o_l = 0.f, o_m = -INFINITY;
+    if (tid < D) {
+        o_m = fmaxf(fmaxf(sm[0], sm[1]), fmaxf(sm[2], sm[3]));
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const float f = (sm[w] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sm[w] - o_m);
+            o_acc += f * sacc[w][tid];
+            o_l += f * sl[w];
+        }
+    }
+    if (active == 1) {
+        if (tid < D) out[(size_t)h * D + tid] = o_acc / o_l;
+        return;
+    }
+    constexpr int PS = D + 2;
+    float* pp = part + (size_t)(L.chunk_base[h] + c) * PS;
+    if (tid < D) pp[tid] = o_acc;
+    if (tid == 0) {
+        pp[D] = o_m;
+        pp[D + 1] = o_l;
+    }
+    __threadfence();
+    __syncthreads();
+    __shared__ int s_last;
+    if (tid == 0) {
+        const unsigned prev = atomicAdd(&L.counter[h], 1u);
+        s_last = (prev == (unsigned)(active - 1)) ? 1 : 0;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    if (tid < D) {
+        const float* p0 = part + (size_t)L.chunk_base[h] * PS;
+        float mx = -INFINITY;
+        for (int i = 0; i < active; ++i) mx = fmaxf(mx, p0[(size_t)i * PS + D]);
+        float num = 0.f, den = 0.f;
+        for (int i = 0; i < active; ++i) {
+            const float mi = p0[(size_t)i * PS + D];
+            const float f = (mi == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mi - mx);
+            num += f * p0[(size_t)i * PS + tid];
+            den += f * p0[(size_t)i * PS + D + 1];
+        }
+        out[(size_t)h * D + tid] = num / den;
+    }
+    if (tid == 0) L.counter[h] = 0u;
+}
+
+// ------------------------------------------------------------------- export
+__global__ __launch_bounds__(kBlock) void k_export(LayerDev L, int C, int d, int N, uint8_t* mask,
+                                                   int32_t* count) {
+    const int h = blockIdx.x, tid = threadIdx.x;
+    const int n = L.n[h];
+    SegPtrs s = seg_ptrs(L.kv + L.seg_off[h], C, L.cap[h], d);
+    for (int p = tid; p < N; p += kBlock) mask[(size_t)h * N + p] = 0;
+    __syncthreads();
+    for (int j = tid; j < n; j += kBlock) mask[(size_t)h * N + s.pos[j]] = 1;
+    if (tid == 0) count[h] = n;
+}
+
+inline int last_error() { return (int)hipGetLastError(); }
+
+}  // namespace
+
+int launch_prefill(const LayerDev& L, const Shape& s, const uint16_t* kc, const uint16_t* vc,
+                   int64_t dense_seg_bytes, int dense_cap, int dense_cph, void* stream) {
+    hipLaunchKernelGGL(k_prefill, dim3(s.BH), dim3(kBlock), 0, (hipStream_t)stream, L, s.C, s.d,
+                       kc, vc, dense_seg_bytes, dense_cap, dense_cph);
+    return last_error();
+}
+
+int launch_append(const LayerDev& L, const Shape& s, const uint16_t* q, const uint16_t* k,
+                  const uint16_t* v, int step, int accumulate, int reset, void* stream) {
+    hipLaunchKernelGGL(k_append, dim3(s.BH), dim3(s.d), 0, (hipStream_t)stream, L, s.C, s.d, q, k,
+                       v, step, accumulate, reset);
+    return last_error();
+}
+
+int launch_score(const LayerDev& L, const Shape& s, const uint16_t* q, int32_t* n_star,
+                 uint8_t* is_local, int len, double sqrt_d, double tau, int local_window,
+                 void* stream) {
+    hipLaunchKernelGGL(k_score, dim3(s.BH), dim3(kBlock), sizeof(double) * (size_t)len,
+                       (hipStream_t)stream, L, s.d, q, n_star, is_local, len, sqrt_d, tau,
+                       local_window);
+    return last_error();
+}
+
+int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
+                   const int32_t* override_b, int32_t* budgets, int mode, int row_len,
+                   int recent_len, int rho_num, int rho_den, void* stream) {
+    hipLaunchKernelGGL(k_budgets, dim3(s.B), dim3(s.H), 0, (hipStream_t)stream, L, s.H, s.N,
+                       is_local, override_b, budgets, mode, row_len, recent_len, rho_num, rho_den);
+    return last_error();
+}
+
+int launch_update(const LayerDev& L, const Shape& s, const char* src_kv, int relayout,
+                  int64_t dense_seg_bytes, int dense_cap, int recent_len, int rs_num,
+                  int rs_den, int u, void* stream) {
+    if (s.d == 128)
+        hipLaunchKernelGGL(k_update<128>, dim3(s.BH), dim3(kBlock), 0, (hipStream_t)stream, L,
+                           s.C, s.N, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
+                           rs_num, rs_den, u);
+    else
+        hipLaunchKernelGGL(k_update<64>, dim3(s.BH), dim3(kBlock), 0, (hipStream_t)stream, L,
+                           s.C, s.N, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
+                           rs_num, rs_den, u);
+    return last_error();
+}
+
+int launch_decode(const LayerDev& L, const Shape& s, const uint16_t* q, float* out,
+                  float* partials, int uniform_active, int n_items, void* stream) {
+    const float qscale = (float)(1.4426950408889634 / std::sqrt((double)s.d));
+    const int grid = uniform_active > 0 ? s.BH * uniform_active : n_items;
+    if (grid <= 0) return 0;
+    if (s.d == 128)
+        hipLaunchKernelGGL(k_decode<128>, dim3(grid), dim3(kBlock), 0, (hipStream_t)stream, L,
+                           s.C, q, out, partials, qscale, uniform_active);
+    else
+        hipLaunchKernelGGL(k_decode<64>, dim3(grid), dim3(kBlock), 0, (hipStream_t)stream, L, s.C,
+                           q, out, partials, qscale, uniform_active);
+    return last_error();
+}
+
+int launch_export(const LayerDev& L, const Shape& s, uint8_t* mask, int32_t* count,
+                  void* stream) {
+    hipLaunchKernelGGL(k_export, dim3(s.BH), dim3(kBlock), 0, (hipStream_t)stream, L, s.C, s.d,
+                       s.N, mask, count);
+    return last_error();
+}
+
+}  // namespace headkv

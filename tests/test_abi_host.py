@@ -1,0 +1,117 @@
+"""Host-side checks of the C ABI: the library loads, exports every function the
+header declares, and rejects bad arguments and out-of-order calls with the
+documented status before touching the GPU.  No kernel is launched here."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_20600_amd import binding as B
+from paper_2605_20600_amd import workloads as W
+from paper_2605_20600_amd.session import make_config
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "headkv.h")
+FAKE = 0x7F0000000000          # 256-byte aligned, never dereferenced by these calls
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(headkv_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = B.load()
+    names = _declared()
+    assert set(names) == set(B.EXPORTED), names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _status(fn, *args):
+    return getattr(B.load(), fn)(*args)
+
+
+def test_plan_sizes_and_validation():
+    cfg = make_config(W.LUMINA768)
+    dense, meta, ws = B.headkv_plan(cfg)
+    assert dense > 0 and meta > 0 and ws > 0
+    # dense cache holds prefix + threshold tokens (K and V) for every head
+    per_head = 2 * (128 + 300) * 128 * 2 + 300 * 4
+    assert dense >= 8 * 32 * per_head
+    bad = [dict(head_dim=96), dict(batch=0), dict(num_visual=0), dict(group_threshold=0),
+           dict(group_threshold=99999), dict(period=0), dict(tau=0.0), dict(tau=1.5),
+           dict(rho_num=0), dict(rho_num=3, rho_den=2), dict(rs_num=3, rs_den=2),
+           dict(budget_mode=7), dict(prefix_len=-1), dict(row_len=0), dict(recent_len=0),
+           dict(num_heads=2000)]
+    for kw in bad:
+        c = make_config(W.LUMINA768)
+        for k, v in kw.items():
+            setattr(c, k, v)
+        with pytest.raises(B.HeadKVError) as e:
+            B.headkv_plan(c)
+        assert e.value.status in (B.HEADKV_ERR_INVALID_ARG, B.HEADKV_ERR_UNSUPPORTED), kw
+        assert B.headkv_last_error() != ""
+
+
+def _handle(wl=W.TINY):
+    cfg = make_config(wl)
+    return B.headkv_create(cfg, [FAKE] * cfg.num_layers, [FAKE + 4096] * cfg.num_layers, FAKE), cfg
+
+
+def test_create_rejects_bad_buffers():
+    cfg = make_config(W.TINY)
+    with pytest.raises(B.HeadKVError) as e:
+        B.headkv_create(cfg, [0], [FAKE], FAKE)
+    assert e.value.status == B.HEADKV_ERR_INVALID_ARG
+    with pytest.raises(B.HeadKVError) as e:
+        B.headkv_create(cfg, [FAKE + 8], [FAKE], FAKE)
+    assert e.value.status == B.HEADKV_ERR_INVALID_ARG
+    with pytest.raises(B.HeadKVError):
+        B.headkv_create(cfg, [FAKE], [FAKE], FAKE + 4)
+
+
+def test_calls_out_of_order_are_state_errors():
+    h, cfg = _handle()
+    try:
+        S = B.HEADKV_ERR_STATE
+        assert _status("headkv_decode_attn", h, 0, FAKE, FAKE, None) == S
+        assert _status("headkv_append_and_evict", h, 0, 0, FAKE, FAKE, FAKE, None) == S
+        assert _status("headkv_score_heads", h, 0, FAKE, FAKE, FAKE, None) == S
+        need = ctypes.c_size_t()
+        assert _status("headkv_assign_budgets", h, 0, FAKE, None, FAKE, None, 0,
+                       ctypes.byref(need), None) == S
+        assert _status("headkv_export_retained", h, 0, FAKE, FAKE, None) == S
+    finally:
+        B.headkv_destroy(h)
+
+
+def test_bad_arguments_are_rejected():
+    h, cfg = _handle()
+    try:
+        I = B.HEADKV_ERR_INVALID_ARG
+        assert _status("headkv_decode_attn", h, 5, FAKE, FAKE, None) == I      # layer
+        assert _status("headkv_decode_attn", h, -1, FAKE, FAKE, None) == I
+        assert _status("headkv_decode_attn", h, 0, None, FAKE, None) == I
+        assert _status("headkv_prefill", h, 0, None, None, None) == I          # C = 32 > 0
+        assert _status("headkv_prefill", h, 0, FAKE + 2, FAKE, None) == I      # misaligned
+        assert _status("headkv_decode_attn", None, 0, FAKE, FAKE, None) == I   # handle
+        assert _status("headkv_append_and_evict", h, 0, 0, None, FAKE, FAKE, None) == I
+        need = ctypes.c_size_t()
+        assert _status("headkv_assign_budgets", h, 0, None, None, FAKE, None, 0,
+                       ctypes.byref(need), None) == I
+    finally:
+        B.headkv_destroy(h)
+
+
+def test_override_mode_requires_budgets():
+    wl = W.TINY.with_(budget_mode=W.BUDGET_OVERRIDE)
+    h, cfg = _handle(wl)
+    try:
+        need = ctypes.c_size_t()
+        assert _status("headkv_assign_budgets", h, 0, FAKE, None, FAKE, None, 0,
+                       ctypes.byref(need), None) == B.HEADKV_ERR_INVALID_ARG
+    finally:
+        B.headkv_destroy(h)
