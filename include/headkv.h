@@ -92,9 +92,11 @@ typedef struct headkv_ctx* headkv_t;
 /* Sizes of the caller-owned device buffers.
  *   dense_kv_bytes: per layer, the cache before grouping (every head holds
  *                   its prefix and up to group_threshold visual tokens);
- *   meta_bytes:     per layer, lengths, positions tables, labels, budgets,
- *                   query sums and the work list;
- *   workspace_bytes: one buffer shared by all layers (split-K partials). */
+ *   meta_bytes:     per layer, segment table, lengths, labels, budgets,
+ *                   query sums and the attention dispatch order;
+ *   workspace_bytes: one buffer shared by all layers: attention partials of
+ *                   layers with fewer heads than compute units, which split
+ *                   each head over several blocks. */
 headkv_status headkv_plan(const headkv_config* cfg, size_t* dense_kv_bytes,
                           size_t* meta_bytes, size_t* workspace_bytes);
 
@@ -158,6 +160,43 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
  * out: [B][H][d] fp32, both device.  bf16 storage, fp32 accumulation. */
 headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q,
                                  float* out, void* stream);
+
+/* One whole decode step of `layer` in the fewest launches: the append of
+ * headkv_append_and_evict (with its periodic update when due) followed by the
+ * attention of headkv_decode_attn, with identical results.  Without an update
+ * the append is fused into the attention kernel.  Arguments as for those two
+ * calls.  The grouping step t_g needs the separate calls (HEADKV_ERR_STATE). */
+headkv_status headkv_decode_step(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
+                                 const uint16_t* k, const uint16_t* v, float* out,
+                                 void* stream);
+
+/* ---- Driver and measurement (not needed by a model, which calls the
+ * per-layer entry points between its own kernels). ---- */
+
+/* Runs headkv_decode_step for steps [step_begin, step_end) of every layer,
+ * step by step and layer by layer, from one host call.  q, k, v: host arrays
+ * of num_layers device pointers, each to [steps][B][H][d] bf16 with
+ * step_stride elements between consecutive steps; out: host array of
+ * num_layers device pointers to [B][H][d] fp32, overwritten every step.
+ * timing_every > 0: every step t with t % timing_every == 0 whose attention is
+ * one kernel launch is timed with the kernel's own start/end timestamps (see
+ * headkv_timing_reserve / headkv_timing_collect).  The range must not contain
+ * the grouping step (HEADKV_ERR_STATE); stops at the first failing call. */
+headkv_status headkv_run_steps(headkv_t h, int32_t step_begin, int32_t step_end,
+                               const uint16_t* const* q, const uint16_t* const* k,
+                               const uint16_t* const* v, int64_t step_stride,
+                               float* const* out, int32_t timing_every, void* stream);
+
+/* Creates events for `launches` timed attention launches (host call). */
+headkv_status headkv_timing_reserve(headkv_t h, int64_t launches);
+
+/* Waits for the timed launches since the last collect and returns the sum of
+ * their kernel durations (ms), their number, the sum of their algorithmic HBM
+ * bytes (K/V of every attended token, q, the output, the appended row, its
+ * position and the query-sum update), and the number of launches that found
+ * no free event. */
+headkv_status headkv_timing_collect(headkv_t h, double* kernel_ms, int64_t* launches,
+                                    double* alg_bytes, int64_t* dropped);
 
 /* Parity export: mask[b][h][p] = 1 iff visual position p is retained
  * ([B][H][N] uint8, device) and count[b][h] = number retained ([B][H] int32,

@@ -170,13 +170,18 @@ def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
                   wl.rho, None if ov is None else ov[layer, b])
     res = {"labels": labels, "n_star": n_star, "margin": margins, "mass_window": mass,
            "budgets": bud, "out": {}, "snaps": {}, "stats": {}}
-    for h in heads:
+    def one(h):
         q, k, v, kc, vc = inputs[h]
-        out, snaps, st = run_head(q, k, v, kc, vc, t_g, wl.period, bool(labels[h]),
-                                  int(bud[h]), wl.recent_len, wl.r_s, want_out, snap_steps)
-        res["out"][h] = out
-        res["snaps"][h] = snaps
-        res["stats"][h] = st
+        return h, run_head(q, k, v, kc, vc, t_g, wl.period, bool(labels[h]), int(bud[h]),
+                           wl.recent_len, wl.r_s, want_out, snap_steps)
+
+    # heads are independent; the C code runs without the GIL
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=max(1, min(16, os.cpu_count() or 1))) as ex:
+        for h, (out, snaps, st) in ex.map(one, heads):
+            res["out"][h] = out
+            res["snaps"][h] = snaps
+            res["stats"][h] = st
     return res
 
 

@@ -26,7 +26,9 @@ HEADKV_BUDGET_TOTAL = 2
 EXPORTED = (
     "headkv_plan", "headkv_create", "headkv_destroy", "headkv_prefill",
     "headkv_append_and_evict", "headkv_score_heads", "headkv_assign_budgets",
-    "headkv_decode_attn", "headkv_export_retained", "headkv_last_error",
+    "headkv_decode_attn", "headkv_decode_step", "headkv_export_retained",
+    "headkv_run_steps", "headkv_timing_reserve", "headkv_timing_collect",
+    "headkv_last_error",
 )
 
 
@@ -71,7 +73,12 @@ def load() -> ctypes.CDLL:
         "headkv_score_heads": [P, I, P, P, P, P],
         "headkv_assign_budgets": [P, I, P, P, P, P, Z, ctypes.POINTER(Z), P],
         "headkv_decode_attn": [P, I, P, P, P],
+        "headkv_decode_step": [P, I, I, P, P, P, P, P],
         "headkv_export_retained": [P, I, P, P, P],
+        "headkv_run_steps": [P, I, I, P, P, P, ctypes.c_int64, P, I, P],
+        "headkv_timing_reserve": [P, ctypes.c_int64],
+        "headkv_timing_collect": [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64),
+                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -149,5 +156,31 @@ def headkv_decode_attn(h: int, layer: int, q: int, out: int, stream: int = 0) ->
     _check(load().headkv_decode_attn(h, layer, q, out, stream), "headkv_decode_attn")
 
 
+def headkv_decode_step(h: int, layer: int, step: int, q: int, k: int, v: int, out: int,
+                       stream: int = 0) -> None:
+    _check(load().headkv_decode_step(h, layer, step, q, k, v, out, stream), "headkv_decode_step")
+
+
 def headkv_export_retained(h: int, layer: int, mask: int, count: int, stream: int = 0) -> None:
     _check(load().headkv_export_retained(h, layer, mask, count, stream), "headkv_export_retained")
+
+
+def headkv_run_steps(h: int, step_begin: int, step_end: int, q: Sequence[int], k: Sequence[int],
+                     v: Sequence[int], step_stride: int, out: Sequence[int],
+                     timing_every: int = 0, stream: int = 0) -> None:
+    n = len(q)
+    arr = lambda xs: (ctypes.c_void_p * n)(*xs)
+    _check(load().headkv_run_steps(h, step_begin, step_end, arr(q), arr(k), arr(v), step_stride,
+                                   arr(out), timing_every, stream), "headkv_run_steps")
+
+
+def headkv_timing_reserve(h: int, launches: int) -> None:
+    _check(load().headkv_timing_reserve(h, launches), "headkv_timing_reserve")
+
+
+def headkv_timing_collect(h: int) -> Tuple[float, int, float, int]:
+    """Returns (kernel ms, launches, algorithmic bytes, dropped)."""
+    ms, n, b, dr = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double(), ctypes.c_int64()
+    _check(load().headkv_timing_collect(h, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(b),
+                                        ctypes.byref(dr)), "headkv_timing_collect")
+    return ms.value, n.value, b.value, dr.value

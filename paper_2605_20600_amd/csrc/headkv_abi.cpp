@@ -33,8 +33,6 @@ headkv_status ok() { return HEADKV_OK; }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
-
 struct Layer {
     void* dense = nullptr;
     void* meta = nullptr;
@@ -42,7 +40,6 @@ struct Layer {
     bool prefilled = false;
     bool grouped = false;
     int last_step = -1;
-    int n_items = 0;               // decode work items after grouping
     std::vector<int> n, budget, cap;
 };
 
@@ -54,12 +51,18 @@ struct headkv_ctx {
     MetaLayout ml;
     int t_g = 0;
     int dense_cap = 0;             // visual slots per head before grouping
-    int dense_cph = 0;             // decode chunks per head before grouping
     int64_t dense_seg = 0;         // bytes per head segment before grouping
-    int max_chunks = 0;            // decode chunks of the largest possible head
     size_t ws_bytes = 0;
     void* ws = nullptr;
     std::vector<Layer> layers;
+    // timing of single-kernel decode steps: event pairs and algorithmic bytes
+    std::vector<hipEvent_t> events;
+    std::vector<double> timed_bytes;
+    size_t timed = 0;
+    int64_t timing_dropped = 0;
+    ~headkv_ctx() {
+        for (hipEvent_t e : events) (void)hipEventDestroy(e);
+    }
 };
 
 namespace {
@@ -96,7 +99,7 @@ headkv_status validate_config(const headkv_config* c) {
 }
 
 struct Plan {
-    int BH, dense_cap, dense_cph, max_chunks, max_items;
+    int BH, dense_cap;
     int64_t dense_seg;
     size_t dense_bytes, ws_bytes;
     MetaLayout ml;
@@ -108,15 +111,20 @@ Plan make_plan(const headkv_config& c) {
     p.dense_cap = c.group_threshold;
     p.dense_seg = (int64_t)segment_bytes(c.prefix_len, p.dense_cap, c.head_dim);
     p.dense_bytes = (size_t)p.dense_seg * p.BH;
-    p.dense_cph = ceil_div(c.prefix_len + p.dense_cap, kChunk);
-    const int cap_max = std::min(c.num_visual, HEADKV_MAX_CAPACITY);
-    p.max_chunks = ceil_div(c.prefix_len + cap_max, kChunk);
-    // ragged work list: every head's chunks, padded to equal XCD bins
-    p.max_items = p.BH * std::max(p.max_chunks, p.dense_cph) + kXcds * (p.max_chunks + 1);
-    p.ml.compute(p.BH, c.head_dim, p.max_items);
-    const size_t partials = (size_t)p.BH * std::max(p.max_chunks, p.dense_cph);
-    p.ws_bytes = align_up(partials * (c.head_dim + 2) * sizeof(float), 256);
+    p.ml.compute(p.BH, c.head_dim);
+    // partial (max, sum, weighted V) of every split of every head
+    p.ws_bytes = align_up((size_t)p.BH * kMaxSplits * (c.head_dim + 2) * sizeof(float), 256);
     return p;
+}
+
+// Attention splits per head: one block per head when the layer has at least
+// as many heads as compute units, else enough splits to fill the chip (each
+// split at least 256 tokens).
+int attn_splits(int BH, int max_len) {
+    if (BH >= kCus) return 1;
+    int s = (kCus + BH - 1) / BH;
+    s = std::min(s, (max_len + 255) / 256);
+    return std::max(1, std::min(s, kMaxSplits));
 }
 
 headkv_status check_layer(headkv_t h, int32_t layer) {
@@ -170,9 +178,7 @@ headkv_status headkv_create(const headkv_config* cfg, void* const* dense_kv, voi
     h->ml = p.ml;
     h->t_g = cfg->group_threshold - 1;
     h->dense_cap = p.dense_cap;
-    h->dense_cph = p.dense_cph;
     h->dense_seg = p.dense_seg;
-    h->max_chunks = p.max_chunks;
     h->ws_bytes = p.ws_bytes;
     h->ws = workspace;
     h->layers.resize(cfg->num_layers);
@@ -203,15 +209,22 @@ headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c, con
     L.cap.assign(h->shape.BH, h->dense_cap);
     L.budget.assign(h->shape.BH, 0);
     st = hip_status(launch_prefill(dev_of(h, L), h->shape, k_c, v_c, h->dense_seg, h->dense_cap,
-                                   h->dense_cph, stream),
+                                   stream),
                     "prefill launch");
     if (st) return st;
     L.prefilled = true;
     return ok();
 }
 
-headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
-                                      const uint16_t* k, const uint16_t* v, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks shared by every call that appends the token of `step`; fills the
+// append arguments and tells whether a periodic update follows the append.
+headkv_status prepare_append(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
+                             const uint16_t* k, const uint16_t* v, AppendArgs* a, bool* update,
+                             int* u) {
     headkv_status st = check_layer(h, layer);
     if (st) return st;
     if (!q || !k || !v) return fail(HEADKV_ERR_INVALID_ARG, "q / k / v is NULL");
@@ -227,21 +240,185 @@ headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step, c
     // window of the past-P queries that the next update scores against (Eq. 6)
     const int P = c.period;
     const int first = std::max(0, h->t_g - P + 1);
-    const int accumulate = step >= first ? 1 : 0;
-    const int reset = (step == first) || (step > h->t_g && (step - h->t_g - 1) % P == 0);
-    LayerDev D = dev_of(h, L);
-    st = hip_status(launch_append(D, h->shape, q, k, v, step, accumulate, reset, stream), "append launch");
-    if (st) return st;
+    a->q = q;
+    a->k = k;
+    a->v = v;
+    a->step = step;
+    a->accumulate = step >= first ? 1 : 0;
+    a->reset = (step == first) || (step > h->t_g && (step - h->t_g - 1) % P == 0);
+    *update = L.grouped && step > h->t_g && (step - h->t_g) % P == 0;
+    *u = (step - h->t_g) / P;
+    return ok();
+}
+
+// Host mirror after the append (and update) of `step`.
+void commit_append(headkv_t h, Layer& L, int32_t step, bool update) {
     for (int i = 0; i < h->shape.BH; ++i) L.n[i] += 1;
-    L.last_step = step;
-    if (L.grouped && step > h->t_g && (step - h->t_g) % P == 0) {
-        const int u = (step - h->t_g) / P;
-        st = hip_status(launch_update(D, h->shape, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
-                                      c.rs_den, u, stream),
-                        "update launch");
-        if (st) return st;
+    if (update)
         for (int i = 0; i < h->shape.BH; ++i) L.n[i] = std::min(L.n[i], L.budget[i]);
+    L.last_step = step;
+}
+
+int max_len(headkv_t h, const Layer& L) {
+    return h->cfg.prefix_len + *std::max_element(L.n.begin(), L.n.end());
+}
+
+}  // namespace
+
+extern "C" {
+
+headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
+                                      const uint16_t* k, const uint16_t* v, void* stream) {
+    AppendArgs a;
+    bool update = false;
+    int u = 0;
+    headkv_status st = prepare_append(h, layer, step, q, k, v, &a, &update, &u);
+    if (st) return st;
+    Layer& L = h->layers[layer];
+    const headkv_config& c = h->cfg;
+    LayerDev D = dev_of(h, L);
+    if (update)
+        st = hip_status(launch_update(D, h->shape, a, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
+                                      c.rs_den, u, stream),
+                        "append + update launch");
+    else
+        st = hip_status(launch_append(D, h->shape, a, stream), "append launch");
+    if (st) return st;
+    commit_append(h, L, step, update);
+    return ok();
+}
+
+}  // extern "C"
+
+namespace {
+
+// Algorithmic HBM bytes of one fused append + attention launch, from the host
+// mirror before the append: K and V of the prefix, the retained tokens and
+// the new token; q in, the output out; the new K/V row and its position
+// written; the fp64 query sum read and written when accumulating.
+double fused_step_bytes(headkv_t h, const Layer& L, bool accumulate) {
+    const headkv_config& c = h->cfg;
+    const double d = c.head_dim;
+    double tokens = 0;
+    for (int n : L.n) tokens += c.prefix_len + n + 1;
+    const double per_head = d * 2 + d * 4 + 2 * d * 2 + 4 + (accumulate ? 2 * d * 8 : 0);
+    return tokens * 2 * d * 2 + h->shape.BH * per_head;
+}
+
+headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
+                               const uint16_t* k, const uint16_t* v, float* out, void* stream,
+                               bool time_it) {
+    AppendArgs a;
+    bool update = false;
+    int u = 0;
+    headkv_status st = prepare_append(h, layer, step, q, k, v, &a, &update, &u);
+    if (st) return st;
+    if (!out) return fail(HEADKV_ERR_INVALID_ARG, "out is NULL");
+    Layer& L = h->layers[layer];
+    const headkv_config& c = h->cfg;
+    if (!L.grouped && step == h->t_g)
+        return fail(HEADKV_ERR_STATE, "the grouping step needs the separate calls");
+    LayerDev D = dev_of(h, L);
+    const int splits = attn_splits(h->shape.BH, max_len(h, L) + 1);
+    AppendArgs none = a;
+    none.k = none.v = none.q = nullptr;
+    float* ws = static_cast<float*>(h->ws);
+    if (update) {
+        st = hip_status(launch_update(D, h->shape, a, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
+                                      c.rs_den, u, stream),
+                        "append + update launch");
+        if (!st) st = hip_status(launch_attn(D, h->shape, none, q, out, ws, splits, stream), "attention launch");
+    } else if (splits == 1) {
+        void* e0 = nullptr;
+        void* e1 = nullptr;
+        if (time_it) {
+            if (2 * (h->timed + 1) <= h->events.size()) {
+                e0 = h->events[2 * h->timed];
+                e1 = h->events[2 * h->timed + 1];
+                h->timed_bytes[h->timed] = fused_step_bytes(h, L, a.accumulate != 0);
+                ++h->timed;
+            } else {
+                ++h->timing_dropped;
+            }
+        }
+        st = hip_status(launch_attn(D, h->shape, a, q, out, ws, 1, stream, e0, e1),
+                        "append + attention launch");
+    } else {
+        st = hip_status(launch_append(D, h->shape, a, stream), "append launch");
+        if (!st) st = hip_status(launch_attn(D, h->shape, none, q, out, ws, splits, stream), "attention launch");
     }
+    if (st) return st;
+    commit_append(h, L, step, update);
+    return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+headkv_status headkv_decode_step(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
+                                 const uint16_t* k, const uint16_t* v, float* out, void* stream) {
+    return decode_step_impl(h, layer, step, q, k, v, out, stream, false);
+}
+
+headkv_status headkv_run_steps(headkv_t h, int32_t step_begin, int32_t step_end,
+                               const uint16_t* const* q, const uint16_t* const* k,
+                               const uint16_t* const* v, int64_t step_stride, float* const* out,
+                               int32_t timing_every, void* stream) {
+    if (!h) return fail(HEADKV_ERR_INVALID_ARG, "handle is NULL");
+    if (!q || !k || !v || !out) return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer array");
+    if (step_begin < 0 || step_end < step_begin || step_stride < 0 || timing_every < 0)
+        return fail(HEADKV_ERR_INVALID_ARG, "bad step range, stride or timing interval");
+    const int NL = h->cfg.num_layers;
+    for (int t = step_begin; t < step_end; ++t) {
+        const bool time_it = timing_every > 0 && t % timing_every == 0;
+        for (int l = 0; l < NL; ++l) {
+            if (!q[l] || !k[l] || !v[l] || !out[l])
+                return fail(HEADKV_ERR_INVALID_ARG, "NULL layer pointer");
+            const size_t off = (size_t)t * (size_t)step_stride;
+            headkv_status st = decode_step_impl(h, l, t, q[l] + off, k[l] + off, v[l] + off,
+                                                out[l], stream, time_it);
+            if (st) return st;
+        }
+    }
+    return ok();
+}
+
+headkv_status headkv_timing_reserve(headkv_t h, int64_t launches) {
+    if (!h || launches < 0) return fail(HEADKV_ERR_INVALID_ARG, "bad handle or count");
+    while ((int64_t)h->events.size() < 2 * launches) {
+        hipEvent_t e;
+        headkv_status st = hip_status(hipEventCreate(&e), "event create");
+        if (st) return st;
+        h->events.push_back(e);
+    }
+    h->timed_bytes.resize(h->events.size() / 2);
+    return ok();
+}
+
+headkv_status headkv_timing_collect(headkv_t h, double* kernel_ms, int64_t* launches,
+                                    double* alg_bytes, int64_t* dropped) {
+    if (!h || !kernel_ms || !launches || !alg_bytes || !dropped)
+        return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer");
+    double ms = 0, bytes = 0;
+    if (h->timed > 0) {
+        headkv_status st = hip_status(hipEventSynchronize(h->events[2 * h->timed - 1]), "event wait");
+        if (st) return st;
+    }
+    for (size_t i = 0; i < h->timed; ++i) {
+        float e = 0;
+        headkv_status st = hip_status(hipEventElapsedTime(&e, h->events[2 * i], h->events[2 * i + 1]),
+                                      "event time");
+        if (st) return st;
+        ms += e;
+        bytes += h->timed_bytes[i];
+    }
+    *kernel_ms = ms;
+    *launches = (int64_t)h->timed;
+    *alg_bytes = bytes;
+    *dropped = h->timing_dropped;
+    h->timed = 0;
+    h->timing_dropped = 0;
     return ok();
 }
 
@@ -289,9 +466,8 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     if (st) return st;
     // segments: prefix + min(budget + P, N) slots each, in head order
     std::vector<int64_t> off(BH);
-    std::vector<int32_t> cap(BH), base(BH);
+    std::vector<int32_t> cap(BH);
     size_t total = 0;
-    int chunks_total = 0;
     for (int i = 0; i < BH; ++i) {
         if (bud[i] < 1 || bud[i] > c.num_visual)
             return fail(HEADKV_ERR_INVALID_ARG, "a budget is outside [1, num_visual]");
@@ -300,51 +476,28 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
             return fail(HEADKV_ERR_UNSUPPORTED, "budget + period exceeds HEADKV_MAX_CAPACITY");
         off[i] = (int64_t)total;
         total += segment_bytes(c.prefix_len, cap[i], c.head_dim);
-        base[i] = chunks_total;
-        chunks_total += ceil_div(c.prefix_len + cap[i], kChunk);
     }
     *ragged_bytes_needed = total;
     if (!ragged_kv || ragged_bytes < total)
         return fail(HEADKV_ERR_CAPACITY, "ragged_kv is NULL or smaller than *ragged_bytes_needed");
-    // decode work list: heads spread over the XCD bins by chunk count (largest
-    // first onto the lightest bin); block i runs on XCD i % 8, so all chunks of
-    // a head meet in one L2 for the merge
-    std::vector<int> order(BH);
+    // attention dispatch order: longest heads first, so that when a layer
+    // needs more than one round of blocks the short heads fill the tail
+    std::vector<int32_t> order(BH);
     for (int i = 0; i < BH; ++i) order[i] = i;
     std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cap[a] > cap[b]; });
-    std::vector<std::vector<int32_t>> bins(kXcds);
-    std::vector<long long> load(kXcds, 0);
-    for (int i : order) {
-        const int nc = ceil_div(c.prefix_len + cap[i], kChunk);
-        const int x = (int)(std::min_element(load.begin(), load.end()) - load.begin());
-        for (int ch = 0; ch < nc; ++ch) {
-            bins[x].push_back(i);
-            bins[x].push_back(ch);
-        }
-        load[x] += nc;
-    }
-    size_t longest = 0;
-    for (auto& b : bins) longest = std::max(longest, b.size() / 2);
-    const int n_items = (int)longest * kXcds;
-    if (n_items > h->ml.max_items) return fail(HEADKV_ERR_UNSUPPORTED, "work list exceeds its planned size");
-    std::vector<int32_t> work((size_t)n_items * 2, -1);
-    for (int x = 0; x < kXcds; ++x)
-        for (size_t k = 0; k < bins[x].size() / 2; ++k) {
-            work[2 * (k * kXcds + x)] = bins[x][2 * k];
-            work[2 * (k * kXcds + x) + 1] = bins[x][2 * k + 1];
-        }
     // tables of the new layout (the host vectors outlive the copies: the stream
     // is waited for below on every path)
     char* mb = static_cast<char*>(L.meta);
     st = hip_status(hipMemcpyAsync(mb + h->ml.seg_off, off.data(), sizeof(int64_t) * BH, hipMemcpyHostToDevice, s), "table upload");
     if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.cap, cap.data(), sizeof(int32_t) * BH, hipMemcpyHostToDevice, s), "table upload");
-    if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.chunk_base, base.data(), sizeof(int32_t) * BH, hipMemcpyHostToDevice, s), "table upload");
-    if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.work, work.data(), sizeof(int32_t) * work.size(), hipMemcpyHostToDevice, s), "table upload");
+    if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.order, order.data(), sizeof(int32_t) * BH, hipMemcpyHostToDevice, s), "table upload");
     // first update, fused with the move from the dense buffer into the segments
     if (!st) {
         LayerDev Dnew = make_layer_dev(ragged_kv, L.meta, h->ml);
-        st = hip_status(launch_update(Dnew, h->shape, static_cast<const char*>(L.dense), 1, h->dense_seg,
-                                      h->dense_cap, c.recent_len, c.rs_num, c.rs_den, 0, stream),
+        AppendArgs none{};
+        st = hip_status(launch_update(Dnew, h->shape, none, static_cast<const char*>(L.dense), 1,
+                                      h->dense_seg, h->dense_cap, c.recent_len, c.rs_num, c.rs_den,
+                                      0, stream),
                         "relayout launch");
     }
     headkv_status st_wait = hip_status(hipStreamSynchronize(s), "stream wait");
@@ -352,7 +505,6 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     if (st_wait) return st_wait;
     L.ragged = ragged_kv;
     L.grouped = true;
-    L.n_items = n_items;
     L.budget.assign(bud.begin(), bud.end());
     L.cap.assign(cap.begin(), cap.end());
     for (int i = 0; i < BH; ++i) L.n[i] = std::min(L.n[i], L.budget[i]);
@@ -368,10 +520,10 @@ headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, f
     if (!L.prefilled || L.last_step < 0) return fail(HEADKV_ERR_STATE, "decode_attn before the first append");
     if (!L.grouped && L.last_step == h->t_g)
         return fail(HEADKV_ERR_STATE, "assign_budgets must run before attention at step group_threshold - 1");
-    const int uniform = L.grouped ? 0 : ceil_div(h->cfg.prefix_len + L.last_step + 1, kChunk);
-    return hip_status(launch_decode(dev_of(h, L), h->shape, q, out, static_cast<float*>(h->ws), uniform,
-                                    L.n_items, stream),
-                      "decode launch");
+    AppendArgs none{};
+    return hip_status(launch_attn(dev_of(h, L), h->shape, none, q, out, static_cast<float*>(h->ws),
+                                  attn_splits(h->shape.BH, max_len(h, L)), stream),
+                      "attention launch");
 }
 
 headkv_status headkv_export_retained(headkv_t h, int32_t layer, uint8_t* mask, int32_t* count,

@@ -4,20 +4,25 @@
 //   k_prefill  Step 1 cache prefilling (Sec. 4): conditional keys/values into
 //              rows 0..C-1 of every head, layer state reset.
 //   k_append   cache append (Sec. 3, KV Cache) + running sum of the queries of
-//              the current update window (Eq. 6 is linear in the queries).
+//              the current update window (Eq. 6 is linear in the queries);
+//              also fused into k_update and k_attn.
 //   k_score    head grouping (Sec. 4, Step 2), fp64.
 //   k_budgets  per-head budgets (Sec. 5.1, Implementation Details).
 //   k_update   periodic update (Eqs. 2-6): sliding window (Eq. 3) or
 //              Stratified Token Eviction (Eqs. 4-6), fused with the
 //              compaction of the head's slots or, at the grouping step, with
 //              the move into the head's own segment.
-//   k_decode   decode attention, Eq. (1), split over 64-token chunks with an
-//              online softmax per chunk and a last-block merge per head.
+//   k_attn     decode attention, Eq. (1): one 1024-thread block per head with
+//              all of the head's K/V loads in flight, online softmax in
+//              registers, merge through LDS; optionally fused with the append;
+//   k_merge    merge of the splits of a head, for layers with fewer heads
+//              than compute units.
 //   k_export   retained-position masks for parity checks.
 //
 // Everything that decides an index (grouping mass, eviction scores) is
 // computed in fp64 with one fixed summation order and no fused multiply-add,
 // so the decisions do not depend on thread scheduling.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -91,7 +96,7 @@ __device__ __forceinline__ SegPtrs seg_ptrs(char* seg, int C, int cap, int d) {
 // ------------------------------------------------------------------ prefill
 __global__ __launch_bounds__(kBlock) void k_prefill(LayerDev L, int C, int d, const uint16_t* kc,
                                                     const uint16_t* vc, int64_t seg_bytes,
-                                                    int dense_cap, int cph) {
+                                                    int dense_cap) {
     const int h = blockIdx.x, tid = threadIdx.x;
     if (tid == 0) {
         L.seg_off[h] = (int64_t)h * seg_bytes;
@@ -100,8 +105,7 @@ __global__ __launch_bounds__(kBlock) void k_prefill(LayerDev L, int C, int d, co
         L.budget[h] = 0;
         L.nstar[h] = 0;
         L.label[h] = 0;
-        L.counter[h] = 0;
-        L.chunk_base[h] = h * cph;
+        L.order[h] = h;
     }
     for (int i = tid; i < d; i += kBlock) L.qsum[(size_t)h * d + i] = 0.0;
     if (C == 0) return;
@@ -118,24 +122,55 @@ __global__ __launch_bounds__(kBlock) void k_prefill(LayerDev L, int C, int d, co
 }
 
 // ------------------------------------------------------------------- append
-__global__ void k_append(LayerDev L, int C, int d, const uint16_t* q, const uint16_t* k,
-                         const uint16_t* v, int step, int accumulate, int reset) {
+// K <- [K, k_t], V <- [V, v_t] for head h by the threads tid < d of a block:
+// row C+n, pos[n] = step, the query sum of the update window.  Split in a
+// load half and a store half so that a caller can put other loads between
+// them; the length n is changed by append_commit once no thread reads it.
+struct AppendVals {
+    uint16_t k = 0, v = 0;
+    double qs_old = 0.0, q = 0.0;
+};
+
+__device__ __forceinline__ AppendVals append_load(const LayerDev& L, int d, int h,
+                                                  const AppendArgs& a, int tid) {
+    AppendVals r;
+    if (tid < d) {
+        r.k = a.k[(size_t)h * d + tid];
+        r.v = a.v[(size_t)h * d + tid];
+        if (a.accumulate) {
+            r.q = bf_f64(a.q[(size_t)h * d + tid]);
+            if (!a.reset) r.qs_old = L.qsum[(size_t)h * d + tid];
+        }
+    }
+    return r;
+}
+
+__device__ __forceinline__ void append_store(const LayerDev& L, int C, int d, int h, int n,
+                                             const AppendArgs& a, const AppendVals& r, int tid) {
 #pragma clang fp contract(off)
-    const int h = blockIdx.x, i = threadIdx.x;
-    const int n = L.n[h];
+    if (tid >= d) return;
     SegPtrs s = seg_ptrs(L.kv + L.seg_off[h], C, L.cap[h], d);
     const size_t row = (size_t)(C + n) * d;
-    s.K[row + i] = k[(size_t)h * d + i];
-    s.V[row + i] = v[(size_t)h * d + i];
-    if (accumulate) {
-        double* qs = L.qsum + (size_t)h * d + i;
-        *qs = (reset ? 0.0 : *qs) + bf_f64(q[(size_t)h * d + i]);
-    }
+    s.K[row + tid] = r.k;
+    s.V[row + tid] = r.v;
+    if (a.accumulate) L.qsum[(size_t)h * d + tid] = r.qs_old + r.q;  // 0 + q on a reset
+    if (tid == 0) s.pos[n] = a.step;
+}
+
+__device__ __forceinline__ void append_token(const LayerDev& L, int C, int d, int h, int n,
+                                             const AppendArgs& a, int tid) {
+    append_store(L, C, d, h, n, a, append_load(L, d, h, a, tid), tid);
+}
+
+__device__ __forceinline__ void append_commit(const LayerDev& L, int h, int n, int tid) {
+    if (tid == 0) L.n[h] = n + 1;
+}
+
+__global__ void k_append(LayerDev L, int C, int d, AppendArgs a) {
+    const int h = blockIdx.x, n = L.n[h];
+    append_token(L, C, d, h, n, a, threadIdx.x);
     __syncthreads();
-    if (i == 0) {
-        s.pos[n] = step;
-        L.n[h] = n + 1;
-    }
+    append_commit(L, h, n, threadIdx.x);
 }
 
 // ------------------------------------------------------------ head grouping
@@ -234,10 +269,10 @@ __global__ void k_budgets(LayerDev L, int H, int N, const uint8_t* is_local,
 
 // ------------------------------------------------------------------- update
 template <int D>
-__global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, const char* src_kv,
-                                                   int relayout, int64_t dense_seg_bytes,
-                                                   int dense_cap, int recent_len, int rs_num,
-                                                   int rs_den, int u) {
+__global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, AppendArgs a,
+                                                   const char* src_kv, int relayout,
+                                                   int64_t dense_seg_bytes, int dense_cap,
+                                                   int recent_len, int rs_num, int rs_den, int u) {
 #pragma clang fp contract(off)
     constexpr int kMaxCap = HEADKV_MAX_CAPACITY;
     constexpr int kWords = HEADKV_MAX_VISUAL / 32;
@@ -249,6 +284,13 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, con
     __shared__ double sig[kMaxCap];      // score by rank; reused as int lists
     __shared__ double qs[D];
     const int h = blockIdx.x, tid = threadIdx.x;
+    if (a.k != nullptr) {  // the step's append, then the update that follows it
+        const int n0 = L.n[h];
+        append_token(L, C, D, h, n0, a, tid);
+        __syncthreads();
+        append_commit(L, h, n0, tid);
+        __syncthreads();
+    }
     const int n = L.n[h];
     const int B = L.budget[h];
     const int local = L.label[h];
@@ -414,90 +456,132 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, con
     if (tid == 0) L.n[h] = n_new;
 }
 
-// ------------------------------------------------------------------- decode
-// One block = 4 wavefronts = one 64-token chunk of one head.  Each 16-lane
-// row of a wavefront holds one token at a time (d/16 elements per lane, one
-// 8- or 16-byte load per lane), so a K or V row is read by one coalesced row
-// of lanes; the q.k partial dot is summed over the row with DPP.
+// ---------------------------------------------------------------- attention
+// Decode attention, Eq. (1), one block per head (or per split of a head when a
+// layer has fewer heads than compute units).  1024 threads = 64 rows of 16
+// lanes; each row holds one token at a time, d/16 elements per lane (one 8- or
+// 16-byte load), so the 4 rows of a wavefront read 4 consecutive K or V rows
+// of the segment.  A pass covers 64 x kAttnTpr = 512 tokens: every load of the
+// pass is issued before the first one is used (row indices past the end are
+// clamped to the last token and their logits masked, so no load sits behind a
+// branch), which puts a whole head of up to 512 tokens in flight at once.  K/V
+// are read once per step, so the loads are non-temporal.  The softmax is
+// online per row; rows are merged with cross-lane swaps and the 16 wavefronts
+// through LDS.  With `append`, the step's token is attended from the input and
+// written into the cache by the same block.
 template <int D>
-__global__ __launch_bounds__(kBlock) void k_decode(LayerDev L, int C, const uint16_t* __restrict__ q,
-                                                   float* __restrict__ out,
-                                                   float* __restrict__ part, float qscale,
-                                                   int uniform_active) {
-    constexpr int VPL = D / 16;   // bf16 elements per lane
-    constexpr int NW = VPL / 2;   // 32-bit words per lane
+struct AttnRegs {
+    static constexpr int VPL = D / 16;  // bf16 elements per lane
+    static constexpr int NW = VPL / 2;  // 32-bit words per lane
     using Vec = Words<NW>;
-    int h, c;
-    if (uniform_active > 0) {
-        h = blockIdx.x / uniform_active;
-        c = blockIdx.x - h * uniform_active;
-    } else {
-        h = L.work[2 * blockIdx.x];
-        c = L.work[2 * blockIdx.x + 1];
-        if (h < 0) return;
-    }
-    const int n = L.n[h];
-    const int cap = L.cap[h];
-    const int len = C + n;
-    const int active = (len + kChunk - 1) / kChunk;
-    if (c >= active) return;
-    const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + L.seg_off[h]);
-    const uint16_t* V = K + (size_t)(C + cap) * D;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int row = lane >> 4, col = lane & 15;
+};
 
-    float qf[VPL];
-    {
-        const Vec u = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
+template <int NW>
+__device__ __forceinline__ Words<NW> nt_load(const uint16_t* p) {
+    typedef unsigned int vec_t __attribute__((ext_vector_type(NW)));
+    const vec_t t = __builtin_nontemporal_load(reinterpret_cast<const vec_t*>(p));
+    Words<NW> w;
 #pragma unroll
-        for (int e = 0; e < NW; ++e) {
-            qf[2 * e] = bf_lo(u.w[e]) * qscale;
-            qf[2 * e + 1] = bf_hi(u.w[e]) * qscale;
-        }
-    }
-    const int t0 = c * kChunk + wave * 16 + row;
-    Vec kr[4], vr[4];
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-        const int tok = t0 + it * 4;
-        if (tok < len) {
-            kr[it] = *reinterpret_cast<const Vec*>(K + (size_t)tok * D + col * VPL);
-            vr[it] = *reinterpret_cast<const Vec*>(V + (size_t)tok * D + col * VPL);
-        } else {
-#pragma unroll
-            for (int e = 0; e < NW; ++e) kr[it].w[e] = vr[it].w[e] = 0u;
-        }
-    }
-    float s[4];
-#pragma unroll
-    for (int it = 0; it < 4; ++it) {
-        float dp = 0.f;
-#pragma unroll
-        for (int e = 0; e < NW; ++e) {
-            dp += qf[2 * e] * bf_lo(kr[it].w[e]);
-            dp += qf[2 * e + 1] * bf_hi(kr[it].w[e]);
-        }
-        dp = row16_sum(dp);
-        s[it] = (t0 + it * 4 < len) ? dp : -INFINITY;
-    }
-    float m = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
-    float l = 0.f;
+    for (int e = 0; e < NW; ++e) w.w[e] = t[e];
+    return w;
+}
+
+template <int D, bool APPEND>
+__global__ __launch_bounds__(kAttnThreads) void k_attn(LayerDev L, int C, AppendArgs a,
+                                                       const uint16_t* __restrict__ q,
+                                                       float* __restrict__ out,
+                                                       float* __restrict__ part, int splits,
+                                                       int use_order, float qscale) {
+    using Vec = typename AttnRegs<D>::Vec;
+    constexpr int VPL = AttnRegs<D>::VPL;
+    constexpr int NW = AttnRegs<D>::NW;
+    constexpr int ROWS = kAttnThreads / 16;
+    constexpr int TP = ROWS * kAttnTpr;  // tokens per pass
+    constexpr int WAVES = kAttnThreads / 64;
+    const int item = blockIdx.x / splits;
+    const int sp = blockIdx.x - item * splits;
+    const int h = use_order ? L.order[item] : item;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int row = tid >> 4, col = tid & 15;
+    const Vec qraw = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
+    const int n = L.n[h];
+    const int len = C + n + (APPEND ? 1 : 0);
+    const int span = (len + splits - 1) / splits;
+    const int t_begin = sp * span;
+    const int t_end = min(len, t_begin + span);
+    const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + L.seg_off[h]);
+    const uint16_t* V = K + (size_t)(C + L.cap[h]) * D;
+
+    // the append's loads go out before the K/V stream and its stores right
+    // after (the attention reads the new token from the input, never from row
+    // C+n); n itself changes at the end
+    AppendVals av;
+    if (APPEND) av = append_load(L, D, h, a, tid);
+    float m = -INFINITY, l = 0.f;
     float acc[VPL];
 #pragma unroll
     for (int e = 0; e < VPL; ++e) acc[e] = 0.f;
-    if (m != -INFINITY) {
+    float qf[VPL];
+    bool q_ready = false;
+    for (int t0 = t_begin; t0 < t_end; t0 += TP) {
+        Vec kk[kAttnTpr], vv[kAttnTpr];
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
-            const float p = __builtin_amdgcn_exp2f(s[it] - m);
-            l += p;
+        for (int j = 0; j < kAttnTpr; ++j) {
+            const int tok = min(t0 + j * ROWS + row, t_end - 1);
+            const uint16_t* kp = K + (size_t)tok * D;
+            const uint16_t* vp = V + (size_t)tok * D;
+            if (APPEND && tok == len - 1) {
+                kp = a.k + (size_t)h * D;
+                vp = a.v + (size_t)h * D;
+            }
+            kk[j] = nt_load<NW>(kp + col * VPL);
+            vv[j] = nt_load<NW>(vp + col * VPL);
+        }
+        // keep every load of the pass ahead of its first use
+        __builtin_amdgcn_sched_barrier(0);
+        if (!q_ready) {
+            if (APPEND) append_store(L, C, D, h, n, a, av, tid);
 #pragma unroll
             for (int e = 0; e < NW; ++e) {
-                acc[2 * e] += p * bf_lo(vr[it].w[e]);
-                acc[2 * e + 1] += p * bf_hi(vr[it].w[e]);
+                qf[2 * e] = bf_lo(qraw.w[e]) * qscale;
+                qf[2 * e + 1] = bf_hi(qraw.w[e]) * qscale;
             }
+            q_ready = true;
+        }
+        float s[kAttnTpr];
+        float mx = m;
+#pragma unroll
+        for (int j = 0; j < kAttnTpr; ++j) {
+            float dp = 0.f;
+#pragma unroll
+            for (int e = 0; e < NW; ++e) {
+                dp += qf[2 * e] * bf_lo(kk[j].w[e]);
+                dp += qf[2 * e + 1] * bf_hi(kk[j].w[e]);
+            }
+            dp = row16_sum(dp);
+            s[j] = (t0 + j * ROWS + row < t_end) ? dp : -INFINITY;
+            mx = fmaxf(mx, s[j]);
+        }
+        if (mx != -INFINITY) {
+            const float f = __builtin_amdgcn_exp2f(m - mx);  // m = -inf gives 0
+            l *= f;
+#pragma unroll
+            for (int e = 0; e < VPL; ++e) acc[e] *= f;
+#pragma unroll
+            for (int j = 0; j < kAttnTpr; ++j) {
+                const float p = __builtin_amdgcn_exp2f(s[j] - mx);
+                l += p;
+#pragma unroll
+                for (int e = 0; e < NW; ++e) {
+                    acc[2 * e] += p * bf_lo(vv[j].w[e]);
+                    acc[2 * e + 1] += p * bf_hi(vv[j].w[e]);
+                }
+            }
+            m = mx;
         }
     }
-    // merge the four rows of the wavefront
+    if (APPEND && !q_ready) append_store(L, C, D, h, n, a, av, tid);  // empty range
+    // merge the four rows of each wavefront
 #pragma unroll
     for (int off = 16; off <= 32; off <<= 1) {
         const float mo = __shfl_xor(m, off);
@@ -513,62 +597,68 @@ __global__ __launch_bounds__(kBlock) void k_decode(LayerDev L, int C, const uint
         }
         m = mn;
     }
-    __shared__ float sm[4], sl[4];
-    __shared__ float sacc[4][D];
-    if (row == 0) {
+    __shared__ float sm[WAVES], sl[WAVES];
+    __shared__ float sacc[WAVES][D];
+    if (lane < 16) {
 #pragma unroll
         for (int e = 0; e < VPL; ++e) sacc[wave][col * VPL + e] = acc[e];
-        if (col == 0) {
+        if (lane == 0) {
             sm[wave] = m;
             sl[wave] = l;
         }
     }
-    __syncthreads();
-    float o_acc = 0.f, o_l = 0.f, o_m = -INFINITY;
+    __syncthreads();  // every wavefront has read n before the append changes it
+    if (APPEND) append_commit(L, h, n, tid);
     if (tid < D) {
-        o_m = fmaxf(fmaxf(sm[0], sm[1]), fmaxf(sm[2], sm[3]));
+        float mx = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            const float f = (sm[w] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sm[w] - o_m);
-            o_acc += f * sacc[w][tid];
-            o_l += f * sl[w];
+        for (int w = 0; w < WAVES; ++w) mx = fmaxf(mx, sm[w]);
+        float o = 0.f, z = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) {
+            const float f = (sm[w] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sm[w] - mx);
+            o += f * sacc[w][tid];
+            z += f * sl[w];
+        }
+        if (splits == 1) {
+            out[(size_t)h * D + tid] = o / z;
+        } else {
+            float* pp = part + ((size_t)h * splits + sp) * (D + 2);
+            pp[tid] = o;
+            if (tid == 0) {
+                pp[D] = mx;
+                pp[D + 1] = z;
+            }
         }
     }
-    if (active == 1) {
-        if (tid < D) out[(size_t)h * D + tid] = o_acc / o_l;
-        return;
-    }
+}
+
+// Merge of the splits of every head (layers with fewer heads than compute
+// units).  A kernel of its own: plain device memory is only coherent across
+// the XCDs' L2 caches at kernel boundaries.
+template <int D>
+__global__ __launch_bounds__(D) void k_merge(float* __restrict__ out,
+                                             const float* __restrict__ part, int splits) {
+    const int h = blockIdx.x, tid = threadIdx.x;
     constexpr int PS = D + 2;
-    float* pp = part + (size_t)(L.chunk_base[h] + c) * PS;
-    if (tid < D) pp[tid] = o_acc;
-    if (tid == 0) {
-        pp[D] = o_m;
-        pp[D + 1] = o_l;
+    const float* p0 = part + (size_t)h * splits * PS;
+    float mi[kMaxSplits];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kMaxSplits; ++i) {
+        mi[i] = i < splits ? p0[(size_t)i * PS + D] : -INFINITY;
+        mx = fmaxf(mx, mi[i]);
     }
-    __threadfence();
-    __syncthreads();
-    __shared__ int s_last;
-    if (tid == 0) {
-        const unsigned prev = atomicAdd(&L.counter[h], 1u);
-        s_last = (prev == (unsigned)(active - 1)) ? 1 : 0;
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    if (tid < D) {
-        const float* p0 = part + (size_t)L.chunk_base[h] * PS;
-        float mx = -INFINITY;
-        for (int i = 0; i < active; ++i) mx = fmaxf(mx, p0[(size_t)i * PS + D]);
-        float num = 0.f, den = 0.f;
-        for (int i = 0; i < active; ++i) {
-            const float mi = p0[(size_t)i * PS + D];
-            const float f = (mi == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mi - mx);
+    float num = 0.f, den = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMaxSplits; ++i) {
+        if (i < splits && mi[i] != -INFINITY) {
+            const float f = __builtin_amdgcn_exp2f(mi[i] - mx);
             num += f * p0[(size_t)i * PS + tid];
             den += f * p0[(size_t)i * PS + D + 1];
         }
-        out[(size_t)h * D + tid] = num / den;
     }
-    if (tid == 0) L.counter[h] = 0u;
+    out[(size_t)h * D + tid] = num / den;
 }
 
 // ------------------------------------------------------------------- export
@@ -588,16 +678,14 @@ inline int last_error() { return (int)hipGetLastError(); }
 }  // namespace
 
 int launch_prefill(const LayerDev& L, const Shape& s, const uint16_t* kc, const uint16_t* vc,
-                   int64_t dense_seg_bytes, int dense_cap, int dense_cph, void* stream) {
+                   int64_t dense_seg_bytes, int dense_cap, void* stream) {
     hipLaunchKernelGGL(k_prefill, dim3(s.BH), dim3(kBlock), 0, (hipStream_t)stream, L, s.C, s.d,
-                       kc, vc, dense_seg_bytes, dense_cap, dense_cph);
+                       kc, vc, dense_seg_bytes, dense_cap);
     return last_error();
 }
 
-int launch_append(const LayerDev& L, const Shape& s, const uint16_t* q, const uint16_t* k,
-                  const uint16_t* v, int step, int accumulate, int reset, void* stream) {
-    hipLaunchKernelGGL(k_append, dim3(s.BH), dim3(s.d), 0, (hipStream_t)stream, L, s.C, s.d, q, k,
-                       v, step, accumulate, reset);
+int launch_append(const LayerDev& L, const Shape& s, const AppendArgs& a, void* stream) {
+    hipLaunchKernelGGL(k_append, dim3(s.BH), dim3(s.d), 0, (hipStream_t)stream, L, s.C, s.d, a);
     return last_error();
 }
 
@@ -618,31 +706,46 @@ int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
     return last_error();
 }
 
-int launch_update(const LayerDev& L, const Shape& s, const char* src_kv, int relayout,
-                  int64_t dense_seg_bytes, int dense_cap, int recent_len, int rs_num,
-                  int rs_den, int u, void* stream) {
+int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
+                  int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
+                  int rs_num, int rs_den, int u, void* stream) {
+    hipStream_t st = (hipStream_t)stream;
     if (s.d == 128)
-        hipLaunchKernelGGL(k_update<128>, dim3(s.BH), dim3(kBlock), 0, (hipStream_t)stream, L,
-                           s.C, s.N, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
-                           rs_num, rs_den, u);
+        hipLaunchKernelGGL(k_update<128>, dim3(s.BH), dim3(kBlock), 0, st, L, s.C, s.N, a, src_kv,
+                           relayout, dense_seg_bytes, dense_cap, recent_len, rs_num, rs_den, u);
     else
-        hipLaunchKernelGGL(k_update<64>, dim3(s.BH), dim3(kBlock), 0, (hipStream_t)stream, L,
-                           s.C, s.N, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
-                           rs_num, rs_den, u);
+        hipLaunchKernelGGL(k_update<64>, dim3(s.BH), dim3(kBlock), 0, st, L, s.C, s.N, a, src_kv,
+                           relayout, dense_seg_bytes, dense_cap, recent_len, rs_num, rs_den, u);
     return last_error();
 }
 
-int launch_decode(const LayerDev& L, const Shape& s, const uint16_t* q, float* out,
-                  float* partials, int uniform_active, int n_items, void* stream) {
-    const float qscale = (float)(1.4426950408889634 / std::sqrt((double)s.d));
-    const int grid = uniform_active > 0 ? s.BH * uniform_active : n_items;
-    if (grid <= 0) return 0;
-    if (s.d == 128)
-        hipLaunchKernelGGL(k_decode<128>, dim3(grid), dim3(kBlock), 0, (hipStream_t)stream, L,
-                           s.C, q, out, partials, qscale, uniform_active);
+template <int D>
+static void attn_dispatch(const LayerDev& L, const Shape& s, const AppendArgs& a,
+                          const uint16_t* q, float* out, float* partials, int splits,
+                          hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+    const float qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
+    const dim3 grid(s.BH * splits), block(kAttnThreads);
+    // the longest-first order only matters when the blocks take more than one round
+    const int use_order = s.BH * splits > kCus ? 1 : 0;
+    // with events, they take the kernel's own start and end timestamps
+    if (a.k != nullptr)
+        hipExtLaunchKernelGGL((k_attn<D, true>), grid, block, 0, st, ev0, ev1, 0, L, s.C, a, q,
+                              out, partials, splits, use_order, qscale);
     else
-        hipLaunchKernelGGL(k_decode<64>, dim3(grid), dim3(kBlock), 0, (hipStream_t)stream, L, s.C,
-                           q, out, partials, qscale, uniform_active);
+        hipExtLaunchKernelGGL((k_attn<D, false>), grid, block, 0, st, ev0, ev1, 0, L, s.C, a, q,
+                              out, partials, splits, use_order, qscale);
+    if (splits > 1)
+        hipLaunchKernelGGL(k_merge<D>, dim3(s.BH), dim3(D), 0, st, out, partials, splits);
+}
+
+int launch_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
+                float* out, float* partials, int splits, void* stream, void* ev_start,
+                void* ev_stop) {
+    hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
+    if (s.d == 128)
+        attn_dispatch<128>(L, s, a, q, out, partials, splits, (hipStream_t)stream, e0, e1);
+    else
+        attn_dispatch<64>(L, s, a, q, out, partials, splits, (hipStream_t)stream, e0, e1);
     return last_error();
 }
 

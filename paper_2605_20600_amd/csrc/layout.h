@@ -16,9 +16,11 @@
 
 namespace headkv {
 
-constexpr int kChunk = 64;          // tokens per decode work item
 constexpr int kBlock = 256;         // threads per block of the cache kernels
-constexpr int kXcds = 8;            // MI355X: 8 accelerator complex dies
+constexpr int kAttnThreads = 1024;  // threads per attention block (one head or split)
+constexpr int kAttnTpr = 8;         // tokens per 16-lane row per attention pass
+constexpr int kMaxSplits = 8;       // attention splits per head (layers with few heads)
+constexpr int kCus = 256;           // MI355X compute units
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -27,11 +29,9 @@ inline size_t segment_bytes(int C, int cap, int d) {
 }
 
 struct MetaLayout {
-    size_t seg_off, cap, n, budget, nstar, label, counter, chunk_base, qsum, work, total;
-    int max_items;
+    size_t seg_off, cap, n, budget, nstar, label, order, qsum, total;
 
-    void compute(int BH, int d, int max_items_) {
-        max_items = max_items_;
+    void compute(int BH, int d) {
         size_t o = 0;
         auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
         seg_off = take(sizeof(int64_t) * BH);
@@ -40,10 +40,8 @@ struct MetaLayout {
         budget = take(sizeof(int32_t) * BH);
         nstar = take(sizeof(int32_t) * BH);
         label = take(sizeof(int32_t) * BH);
-        counter = take(sizeof(uint32_t) * BH);
-        chunk_base = take(sizeof(int32_t) * BH);
+        order = take(sizeof(int32_t) * BH);
         qsum = take(sizeof(double) * (size_t)BH * d);
-        work = take(sizeof(int32_t) * 2 * (size_t)max_items);
         total = o;
     }
 };
@@ -57,10 +55,8 @@ struct LayerDev {
     int32_t* budget;      // visual-token budget (after grouping)
     int32_t* nstar;       // n* from grouping
     int32_t* label;       // 1 = local head
-    uint32_t* counter;    // split-K arrival counters, zero between launches
-    int32_t* chunk_base;  // first partial slot of each head
+    int32_t* order;       // attention dispatch order of the heads (longest first)
     double* qsum;         // [BH][d] running sum of the queries of this window
-    int32_t* work;        // [max_items][2] (head, chunk) work items, head < 0 = idle
 };
 
 inline LayerDev make_layer_dev(void* kv, void* meta, const MetaLayout& m) {
@@ -73,10 +69,8 @@ inline LayerDev make_layer_dev(void* kv, void* meta, const MetaLayout& m) {
     L.budget = reinterpret_cast<int32_t*>(b + m.budget);
     L.nstar = reinterpret_cast<int32_t*>(b + m.nstar);
     L.label = reinterpret_cast<int32_t*>(b + m.label);
-    L.counter = reinterpret_cast<uint32_t*>(b + m.counter);
-    L.chunk_base = reinterpret_cast<int32_t*>(b + m.chunk_base);
+    L.order = reinterpret_cast<int32_t*>(b + m.order);
     L.qsum = reinterpret_cast<double*>(b + m.qsum);
-    L.work = reinterpret_cast<int32_t*>(b + m.work);
     return L;
 }
 
@@ -85,21 +79,35 @@ struct Shape {
     int BH, B, H, d, C, N;
 };
 
+// The token appended by a step (fused into the kernel that consumes it).
+struct AppendArgs {
+    const uint16_t* q;   // [BH][d] bf16
+    const uint16_t* k;
+    const uint16_t* v;
+    int step;            // visual position of the token
+    int accumulate;      // add q to the head's query sum
+    int reset;           // the query sum restarts with this q
+};
+
 int launch_prefill(const LayerDev& L, const Shape& s, const uint16_t* kc, const uint16_t* vc,
-                   int64_t dense_seg_bytes, int dense_cap, int dense_cph, void* stream);
-int launch_append(const LayerDev& L, const Shape& s, const uint16_t* q, const uint16_t* k,
-                  const uint16_t* v, int step, int accumulate, int reset, void* stream);
+                   int64_t dense_seg_bytes, int dense_cap, void* stream);
+int launch_append(const LayerDev& L, const Shape& s, const AppendArgs& a, void* stream);
 int launch_score(const LayerDev& L, const Shape& s, const uint16_t* q, int32_t* n_star,
                  uint8_t* is_local, int len, double sqrt_d, double tau, int local_window,
                  void* stream);
 int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
                    const int32_t* override_b, int32_t* budgets, int mode, int row_len,
                    int recent_len, int rho_num, int rho_den, void* stream);
-int launch_update(const LayerDev& L, const Shape& s, const char* src_kv, int relayout,
-                  int64_t dense_seg_bytes, int dense_cap, int recent_len, int rs_num,
-                  int rs_den, int u, void* stream);
-int launch_decode(const LayerDev& L, const Shape& s, const uint16_t* q, float* out,
-                  float* partials, int uniform_active, int n_items, void* stream);
+// a.k == nullptr: no append.
+int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
+                  int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
+                  int rs_num, int rs_den, int u, void* stream);
+// a.k == nullptr: no append (only allowed with splits == 1 otherwise).
+// ev_start / ev_stop (hipEvent_t or nullptr) receive the attention kernel's
+// own start and end timestamps.
+int launch_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
+                float* out, float* partials, int splits, void* stream,
+                void* ev_start = nullptr, void* ev_stop = nullptr);
 int launch_export(const LayerDev& L, const Shape& s, uint8_t* mask, int32_t* count,
                   void* stream);
 

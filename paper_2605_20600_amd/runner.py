@@ -8,6 +8,7 @@ from typing import Dict, Iterable, List, Optional
 
 import torch
 
+from . import binding as B
 from . import synth
 from .session import Session, make_config
 from .workloads import Workload
@@ -47,12 +48,15 @@ def run_generation(sess: Session, inp: DeviceInputs, out_steps: Iterable[int] = 
                    snap_steps: Iterable[int] = (), steps: Optional[int] = None,
                    outs: Optional[Dict[int, torch.Tensor]] = None,
                    label_override: Optional[Dict[int, torch.Tensor]] = None,
-                   decode_hook=None, record_layers: Optional[Iterable[int]] = None) -> Dict:
+                   decode_hook=None, record_layers: Optional[Iterable[int]] = None,
+                   fused: bool = True) -> Dict:
     """Runs steps 0..steps-1 (default N) of every layer in `inp.layers`.
 
     Returns {"out": {(t, l): fp32 [B][H][d]}, "snap": {(t, l): (mask, count)},
     "n_star"/"is_local"/"budgets": {l: tensor}} for the requested steps.
-    decode_hook(t, l, launch) may wrap the attention launch (timing)."""
+    decode_hook(t, l, launch) may wrap the attention launch (timing).
+    fused: use headkv_decode_step (append + update + attention in the fewest
+    launches) on every step but the grouping step; else the separate calls."""
     wl = inp.wl
     N = wl.num_visual if steps is None else steps
     t_g = wl.group_threshold - 1
@@ -66,19 +70,23 @@ def run_generation(sess: Session, inp: DeviceInputs, out_steps: Iterable[int] = 
         sess.prefill(l, inp.kc[l], inp.vc[l])
     for t in range(N):
         for l in inp.layers:
-            q = inp.q[l][t]
-            sess.append_and_evict(l, t, q, inp.k[l][t], inp.v[l][t])
-            if t == t_g:
-                n_star, is_local = sess.score_heads(l, q)
-                lab = None if label_override is None else label_override[l]
-                sess.assign_budgets(l, is_local=lab, override=inp.override[l])
-                res["n_star"][l] = n_star.clone()
-                res["is_local"][l] = (is_local if lab is None else lab).clone()
-                res["budgets"][l] = sess.budgets[l].clone()
-            if decode_hook is None:
-                sess.decode_attn(l, q, outs[l])
+            q, k, v = inp.q[l][t], inp.k[l][t], inp.v[l][t]
+            if fused and t != t_g:
+                launch = (lambda: sess.decode_step(l, t, q, k, v, outs[l]))
             else:
-                decode_hook(t, l, lambda: sess.decode_attn(l, q, outs[l]))
+                sess.append_and_evict(l, t, q, k, v)
+                if t == t_g:
+                    n_star, is_local = sess.score_heads(l, q)
+                    lab = None if label_override is None else label_override[l]
+                    sess.assign_budgets(l, is_local=lab, override=inp.override[l])
+                    res["n_star"][l] = n_star.clone()
+                    res["is_local"][l] = (is_local if lab is None else lab).clone()
+                    res["budgets"][l] = sess.budgets[l].clone()
+                launch = (lambda: sess.decode_attn(l, q, outs[l]))
+            if decode_hook is None:
+                launch()
+            else:
+                decode_hook(t, l, launch)
             if t in out_steps and l in rec:
                 res["out"][(t, l)] = outs[l].clone()
             if t in snap_steps and l in rec:
@@ -88,3 +96,35 @@ def run_generation(sess: Session, inp: DeviceInputs, out_steps: Iterable[int] = 
 
 def new_session(wl: Workload, layers: Optional[int] = None, **kw) -> Session:
     return Session(make_config(wl, layers=layers, **kw))
+
+
+def run_generation_native(sess: Session, inp: DeviceInputs, outs: Dict[int, torch.Tensor],
+                          timing_every: int = 0) -> Dict:
+    """The same generation with the step loop in the library (headkv_run_steps):
+    steps before and after the grouping step run from one host call each; the
+    grouping step uses the separate calls.  Needs the inputs of every layer of
+    the handle.  Returns labels, n* and budgets per layer."""
+    wl = inp.wl
+    L = sess.cfg.num_layers
+    assert inp.layers == list(range(L)), "the native loop runs every layer"
+    t_g = wl.group_threshold - 1
+    N = wl.num_visual
+    stride = wl.batch * wl.heads * wl.head_dim
+    qp = [inp.q[l].data_ptr() for l in range(L)]
+    kp = [inp.k[l].data_ptr() for l in range(L)]
+    vp = [inp.v[l].data_ptr() for l in range(L)]
+    op = [outs[l].data_ptr() for l in range(L)]
+    st = sess.stream()
+    res = {"n_star": {}, "is_local": {}, "budgets": {}}
+    for l in range(L):
+        sess.prefill(l, inp.kc[l], inp.vc[l])
+    B.headkv_run_steps(sess.h, 0, t_g, qp, kp, vp, stride, op, timing_every, st)
+    for l in range(L):
+        q = inp.q[l][t_g]
+        sess.append_and_evict(l, t_g, q, inp.k[l][t_g], inp.v[l][t_g])
+        n_star, is_local = sess.score_heads(l, q)
+        sess.assign_budgets(l, override=inp.override[l])
+        sess.decode_attn(l, q, outs[l])
+        res["n_star"][l], res["is_local"][l], res["budgets"][l] = n_star, is_local, sess.budgets[l]
+    B.headkv_run_steps(sess.h, t_g + 1, N, qp, kp, vp, stride, op, timing_every, st)
+    return res

@@ -106,6 +106,14 @@ class Session:
         B.headkv_decode_attn(self.h, layer, q.data_ptr(), out.data_ptr(), self.stream())
         return out
 
+    def decode_step(self, layer: int, step: int, q, k, v,
+                    out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=self.device)
+        B.headkv_decode_step(self.h, layer, step, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                             out.data_ptr(), self.stream())
+        return out
+
     def export_retained(self, layer: int) -> Tuple[torch.Tensor, torch.Tensor]:
         BH = self.cfg.batch * self.cfg.num_heads
         mask = torch.empty((BH, self.cfg.num_visual), dtype=torch.uint8, device=self.device)

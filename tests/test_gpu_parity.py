@@ -2,14 +2,17 @@
 
 Bar: labels, n*, budgets and retained position sets bit-exact; attention
 outputs within max-abs 2e-2 of the fp64 oracle (bf16 storage, fp32
-accumulation)."""
+accumulation).  Full-shape workloads are checked on sampled (layer, batch row)
+slices, every head of a slice, at sampled steps that include the grouping step
+and update steps; labels, n* and budgets on every head of the layers run."""
 import numpy as np
 import pytest
 import torch
 
 import oracle
 from paper_2605_20600_amd import synth, workloads as W
-from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation
+from paper_2605_20600_amd.runner import (DeviceInputs, new_session, run_generation,
+                                         run_generation_native)
 
 pytestmark = pytest.mark.gpu
 ATOL = 2e-2
@@ -19,12 +22,11 @@ def _say(*a):
     print(*a, flush=True)
 
 
-def _check_slice(wl, res, layer, b, steps, ref=None, heads=None):
+def _check_slice(wl, res, layer, b, steps, ref=None):
     """Compares one (layer, b) slice of a GPU run with the oracle."""
     H = wl.heads
-    heads = list(range(H)) if heads is None else heads
     if ref is None:
-        ref = oracle.simulate(wl, layer, b, heads=heads, snap_steps=steps)
+        ref = oracle.simulate(wl, layer, b, snap_steps=steps)
     sl = slice(b * H, (b + 1) * H)
     assert np.array_equal(res["is_local"][layer][sl].cpu().numpy(), ref["labels"]), "labels"
     assert np.array_equal(res["n_star"][layer][sl].cpu().numpy(), ref["n_star"]), "n_star"
@@ -33,15 +35,44 @@ def _check_slice(wl, res, layer, b, steps, ref=None, heads=None):
     for i, t in enumerate(steps):
         mask, count = res["snap"][(t, layer)]
         mask = mask[sl].cpu().numpy()
+        count = count[sl].cpu().numpy()
         out = res["out"][(t, layer)][b].cpu().double().numpy()
-        for h in heads:
+        for h in range(H):
             exp_mask = ref["snaps"][h][i]
             assert np.array_equal(mask[h], exp_mask), (layer, b, h, t)
-            assert int(count[b * H + h]) == int(exp_mask.sum())
+            assert int(count[h]) == int(exp_mask.sum())
             err = float(np.abs(out[h] - ref["out"][h][t]).max())
             worst = max(worst, err)
             assert err <= ATOL, (layer, b, h, t, err)
     return worst, ref
+
+
+def _steps(wl, extra=()):
+    t_g, P, N = wl.group_threshold - 1, wl.period, wl.num_visual
+    s = {0, 1, t_g - 1, t_g, t_g + 1, t_g + P - 1, t_g + P, t_g + P + 1, N // 2, N - 2, N - 1}
+    return sorted(x for x in s.union(extra) if 0 <= x < N)
+
+
+def _run_and_check(wl, layers, slices, steps, fused=True, all_heads=True):
+    inp = DeviceInputs(wl, layers=layers)
+    sess = new_session(wl)
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps, fused=fused,
+                         record_layers=sorted({l for l, _ in slices}))
+    torch.cuda.synchronize()
+    for (layer, b) in slices:
+        worst, ref = _check_slice(wl, res, layer, b, steps)
+        gaps = [st["min_gap"] for st in ref["stats"].values()]
+        _say(f"{wl.name} rho={wl.rho} fused={fused} layer {layer} b {b}: bit-exact; "
+             f"max err {worst:.2e}; min label margin "
+             f"{np.abs(ref['mass_window'] - wl.tau).min():.2e}; min eviction score gap "
+             f"{min(gaps):.2e}")
+    if all_heads:
+        for layer in layers:
+            g = oracle.group_layer(wl, layer)
+            assert np.array_equal(res["is_local"][layer].cpu().numpy(), g["labels"].reshape(-1))
+            assert np.array_equal(res["n_star"][layer].cpu().numpy(), g["n_star"].reshape(-1))
+            assert np.array_equal(res["budgets"][layer].cpu().numpy(), g["budgets"].reshape(-1))
+    return res
 
 
 def test_generator_bitwise_cpu_gpu():
@@ -56,15 +87,16 @@ def test_generator_bitwise_cpu_gpu():
     assert all(torch.equal(x.cpu(), y) for x, y in zip(g, c))
 
 
-def test_tiny_full_generation_every_step():
+@pytest.mark.parametrize("fused", [True, False])
+def test_tiny_full_generation_every_step(fused):
     wl = W.TINY
     steps = list(range(wl.num_visual))
     inp = DeviceInputs(wl)
     sess = new_session(wl)
-    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps)
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps, fused=fused)
     torch.cuda.synchronize()
     worst, _ = _check_slice(wl, res, 0, 0, steps)
-    _say(f"tiny: every step bit-exact, max |out - oracle| = {worst:.3e}")
+    _say(f"tiny fused={fused}: every step bit-exact, max |out - oracle| = {worst:.3e}")
 
 
 @pytest.mark.parametrize("seed", [0, 1, 2])
@@ -97,28 +129,66 @@ def test_tiny_full_budget_is_full_attention():
             assert int(res["snap"][(t, 0)][1][h]) == t + 1
 
 
-def _lumina_steps(wl):
-    t_g, P, N = wl.group_threshold - 1, wl.period, wl.num_visual
-    return sorted({0, 1, 127, t_g - 1, t_g, t_g + 1, t_g + P - 1, t_g + P, t_g + P + 1,
-                   1000, N - 2, N - 1})
-
-
-@pytest.mark.parametrize("rho", [(1, 8), (1, 4)])
-def test_lumina768_two_layers_sampled(rho):
-    # full head count and batch, two of the 32 layers, every step of the generation
-    wl = W.LUMINA768.with_(rho=rho)
-    steps = _lumina_steps(wl)
-    inp = DeviceInputs(wl, layers=[0, 31])
+def test_tiny_linear_uniform_budgets():
+    # every head labelled global: the uniform-budget layout of the line-based
+    # baseline the paper compares against, through the same calls
+    wl = W.TINY
+    steps = list(range(wl.num_visual))
+    inp = DeviceInputs(wl)
     sess = new_session(wl)
-    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps)
+    lab = {0: torch.zeros(wl.heads, dtype=torch.uint8, device="cuda")}
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps, label_override=lab)
     torch.cuda.synchronize()
-    for (layer, b) in ((0, 0), (31, 7)):
-        worst, ref = _check_slice(wl, res, layer, b, steps)
-        _say(f"lumina768 rho={rho} layer {layer} b {b}: bit-exact, max err {worst:.3e}, "
-             f"label margin min {np.abs(ref['mass_window'] - wl.tau).min():.3e}")
-    # labels, n* and budgets of every head of both layers
-    for layer in (0, 31):
-        g = oracle.group_layer(wl, layer)
-        assert np.array_equal(res["is_local"][layer].cpu().numpy(), g["labels"].reshape(-1))
-        assert np.array_equal(res["n_star"][layer].cpu().numpy(), g["n_star"].reshape(-1))
-        assert np.array_equal(res["budgets"][layer].cpu().numpy(), g["budgets"].reshape(-1))
+    ref = oracle.simulate(wl, 0, 0, snap_steps=steps, label_override=[0] * wl.heads)
+    assert list(ref["budgets"]) == [wl.num_visual * wl.rho[0] // wl.rho[1]] * wl.heads
+    _check_slice(wl, res, 0, 0, steps, ref=ref)
+
+
+@pytest.mark.parametrize("rho", [(1, 8), (1, 6), (1, 4)])
+def test_lumina768_sampled(rho):
+    wl = W.LUMINA768.with_(rho=rho)
+    _run_and_check(wl, [0, 31], [(0, 0), (31, 7)], _steps(wl, extra=(127, 1000)))
+
+
+def test_lumina768_separate_calls():
+    wl = W.LUMINA768
+    _run_and_check(wl, [5], [(5, 3)], _steps(wl), fused=False, all_heads=False)
+
+
+def test_janus7b_total_budget_sampled():
+    wl = W.JANUS7B
+    _run_and_check(wl, [0, 29], [(0, 0), (29, 15)], _steps(wl, extra=(200, 400)))
+
+
+def test_lumina1024_override_split_heads():
+    # 4 x 32 = 128 heads per layer < 256 compute units: each head is split over
+    # several blocks and merged
+    wl = W.LUMINA1024
+    _run_and_check(wl, [0, 31], [(0, 0), (31, 3)], _steps(wl, extra=(2000, 3000)))
+
+
+def test_stress_update_every_step():
+    wl = W.STRESS
+    _run_and_check(wl, [0], [(0, 0), (0, 63)], _steps(wl, extra=(310, 1500)))
+
+
+@pytest.mark.parametrize("wl", [W.TINY, W.LUMINA768.with_(layers=2)], ids=["tiny", "lumina2"])
+def test_native_step_loop(wl):
+    # the library's own step loop gives the same final state as the oracle
+    inp = DeviceInputs(wl)
+    sess = new_session(wl)
+    outs = {l: torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32, device="cuda")
+            for l in range(wl.layers)}
+    res = run_generation_native(sess, inp, outs)
+    N = wl.num_visual
+    for l in range(wl.layers):
+        mask, count = sess.export_retained(l)
+        torch.cuda.synchronize()
+        ref = oracle.simulate(wl, l, 0, snap_steps=[N - 1])
+        H = wl.heads
+        assert np.array_equal(res["is_local"][l][:H].cpu().numpy(), ref["labels"])
+        assert np.array_equal(res["budgets"][l][:H].cpu().numpy(), ref["budgets"])
+        out = outs[l][0].cpu().double().numpy()
+        for h in range(H):
+            assert np.array_equal(mask[h].cpu().numpy(), ref["snaps"][h][0]), (l, h)
+            assert np.abs(out[h] - ref["out"][h][N - 1]).max() <= ATOL
