@@ -40,7 +40,25 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--timing-every", type=int, default=4,
                    help="time the attention launch of every n-th step")
+    p.add_argument("--copy-probe", action="store_true",
+                   help="only run a plain 512 MiB device copy five times (calibrates the HBM "
+                        "byte counters of a profiler run) and exit")
     return p.parse_args()
+
+
+def measured_traffic():
+    """HBM bytes per dispatch of the attention kernel from the profiler's byte
+    counters (profiles/), or None once the kernel source differs from the one
+    the counters were taken with."""
+    import hashlib
+    rec_path = os.path.join(ROOT, "profiles", "k_attn_lumina768_b8_rho1-8_traffic.json")
+    src = os.path.join(ROOT, "paper_2605_20600_amd", "csrc", "kernels.hip")
+    try:
+        rec = json.load(open(rec_path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    return rec["traffic_bytes_per_dispatch"] if rec.get("kernels_hip_sha256") == sha else None
 
 
 def cpu_baseline(wl, seconds_target: float):
@@ -102,6 +120,14 @@ def main():
               "shards by batch row or head with no communication, see DESIGN.md", file=sys.stderr)
         sys.exit(2)
     import torch
+    if args.copy_probe:
+        src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print("# copy probe: 5 copies of 536870912 bytes", file=sys.stderr, flush=True)
+        return
     from paper_2605_20600_amd import workloads as W
     from paper_2605_20600_amd import binding as B
     from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation_native
@@ -179,7 +205,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": None,
+            "traffic": measured_traffic() if args.rho == "1/8" else None,
             "kernel": "k_attn<128, append> (headkv_decode_step)",
             "timed_every_nth_step": args.timing_every,
             "launches": n_launch,
