@@ -38,7 +38,7 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="approximate CPU work of the oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--timing-every", type=int, default=4,
+    p.add_argument("--timing-every", type=int, default=16,
                    help="time the attention launch of every n-th step")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 512 MiB device copy five times (calibrates the HBM "

@@ -140,7 +140,7 @@ def run_head(q, k, v, kc, vc, t_g: int, P: int, is_local: bool, budget: int,
 
 def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
              want_out: bool = True, snap_steps: Sequence[int] = (),
-             seed: Optional[int] = None, label_override=None) -> Dict:
+             seed: Optional[int] = None, label_override=None, budget_override=None) -> Dict:
     """The whole compressed decode of one (layer, b) slice of a workload.
 
     Grouping runs for every head of the slice (budgets of the layer-total mode
@@ -165,9 +165,13 @@ def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
                                                      g["margin"], g["mass_window"])
     if label_override is not None:
         labels = np.asarray(label_override, dtype=np.int32)
-    ov = synth.budget_override(wl)
+    if budget_override is not None:
+        ov_slice = np.asarray(budget_override, dtype=np.int32)
+    else:
+        ov = synth.budget_override(wl)
+        ov_slice = None if ov is None else ov[layer, b]
     bud = budgets(wl.budget_mode, labels, wl.num_visual, wl.row_len, wl.recent_len,
-                  wl.rho, None if ov is None else ov[layer, b])
+                  wl.rho, ov_slice)
     res = {"labels": labels, "n_star": n_star, "margin": margins, "mass_window": mass,
            "budgets": bud, "out": {}, "snaps": {}, "stats": {}}
     def one(h):

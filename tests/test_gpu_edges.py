@@ -1,0 +1,96 @@
+"""Edge cases of the decode path on small synthetic workloads, every step of
+the generation checked against the oracle (bit-exact retained sets, labels, n*
+and budgets; attention within 2e-2)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2605_20600_amd import workloads as W
+from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation
+
+pytestmark = pytest.mark.gpu
+ATOL = 2e-2
+
+
+def _run(wl, layer=0, slices=((0, 0),), budgets=None, fused=True, steps=None, **cfg):
+    steps = list(range(wl.num_visual)) if steps is None else steps
+    inp = DeviceInputs(wl, layers=[layer])
+    if budgets is not None:
+        inp.override[layer] = torch.as_tensor(np.asarray(budgets, dtype=np.int32).reshape(-1),
+                                              device="cuda")
+    sess = new_session(wl, **cfg)
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps, fused=fused)
+    torch.cuda.synchronize()
+    H = wl.heads
+    worst = 0.0
+    for (_, b) in slices:
+        ov = None if budgets is None else np.asarray(budgets).reshape(wl.batch, H)[b]
+        ref = oracle.simulate(wl, layer, b, snap_steps=steps, budget_override=ov)
+        sl = slice(b * H, (b + 1) * H)
+        assert np.array_equal(res["is_local"][layer][sl].cpu().numpy(), ref["labels"])
+        assert np.array_equal(res["n_star"][layer][sl].cpu().numpy(), ref["n_star"])
+        assert np.array_equal(res["budgets"][layer][sl].cpu().numpy(), ref["budgets"])
+        for i, t in enumerate(steps):
+            mask = res["snap"][(t, layer)][0][sl].cpu().numpy()
+            out = res["out"][(t, layer)][b].cpu().double().numpy()
+            for h in range(H):
+                assert np.array_equal(mask[h], ref["snaps"][h][i]), (b, h, t)
+                err = float(np.abs(out[h] - ref["out"][h][t]).max())
+                worst = max(worst, err)
+                assert err <= ATOL, (b, h, t, err)
+    return res, worst
+
+
+def test_no_prefix():
+    _run(W.TINY.with_(prefix_len=0))
+
+
+def test_budgets_below_recent_window():
+    wl = W.TINY.with_(budget_mode=W.BUDGET_OVERRIDE)
+    _run(wl, budgets=[[5, 1, 7, 31]])
+
+
+def test_update_every_step():
+    _run(W.TINY.with_(period=1))
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_period_not_dividing_rows(fused):
+    _run(W.TINY.with_(period=7, group_threshold=50), fused=fused)
+
+
+@pytest.mark.parametrize("r_s", [(0, 1), (1, 1), (3, 10), (4, 5)])
+def test_stratification_ratio(r_s):
+    _run(W.TINY.with_(r_s=r_s), r_s=r_s)
+
+
+@pytest.mark.parametrize("tau", [0.85, 0.95, 1.0])
+def test_grouping_threshold_tau(tau):
+    _run(W.TINY.with_(tau=tau), tau=tau)
+
+
+@pytest.mark.parametrize("thr", [1, 2, 256])
+def test_grouping_at_first_and_last_steps(thr):
+    _run(W.TINY.with_(group_threshold=thr))
+
+
+def test_row_end_tokens_odd_grid():
+    wl = W.TINY.with_(grid_rows=11, grid_cols=13, row_end=True, period=14, group_threshold=40,
+                      heads=6, batch=2)
+    _run(wl, slices=((0, 0), (0, 1)))
+
+
+def test_many_heads_dispatch_order_d64():
+    # 8 x 40 = 320 heads per layer: more attention blocks than compute units
+    wl = W.TINY.with_(batch=8, heads=40, budget_mode=W.BUDGET_OVERRIDE)
+    rng = np.random.default_rng(5)
+    bud = rng.integers(1, 257, size=(8, 40))
+    _run(wl, budgets=bud, slices=((0, 0), (0, 7)), steps=[0, 63, 64, 65, 100, 200, 255])
+
+
+def test_few_long_heads_split_d64():
+    # 1 x 2 heads of up to 1024 tokens: each head split over several blocks
+    wl = W.TINY.with_(heads=2, grid_rows=32, grid_cols=32, period=32, group_threshold=600,
+                      budget_mode=W.BUDGET_OVERRIDE)
+    _run(wl, budgets=[[1000, 900]], steps=[0, 300, 599, 600, 601, 800, 1023])
