@@ -34,7 +34,10 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=3)
     p.add_argument("--warmup", type=int, default=1)
-    p.add_argument("--rho", default="1/8")
+    p.add_argument("--rho", default=None, help="budget ratio, e.g. 1/6 (default: the workload's)")
+    p.add_argument("--workload", default="lumina_mgpt_768",
+                   help="lumina_mgpt_768 (default), janus_pro_7b, lumina_mgpt_1024, "
+                        "stress_768_b64_p1 or tiny")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="approximate CPU work of the oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -62,8 +65,9 @@ def measured_traffic():
 
 
 def cpu_baseline(wl, seconds_target: float):
-    """The fp64 oracle through whole generations of a sample of heads, one head
-    per host thread (the C code runs without the GIL)."""
+    """The fp64 oracle through grouping, budgets and whole generations of
+    sampled (layer, batch row) slices, one head per host thread (the C code
+    runs without the GIL).  Inputs are generated before timing."""
     import numpy as np
     import torch
     import oracle
@@ -71,45 +75,45 @@ def cpu_baseline(wl, seconds_target: float):
 
     threads = min(16, os.cpu_count() or 1)
     t_g = wl.group_threshold - 1
-    # calibrate on one head: grouping + the whole generation
-    q, k, v, kc, vc = synth.head_inputs(wl, 0, 0, 0)
-    t0 = time.perf_counter()
-    oracle.group_head(q[t_g], torch.cat([kc, k[: t_g + 1]]), wl.tau, wl.local_window)
-    oracle.run_head(q, k, v, kc, vc, t_g, wl.period, False,
-                    wl.num_visual * wl.rho[0] // wl.rho[1], wl.recent_len)
-    per_head = time.perf_counter() - t0
-    n_heads = max(threads, int(round(seconds_target / per_head / threads)) * threads)
-    heads = [(l % wl.layers, (l // wl.layers) % wl.batch, (7 * l) % wl.heads) for l in range(n_heads)]
-    inputs = [synth.head_inputs(wl, *x) for x in heads]
-    amp = synth.amplitudes(wl)
-    budgets = {True: wl.recent_len, False: wl.num_visual * wl.rho[0] // wl.rho[1]}
-    lock = threading.Lock()
-    todo = list(range(n_heads))
+    ov = synth.budget_override(wl)
 
-    def work():
-        while True:
-            with lock:
-                if not todo:
-                    return
-                i = todo.pop()
-            q, k, v, kc, vc = inputs[i]
+    def prepare(layer, b):
+        return [synth.head_inputs(wl, layer, b, h) for h in range(wl.heads)]
+
+    def run_slice(layer, b, inputs, pool):
+        labels = []
+        for (q, k, v, kc, vc) in inputs:
             g = oracle.group_head(q[t_g], torch.cat([kc, k[: t_g + 1]]), wl.tau, wl.local_window)
-            loc = bool(g["is_local"])
-            oracle.run_head(q, k, v, kc, vc, t_g, wl.period, loc, budgets[loc], wl.recent_len)
+            labels.append(g["is_local"])
+        bud = oracle.budgets(wl.budget_mode, labels, wl.num_visual, wl.row_len, wl.recent_len,
+                             wl.rho, None if ov is None else ov[layer, b])
 
-    t0 = time.perf_counter()
-    ths = [threading.Thread(target=work) for _ in range(threads)]
-    for th in ths:
-        th.start()
-    for th in ths:
-        th.join()
-    wall = time.perf_counter() - t0
+        def one(h):
+            q, k, v, kc, vc = inputs[h]
+            oracle.run_head(q, k, v, kc, vc, t_g, wl.period, bool(labels[h]), int(bud[h]),
+                            wl.recent_len, wl.r_s)
+        list(pool.map(one, range(wl.heads)))
+
+    from concurrent.futures import ThreadPoolExecutor
+    slices = [((7 * i) % wl.layers, (3 * i) % wl.batch) for i in range(wl.layers * wl.batch)]
+    with ThreadPoolExecutor(max_workers=threads) as pool:
+        first = prepare(*slices[0])
+        t0 = time.perf_counter()
+        run_slice(*slices[0], first, pool)
+        per_slice = time.perf_counter() - t0
+        # seconds_target is CPU time: wall per slice x threads busy
+        n_slices = max(1, min(len(slices), int(seconds_target / max(per_slice * threads, 1e-9))))
+        prepared = [first] + [prepare(*x) for x in slices[1:n_slices]]
+        t0 = time.perf_counter()
+        for x, inp in zip(slices[:n_slices], prepared):
+            run_slice(*x, inp, pool)
+        wall = time.perf_counter() - t0
+    heads = n_slices * wl.heads
     # a visual token of the workload = one step of all layers x heads of one batch row
-    tokens = n_heads * wl.num_visual / (wl.layers * wl.heads)
-    local = sum(int(amp[l, b, h] == 3.0) for (l, b, h) in heads)
+    tokens = heads * wl.num_visual / (wl.layers * wl.heads)
     return {"value": tokens / wall, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": (f"{n_heads} (layer, batch, head) heads ({local} planted local) through "
-                       f"grouping + all {wl.num_visual} steps, fp64, {wall:.2f} s wall on "
+            "sample": (f"{n_slices} (layer, batch row) slices = {heads} heads through grouping, "
+                       f"budgets and all {wl.num_visual} steps, fp64, {wall:.2f} s wall on "
                        f"{threads} threads; scaled to all {wl.layers}x{wl.heads} heads per token")}
 
 
@@ -132,8 +136,10 @@ def main():
     from paper_2605_20600_amd import binding as B
     from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation_native
 
-    rho = tuple(int(x) for x in args.rho.split("/"))
-    wl = W.LUMINA768.with_(rho=rho)
+    wl = W.ALL[args.workload]
+    if args.rho is not None:
+        wl = wl.with_(rho=tuple(int(x) for x in args.rho.split("/")))
+    rho_s = f"{wl.rho[0]}/{wl.rho[1]}"
     dev = torch.cuda.current_device()
     torch.cuda.set_device(dev)
     t0 = time.perf_counter()
@@ -153,7 +159,7 @@ def main():
     # timed region: K whole generations, the step loop in the library.  Every
     # `timing_every`-th step's fused append + attention launch (one kernel) is
     # timed with HIP events that take the kernel's own start and end.
-    per_gen = (wl.num_visual + args.timing_every - 1) // args.timing_every * wl.layers
+    per_gen = (wl.num_visual + args.timing_every - 1) // args.timing_every * wl.layers * 2
     B.headkv_timing_reserve(sess.h, per_gen * args.steps)
     B.headkv_timing_collect(sess.h)              # discard warm-up records
     torch.cuda.synchronize()
@@ -163,14 +169,29 @@ def main():
         print(f"# step {i + 1}/{args.steps} issued", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
-    kern_ms, n_launch, bytes_sum, dropped = B.headkv_timing_collect(sess.h)
-    avg_us = kern_ms / n_launch * 1e3
-    avg_bytes = bytes_sum / n_launch
-    achieved = avg_bytes / (avg_us * 1e-6) / 1e9
+    per_kind, dropped = B.headkv_timing_collect(sess.h)
+    names = ["k_attn<d, append> (headkv_decode_step)", "k_attn<d> (after an update)",
+             "k_update<d> (append + periodic update)"]
+    kinds = {}
+    for name, (kms, kn, kb) in zip(names, per_kind):
+        if kn:
+            kinds[name] = {"launches": kn, "avg_us": kms / kn * 1e3, "alg_bytes_per_launch": kb / kn,
+                           "achieved_gbps": kb / kn / (kms / kn * 1e-3) / 1e9,
+                           "share_of_timed_ms": kms}
+    total_ms = sum(v["share_of_timed_ms"] for v in kinds.values())
+    for v in kinds.values():
+        v["share_of_timed_ms"] = v["share_of_timed_ms"] / total_ms
+    dominant = max(kinds, key=lambda k: kinds[k]["share_of_timed_ms"])
+    dom = kinds[dominant]
+    avg_us, avg_bytes, n_launch = dom["avg_us"], dom["alg_bytes_per_launch"], dom["launches"]
+    achieved = dom["achieved_gbps"]
     tokens = wl.batch * wl.num_visual * args.steps
     ms_per_step = elapsed / args.steps * 1e3
-    print(f"# attention: {n_launch} timed launches ({dropped} untimed), avg {avg_us:.2f} us, "
-          f"{avg_bytes / 1e6:.2f} MB algorithmic -> {achieved:.0f} GB/s", file=sys.stderr, flush=True)
+    for k, v in kinds.items():
+        print(f"# {k}: {v['launches']} timed launches, avg {v['avg_us']:.2f} us, "
+              f"{v['alg_bytes_per_launch'] / 1e6:.2f} MB algorithmic -> {v['achieved_gbps']:.0f} GB/s, "
+              f"{v['share_of_timed_ms']:.1%} of timed kernel time", file=sys.stderr, flush=True)
+    print(f"# {dropped} launches untimed", file=sys.stderr, flush=True)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -190,12 +211,15 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": "lumina_mgpt_768_shape",
-            "step": "one whole generation: prefill, 2352 visual steps x 32 layers of "
-                    "append/update + grouping at step 299 + decode attention",
+            "workload": wl.name + "_shape",
+            "step": (f"one whole generation: prefill, {wl.num_visual} visual steps x "
+                     f"{wl.layers} layers of append/update + grouping at step "
+                     f"{wl.group_threshold - 1} + decode attention"),
             "batch": wl.batch, "layers": wl.layers, "heads": wl.heads,
             "head_dim": wl.head_dim, "prefix_tokens": wl.prefix_len,
-            "visual_tokens": wl.num_visual, "rho": args.rho, "period": wl.period,
+            "visual_tokens": wl.num_visual, "rho": rho_s,
+            "budget_mode": ["paper", "override", "layer_total"][wl.budget_mode],
+            "period": wl.period,
             "group_threshold": wl.group_threshold, "recent_window": wl.recent_len,
             "kv_storage": "bf16", "accumulate": "fp32 (attention), fp64 (grouping, eviction)",
         },
@@ -205,14 +229,16 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": measured_traffic() if args.rho == "1/8" else None,
-            "kernel": "k_attn<128, append> (headkv_decode_step)",
+            "traffic": (measured_traffic() if wl.name == "lumina_mgpt_768" and rho_s == "1/8"
+                        and dominant == names[0] else None),
+            "kernel": dominant.replace("<d", f"<{wl.head_dim}"),
             "timed_every_nth_step": args.timing_every,
             "launches": n_launch,
             "avg_launch_us": avg_us,
             "alg_bytes_per_launch": avg_bytes,
         },
         "cpu_baseline": cpu,
+        "kernels": {k.replace("<d", f"<{wl.head_dim}"): v for k, v in kinds.items()},
     }
     print(json.dumps(line), flush=True)
 

@@ -190,11 +190,19 @@ headkv_status headkv_run_steps(headkv_t h, int32_t step_begin, int32_t step_end,
 /* Creates events for `launches` timed attention launches (host call). */
 headkv_status headkv_timing_reserve(headkv_t h, int64_t launches);
 
-/* Waits for the timed launches since the last collect and returns the sum of
- * their kernel durations (ms), their number, the sum of their algorithmic HBM
- * bytes (K/V of every attended token, q, the output, the appended row, its
- * position and the query-sum update), and the number of launches that found
- * no free event. */
+/* Kinds of timed launches. */
+#define HEADKV_TIMED_ATTN_APPEND 0 /* fused append + attention (one kernel) */
+#define HEADKV_TIMED_ATTN 1        /* attention after an update or a split append */
+#define HEADKV_TIMED_UPDATE 2      /* append + periodic update */
+#define HEADKV_TIMED_KINDS 3
+
+/* Waits for the timed launches since the last collect and returns, per kind
+ * (arrays of HEADKV_TIMED_KINDS), the sum of their kernel durations (ms), their
+ * number and the sum of their algorithmic HBM bytes, plus the number of
+ * launches that found no free event.  Algorithmic bytes: K/V of every attended
+ * token, q and the output for attention; the appended row, its position and
+ * the query-sum update for the append; positions, the history keys of
+ * evicting global heads and at most M moved rows for the update. */
 headkv_status headkv_timing_collect(headkv_t h, double* kernel_ms, int64_t* launches,
                                     double* alg_bytes, int64_t* dropped);
 

@@ -77,8 +77,7 @@ def load() -> ctypes.CDLL:
         "headkv_export_retained": [P, I, P, P, P],
         "headkv_run_steps": [P, I, I, P, P, P, ctypes.c_int64, P, I, P],
         "headkv_timing_reserve": [P, ctypes.c_int64],
-        "headkv_timing_collect": [P, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64),
-                                  ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)],
+        "headkv_timing_collect": [P, P, P, P, ctypes.POINTER(ctypes.c_int64)],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -178,9 +177,13 @@ def headkv_timing_reserve(h: int, launches: int) -> None:
     _check(load().headkv_timing_reserve(h, launches), "headkv_timing_reserve")
 
 
-def headkv_timing_collect(h: int) -> Tuple[float, int, float, int]:
-    """Returns (kernel ms, launches, algorithmic bytes, dropped)."""
-    ms, n, b, dr = ctypes.c_double(), ctypes.c_int64(), ctypes.c_double(), ctypes.c_int64()
-    _check(load().headkv_timing_collect(h, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(b),
-                                        ctypes.byref(dr)), "headkv_timing_collect")
-    return ms.value, n.value, b.value, dr.value
+def headkv_timing_collect(h: int):
+    """Returns per kind (fused append + attention, attention, append + update)
+    a list of (kernel ms, launches, algorithmic bytes), and the dropped count."""
+    K = 3
+    ms = (ctypes.c_double * K)()
+    n = (ctypes.c_int64 * K)()
+    b = (ctypes.c_double * K)()
+    dr = ctypes.c_int64()
+    _check(load().headkv_timing_collect(h, ms, n, b, ctypes.byref(dr)), "headkv_timing_collect")
+    return [(ms[i], n[i], b[i]) for i in range(K)], dr.value

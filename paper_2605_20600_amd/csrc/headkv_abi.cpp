@@ -41,6 +41,7 @@ struct Layer {
     bool grouped = false;
     int last_step = -1;
     std::vector<int> n, budget, cap;
+    std::vector<uint8_t> label_local;  // labels used by the updates (host copy)
 };
 
 }  // namespace
@@ -55,9 +56,10 @@ struct headkv_ctx {
     size_t ws_bytes = 0;
     void* ws = nullptr;
     std::vector<Layer> layers;
-    // timing of single-kernel decode steps: event pairs and algorithmic bytes
+    // timing of sampled launches: event pairs, kind and algorithmic bytes
     std::vector<hipEvent_t> events;
     std::vector<double> timed_bytes;
+    std::vector<int> timed_kind;
     size_t timed = 0;
     int64_t timing_dropped = 0;
     ~headkv_ctx() {
@@ -208,6 +210,7 @@ headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c, con
     L.n.assign(h->shape.BH, 0);
     L.cap.assign(h->shape.BH, h->dense_cap);
     L.budget.assign(h->shape.BH, 0);
+    L.label_local.assign(h->shape.BH, 0);
     st = hip_status(launch_prefill(dev_of(h, L), h->shape, k_c, v_c, h->dense_seg, h->dense_cap,
                                    stream),
                     "prefill launch");
@@ -279,7 +282,7 @@ headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step, c
     LayerDev D = dev_of(h, L);
     if (update)
         st = hip_status(launch_update(D, h->shape, a, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
-                                      c.rs_den, u, stream),
+                                      c.rs_den, u, stream, nullptr, nullptr),
                         "append + update launch");
     else
         st = hip_status(launch_append(D, h->shape, a, stream), "append launch");
@@ -292,10 +295,11 @@ headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step, c
 
 namespace {
 
-// Algorithmic HBM bytes of one fused append + attention launch, from the host
-// mirror before the append: K and V of the prefix, the retained tokens and
-// the new token; q in, the output out; the new K/V row and its position
-// written; the fp64 query sum read and written when accumulating.
+// Algorithmic HBM bytes of the kernels of a decode step, from the host mirror
+// (n before the step's append).
+//   fused append + attention: K and V of the prefix, the retained tokens and
+//   the new token; q in, the output out; the new K/V row and its position
+//   written; the fp64 query sum read and written when accumulating.
 double fused_step_bytes(headkv_t h, const Layer& L, bool accumulate) {
     const headkv_config& c = h->cfg;
     const double d = c.head_dim;
@@ -303,6 +307,52 @@ double fused_step_bytes(headkv_t h, const Layer& L, bool accumulate) {
     for (int n : L.n) tokens += c.prefix_len + n + 1;
     const double per_head = d * 2 + d * 4 + 2 * d * 2 + 4 + (accumulate ? 2 * d * 8 : 0);
     return tokens * 2 * d * 2 + h->shape.BH * per_head;
+}
+
+//   attention alone (n after the step's update): K, V, q and the output.
+double attn_bytes(headkv_t h, const Layer& L) {
+    const headkv_config& c = h->cfg;
+    const double d = c.head_dim;
+    double tokens = 0;
+    for (int n : L.n) tokens += c.prefix_len + n;
+    return tokens * 2 * d * 2 + h->shape.BH * (d * 2 + d * 4);
+}
+
+//   append + periodic update: the append (q, k, v in; K/V row, position and
+//   query sum written); every head's positions; for a global head that evicts,
+//   the keys of its history and its query sum; and at most M K/V rows and
+//   positions moved by the compaction.
+double update_bytes(headkv_t h, const Layer& L) {
+    const headkv_config& c = h->cfg;
+    const double d = c.head_dim;
+    double b = 0;
+    for (int i = 0; i < h->shape.BH; ++i) {
+        const int n = L.n[i] + 1, B = L.budget[i];
+        const int w_eff = std::min(c.recent_len, B);
+        const int T = std::max(0, n - w_eff);
+        const int M = std::max(0, T - (B - w_eff));
+        b += 3 * 2 * d + 2 * 2 * d + 4 + 2 * 8 * d + 4.0 * n;
+        if (M > 0) {
+            if (!L.label_local[i]) b += T * 2 * d + 8 * d;
+            b += M * (2 * 2 * 2 * d + 8);
+        }
+    }
+    return b;
+}
+
+// Event pair for a sampled launch of `kind`, or nullptrs.
+void take_events(headkv_t h, bool time_it, int kind, double bytes, void** e0, void** e1) {
+    *e0 = *e1 = nullptr;
+    if (!time_it) return;
+    if (2 * (h->timed + 1) > h->events.size()) {
+        ++h->timing_dropped;
+        return;
+    }
+    *e0 = h->events[2 * h->timed];
+    *e1 = h->events[2 * h->timed + 1];
+    h->timed_bytes[h->timed] = bytes;
+    h->timed_kind[h->timed] = kind;
+    ++h->timed;
 }
 
 headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
@@ -323,33 +373,33 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
     AppendArgs none = a;
     none.k = none.v = none.q = nullptr;
     float* ws = static_cast<float*>(h->ws);
+    void *e0, *e1;
     if (update) {
+        take_events(h, time_it, HEADKV_TIMED_UPDATE, update_bytes(h, L), &e0, &e1);
         st = hip_status(launch_update(D, h->shape, a, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
-                                      c.rs_den, u, stream),
+                                      c.rs_den, u, stream, e0, e1),
                         "append + update launch");
-        if (!st) st = hip_status(launch_attn(D, h->shape, none, q, out, ws, splits, stream), "attention launch");
-    } else if (splits == 1) {
-        void* e0 = nullptr;
-        void* e1 = nullptr;
-        if (time_it) {
-            if (2 * (h->timed + 1) <= h->events.size()) {
-                e0 = h->events[2 * h->timed];
-                e1 = h->events[2 * h->timed + 1];
-                h->timed_bytes[h->timed] = fused_step_bytes(h, L, a.accumulate != 0);
-                ++h->timed;
-            } else {
-                ++h->timing_dropped;
-            }
-        }
+        if (st) return st;
+        commit_append(h, L, step, update);
+        take_events(h, time_it, HEADKV_TIMED_ATTN, attn_bytes(h, L), &e0, &e1);
+        return hip_status(launch_attn(D, h->shape, none, q, out, ws, splits, stream, e0, e1),
+                          "attention launch");
+    }
+    if (splits == 1) {
+        take_events(h, time_it, HEADKV_TIMED_ATTN_APPEND, fused_step_bytes(h, L, a.accumulate != 0),
+                    &e0, &e1);
         st = hip_status(launch_attn(D, h->shape, a, q, out, ws, 1, stream, e0, e1),
                         "append + attention launch");
-    } else {
-        st = hip_status(launch_append(D, h->shape, a, stream), "append launch");
-        if (!st) st = hip_status(launch_attn(D, h->shape, none, q, out, ws, splits, stream), "attention launch");
+        if (st) return st;
+        commit_append(h, L, step, update);
+        return ok();
     }
+    st = hip_status(launch_append(D, h->shape, a, stream), "append launch");
     if (st) return st;
     commit_append(h, L, step, update);
-    return ok();
+    take_events(h, time_it, HEADKV_TIMED_ATTN, attn_bytes(h, L), &e0, &e1);
+    return hip_status(launch_attn(D, h->shape, none, q, out, ws, splits, stream, e0, e1),
+                      "attention launch");
 }
 
 }  // namespace
@@ -393,6 +443,7 @@ headkv_status headkv_timing_reserve(headkv_t h, int64_t launches) {
         h->events.push_back(e);
     }
     h->timed_bytes.resize(h->events.size() / 2);
+    h->timed_kind.resize(h->events.size() / 2);
     return ok();
 }
 
@@ -400,7 +451,11 @@ headkv_status headkv_timing_collect(headkv_t h, double* kernel_ms, int64_t* laun
                                     double* alg_bytes, int64_t* dropped) {
     if (!h || !kernel_ms || !launches || !alg_bytes || !dropped)
         return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer");
-    double ms = 0, bytes = 0;
+    for (int k = 0; k < HEADKV_TIMED_KINDS; ++k) {
+        kernel_ms[k] = 0;
+        launches[k] = 0;
+        alg_bytes[k] = 0;
+    }
     if (h->timed > 0) {
         headkv_status st = hip_status(hipEventSynchronize(h->events[2 * h->timed - 1]), "event wait");
         if (st) return st;
@@ -410,12 +465,11 @@ headkv_status headkv_timing_collect(headkv_t h, double* kernel_ms, int64_t* laun
         headkv_status st = hip_status(hipEventElapsedTime(&e, h->events[2 * i], h->events[2 * i + 1]),
                                       "event time");
         if (st) return st;
-        ms += e;
-        bytes += h->timed_bytes[i];
+        const int k = h->timed_kind[i];
+        kernel_ms[k] += e;
+        launches[k] += 1;
+        alg_bytes[k] += h->timed_bytes[i];
     }
-    *kernel_ms = ms;
-    *launches = (int64_t)h->timed;
-    *alg_bytes = bytes;
     *dropped = h->timing_dropped;
     h->timed = 0;
     h->timing_dropped = 0;
@@ -459,9 +513,15 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
                     "budget launch");
     if (st) return st;
     std::vector<int32_t> bud(BH);
+    std::vector<uint8_t> lab(BH);
     st = hip_status(hipMemcpyAsync(bud.data(), budgets, sizeof(int32_t) * BH, hipMemcpyDeviceToHost, s),
                     "budget read-back");
-    if (st) return st;
+    if (!st) st = hip_status(hipMemcpyAsync(lab.data(), is_local, BH, hipMemcpyDeviceToHost, s),
+                             "label read-back");
+    if (st) {
+        (void)hipStreamSynchronize(s);
+        return st;
+    }
     st = hip_status(hipStreamSynchronize(s), "stream wait");
     if (st) return st;
     // segments: prefix + min(budget + P, N) slots each, in head order
@@ -497,7 +557,7 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
         AppendArgs none{};
         st = hip_status(launch_update(Dnew, h->shape, none, static_cast<const char*>(L.dense), 1,
                                       h->dense_seg, h->dense_cap, c.recent_len, c.rs_num, c.rs_den,
-                                      0, stream),
+                                      0, stream, nullptr, nullptr),
                         "relayout launch");
     }
     headkv_status st_wait = hip_status(hipStreamSynchronize(s), "stream wait");
@@ -506,6 +566,7 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     L.ragged = ragged_kv;
     L.grouped = true;
     L.budget.assign(bud.begin(), bud.end());
+    L.label_local.assign(lab.begin(), lab.end());
     L.cap.assign(cap.begin(), cap.end());
     for (int i = 0; i < BH; ++i) L.n[i] = std::min(L.n[i], L.budget[i]);
     return ok();

@@ -708,14 +708,17 @@ int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
 
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
                   int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
-                  int rs_num, int rs_den, int u, void* stream) {
+                  int rs_num, int rs_den, int u, void* stream, void* ev_start, void* ev_stop) {
     hipStream_t st = (hipStream_t)stream;
+    hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
     if (s.d == 128)
-        hipLaunchKernelGGL(k_update<128>, dim3(s.BH), dim3(kBlock), 0, st, L, s.C, s.N, a, src_kv,
-                           relayout, dense_seg_bytes, dense_cap, recent_len, rs_num, rs_den, u);
+        hipExtLaunchKernelGGL(k_update<128>, dim3(s.BH), dim3(kBlock), 0, st, e0, e1, 0, L, s.C,
+                              s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
+                              rs_num, rs_den, u);
     else
-        hipLaunchKernelGGL(k_update<64>, dim3(s.BH), dim3(kBlock), 0, st, L, s.C, s.N, a, src_kv,
-                           relayout, dense_seg_bytes, dense_cap, recent_len, rs_num, rs_den, u);
+        hipExtLaunchKernelGGL(k_update<64>, dim3(s.BH), dim3(kBlock), 0, st, e0, e1, 0, L, s.C,
+                              s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
+                              rs_num, rs_den, u);
     return last_error();
 }
 

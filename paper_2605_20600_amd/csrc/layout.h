@@ -101,7 +101,7 @@ int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
 // a.k == nullptr: no append.
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
                   int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
-                  int rs_num, int rs_den, int u, void* stream);
+                  int rs_num, int rs_den, int u, void* stream, void* ev_start, void* ev_stop);
 // a.k == nullptr: no append (only allowed with splits == 1 otherwise).
 // ev_start / ev_stop (hipEvent_t or nullptr) receive the attention kernel's
 // own start and end timestamps.
