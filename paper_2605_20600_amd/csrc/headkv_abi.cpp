@@ -262,6 +262,8 @@ void commit_append(headkv_t h, Layer& L, int32_t step, bool update) {
     L.last_step = step;
 }
 
+int max_cap(const Layer& L) { return *std::max_element(L.cap.begin(), L.cap.end()); }
+
 int max_len(headkv_t h, const Layer& L) {
     return h->cfg.prefix_len + *std::max_element(L.n.begin(), L.n.end());
 }
@@ -282,7 +284,7 @@ headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step, c
     LayerDev D = dev_of(h, L);
     if (update)
         st = hip_status(launch_update(D, h->shape, a, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
-                                      c.rs_den, u, stream, nullptr, nullptr),
+                                      c.rs_den, u, max_cap(L), stream, nullptr, nullptr),
                         "append + update launch");
     else
         st = hip_status(launch_append(D, h->shape, a, stream), "append launch");
@@ -377,7 +379,7 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
     if (update) {
         take_events(h, time_it, HEADKV_TIMED_UPDATE, update_bytes(h, L), &e0, &e1);
         st = hip_status(launch_update(D, h->shape, a, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
-                                      c.rs_den, u, stream, e0, e1),
+                                      c.rs_den, u, max_cap(L), stream, e0, e1),
                         "append + update launch");
         if (st) return st;
         commit_append(h, L, step, update);
@@ -557,7 +559,7 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
         AppendArgs none{};
         st = hip_status(launch_update(Dnew, h->shape, none, static_cast<const char*>(L.dense), 1,
                                       h->dense_seg, h->dense_cap, c.recent_len, c.rs_num, c.rs_den,
-                                      0, stream, nullptr, nullptr),
+                                      0, h->dense_cap, stream, nullptr, nullptr),
                         "relayout launch");
     }
     headkv_status st_wait = hip_status(hipStreamSynchronize(s), "stream wait");

@@ -268,21 +268,109 @@ __global__ void k_budgets(LayerDev L, int H, int N, const uint8_t* is_local,
 }
 
 // ------------------------------------------------------------------- update
+// LDS of one update block, sized by the host from the largest source capacity
+// of the launch (`cap`) and the number of visual positions (`N`).
+struct UpdateLds {
+    static __host__ __device__ int words(int N) { return (N + 31) >> 5; }
+    static __host__ __device__ size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
+    // bitmap | word prefix | order (u16) | evict (u8) | positions (i32) |
+    // scores (f64, also two int lists) | query sum (f64 [d])
+    static __host__ __device__ size_t off_wpre(int N) { return a16(4 * (size_t)words(N)); }
+    static __host__ __device__ size_t off_order(int N) { return off_wpre(N) + a16(4 * (size_t)words(N)); }
+    static __host__ __device__ size_t off_evict(int N, int cap) { return off_order(N) + a16(2 * (size_t)cap); }
+    static __host__ __device__ size_t off_pos(int N, int cap) { return off_evict(N, cap) + a16((size_t)cap); }
+    static __host__ __device__ size_t off_sig(int N, int cap) { return off_pos(N, cap) + a16(4 * (size_t)cap); }
+    static __host__ __device__ size_t off_qs(int N, int cap) { return off_sig(N, cap) + a16(8 * (size_t)cap); }
+    static __host__ __device__ size_t bytes(int N, int cap, int d) { return off_qs(N, cap) + a16(8 * (size_t)d); }
+};
+
+// fp64 score -> unsigned key with the same order (-0 and +0 map to one key,
+// since they compare equal).
+__device__ __forceinline__ uint64_t score_key(double x) {
+    if (x == 0.0) x = 0.0;
+    const uint64_t u = (uint64_t)__double_as_longlong(x);
+    return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+// Marks for eviction the mq lowest entries of part [lo, hi) by (score, rank):
+// a radix select over the keys, 8 bits per pass from the top, that stops as
+// soon as the chosen digit's bucket leaves entirely; if the exact threshold key
+// is reached, the entries equal to it leave in rank order.
+__device__ void select_lowest(const double* sig, const uint16_t* order, uint8_t* evict, int lo,
+                              int hi, int mq, int tid) {
+    __shared__ uint32_t hist[256];
+    __shared__ int pick[3];  // digit, entries below its bucket, bucket size
+    if (mq <= 0) return;
+    if (mq >= hi - lo) {
+        for (int r = lo + tid; r < hi; r += kBlock) evict[order[r]] = 1;
+        return;
+    }
+    uint64_t prefix = 0;  // chosen digits so far
+    int want = mq;        // entries still to take at or above the prefix
+    for (int shift = 56;; shift -= 8) {
+        const uint64_t above = shift == 56 ? 0ull : ~0ull << (shift + 8);
+        hist[tid] = 0u;
+        __syncthreads();
+        for (int r = lo + tid; r < hi; r += kBlock) {
+            const uint64_t k = score_key(sig[r]);
+            if ((k & above) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+        }
+        __syncthreads();
+        const int c = (int)hist[tid];
+        int tot;
+        const int ex = block_exclusive_scan(c, &tot);
+        if (ex < want && want <= ex + c) {
+            pick[0] = tid;
+            pick[1] = ex;
+            pick[2] = c;
+        }
+        __syncthreads();
+        prefix |= (uint64_t)pick[0] << shift;
+        want -= pick[1];
+        const uint64_t upto = ~0ull << shift;
+        if (want == pick[2]) {  // the whole bucket leaves with everything below it
+            for (int r = lo + tid; r < hi; r += kBlock)
+                if ((score_key(sig[r]) & upto) <= prefix) evict[order[r]] = 1;
+            return;
+        }
+        if (shift == 0) {  // prefix is the exact threshold key
+            int taken = 0;
+            for (int r0 = lo; r0 < hi && taken < want; r0 += kBlock) {
+                const int r = r0 + tid;
+                const uint64_t k = r < hi ? score_key(sig[r]) : ~0ull;
+                const int eq = (r < hi && k == prefix) ? 1 : 0;
+                int t;
+                const int e = block_exclusive_scan(eq, &t);
+                if (eq && taken + e < want) evict[order[r]] = 1;
+                taken += t;
+            }
+            for (int r = lo + tid; r < hi; r += kBlock)
+                if (score_key(sig[r]) < prefix) evict[order[r]] = 1;
+            return;
+        }
+        __syncthreads();  // hist and pick are rewritten next pass
+    }
+}
+
+// One block per head: optional append, then the periodic update of Eqs. 2-6
+// (or, with `relayout`, the first update fused with the move into the head's
+// new segment).
 template <int D>
 __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, AppendArgs a,
                                                    const char* src_kv, int relayout,
                                                    int64_t dense_seg_bytes, int dense_cap,
-                                                   int recent_len, int rs_num, int rs_den, int u) {
+                                                   int recent_len, int rs_num, int rs_den, int u,
+                                                   int lds_cap) {
 #pragma clang fp contract(off)
-    constexpr int kMaxCap = HEADKV_MAX_CAPACITY;
-    constexpr int kWords = HEADKV_MAX_VISUAL / 32;
-    constexpr int kRow16 = D / 8;  // 16-byte pieces per K or V row
-    __shared__ uint32_t bm[kWords];
-    __shared__ int32_t wpre[kWords];
-    __shared__ uint16_t order[kMaxCap];  // slot of rank r (ranks by position)
-    __shared__ uint8_t evict[kMaxCap];   // by slot
-    __shared__ double sig[kMaxCap];      // score by rank; reused as int lists
-    __shared__ double qs[D];
+    constexpr int kRow16 = D / 8;  // 16-byte chunks per row
+    extern __shared__ __align__(16) unsigned char lds[];
+    uint32_t* bm = reinterpret_cast<uint32_t*>(lds);
+    int32_t* wpre = reinterpret_cast<int32_t*>(lds + UpdateLds::off_wpre(N));
+    uint16_t* order = reinterpret_cast<uint16_t*>(lds + UpdateLds::off_order(N));
+    uint8_t* evict = lds + UpdateLds::off_evict(N, lds_cap);
+    double* sig = reinterpret_cast<double*>(lds + UpdateLds::off_sig(N, lds_cap));
+    double* qs = reinterpret_cast<double*>(lds + UpdateLds::off_qs(N, lds_cap));
+    int32_t* pos = reinterpret_cast<int32_t*>(lds + UpdateLds::off_pos(N, lds_cap));
     const int h = blockIdx.x, tid = threadIdx.x;
     if (a.k != nullptr) {  // the step's append, then the update that follows it
         const int n0 = L.n[h];
@@ -307,12 +395,13 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
     SegPtrs S = seg_ptrs(src_seg, C, src_cap, D);
 
     // rank every occupied slot by its position: bitmap + prefix popcount
-    const int nw = (N + 31) >> 5;
+    const int nw = UpdateLds::words(N);
     for (int i = tid; i < nw; i += kBlock) bm[i] = 0u;
     for (int i = tid; i < n; i += kBlock) evict[i] = 0;
     __syncthreads();
     for (int s = tid; s < n; s += kBlock) {
         const int p = S.pos[s];
+        pos[s] = p;
         atomicOr(&bm[p >> 5], 1u << (p & 31));
     }
     __syncthreads();
@@ -327,7 +416,7 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
     }
     __syncthreads();
     for (int s = tid; s < n; s += kBlock) {
-        const int p = S.pos[s];
+        const int p = pos[s];
         const int r = wpre[p >> 5] + __popc(bm[p >> 5] & ((1u << (p & 31)) - 1u));
         order[r] = (uint16_t)s;
     }
@@ -351,48 +440,44 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
                 m_long += m_near - n_near;
                 m_near = n_near;
             }
+            // a part is scored only if it keeps some and loses some tokens
+            const bool sel_long = m_long > 0 && m_long < n_long;
+            const bool sel_near = m_near > 0 && m_near < n_near;
+            const int r_lo = sel_long ? 0 : n_long;
+            const int r_hi = sel_near ? T : n_long;
             // Eq. (6): mean raw logit of the past-P queries; the positive factor
-            // 1/(P sqrt(d)) is dropped, the order is that of (sum q) . k
+            // 1/(P sqrt(d)) is dropped, the order is that of (sum q) . k, summed
+            // over the dims in order in fp64.  Each thread reads its row's 16-byte
+            // chunks together and then walks them in order.
             for (int i = tid; i < D; i += kBlock) qs[i] = L.qsum[(size_t)h * D + i];
             __syncthreads();
-            for (int r = tid; r < T; r += kBlock) {
-                const uint16_t* kr = S.K + (size_t)(C + order[r]) * D;
+            for (int r = r_lo + tid; r < r_hi; r += kBlock) {
+                const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + order[r]) * D);
+                uint4 v[kRow16];
+#pragma unroll
+                for (int c = 0; c < kRow16; ++c) v[c] = kr[c];
                 double acc = 0.0;
-                for (int i = 0; i < D; i += 8) {
-                    const Words<4> w4 = *reinterpret_cast<const Words<4>*>(kr + i);
+#pragma unroll
+                for (int c = 0; c < kRow16; ++c) {
+                    const uint32_t wv[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        acc = acc + qs[i + 2 * e] * (double)bf_lo(w4.w[e]);
-                        acc = acc + qs[i + 2 * e + 1] * (double)bf_hi(w4.w[e]);
+                        acc = acc + qs[8 * c + 2 * e] * (double)bf_lo(wv[e]);
+                        acc = acc + qs[8 * c + 2 * e + 1] * (double)bf_hi(wv[e]);
                     }
                 }
                 sig[r] = acc;
             }
             __syncthreads();
             // per part, evict the m lowest by (score, position)
-            for (int r = tid; r < T; r += kBlock) {
-                const bool lp = r < n_long;
-                const int lo = lp ? 0 : n_long, hi = lp ? n_long : T;
-                const int mq = lp ? m_long : m_near;
-                if (mq == 0) continue;
-                bool ev = true;
-                if (mq < hi - lo) {
-                    const double sr = sig[r];
-                    int cnt = 0;
-                    for (int r2 = lo; r2 < hi && cnt < mq; ++r2) {
-                        const double s2 = sig[r2];
-                        cnt += (s2 < sr) || (s2 == sr && r2 < r);
-                    }
-                    ev = cnt < mq;
-                }
-                if (ev) evict[order[r]] = 1;
-            }
+            select_lowest(sig, order, evict, 0, n_long, m_long, tid);
+            select_lowest(sig, order, evict, n_long, T, m_near, tid);
         }
     }
     __syncthreads();
     const int n_new = n - M;
     int32_t* list_a = reinterpret_cast<int32_t*>(sig);
-    int32_t* list_b = list_a + kMaxCap;
+    int32_t* list_b = list_a + lds_cap;
 
     if (relayout) {
         // prefix rows, then kept slots in position order, into the new segment
@@ -413,7 +498,7 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
             const int ex = block_exclusive_scan(kf, &tot);
             if (kf) {
                 list_a[base + ex] = order[r];
-                Dd.pos[base + ex] = S.pos[order[r]];
+                Dd.pos[base + ex] = pos[order[r]];
             }
             base += tot;
         }
@@ -451,7 +536,7 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
             k4[dst] = k4[src];
             v4[dst] = v4[src];
         }
-        for (int j = tid; j < nh; j += kBlock) S.pos[list_a[j]] = S.pos[list_b[j]];
+        for (int j = tid; j < nh; j += kBlock) S.pos[list_a[j]] = pos[list_b[j]];
     }
     if (tid == 0) L.n[h] = n_new;
 }
@@ -708,19 +793,34 @@ int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
 
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
                   int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
-                  int rs_num, int rs_den, int u, void* stream, void* ev_start, void* ev_stop) {
+                  int rs_num, int rs_den, int u, int lds_cap, void* stream, void* ev_start,
+                  void* ev_stop) {
     hipStream_t st = (hipStream_t)stream;
     hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
+    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d);
+    // allow the update block more than 64 KB of dynamic LDS (gfx950: 160 KB)
+    static const bool lds_ok = [] {
+        const int max_lds = 160 * 1024;
+        bool ok = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_update<128>),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, max_lds) == hipSuccess;
+        ok = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_update<64>),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, max_lds) == hipSuccess && ok;
+        (void)hipGetLastError();
+        return ok;
+    }();
+    (void)lds_ok;
     if (s.d == 128)
-        hipExtLaunchKernelGGL(k_update<128>, dim3(s.BH), dim3(kBlock), 0, st, e0, e1, 0, L, s.C,
+        hipExtLaunchKernelGGL(k_update<128>, dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, s.C,
                               s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
-                              rs_num, rs_den, u);
+                              rs_num, rs_den, u, lds_cap);
     else
-        hipExtLaunchKernelGGL(k_update<64>, dim3(s.BH), dim3(kBlock), 0, st, e0, e1, 0, L, s.C,
+        hipExtLaunchKernelGGL(k_update<64>, dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, s.C,
                               s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
-                              rs_num, rs_den, u);
+                              rs_num, rs_den, u, lds_cap);
     return last_error();
 }
+
+size_t update_lds_bytes(int N, int cap, int d) { return UpdateLds::bytes(N, cap, d); }
 
 template <int D>
 static void attn_dispatch(const LayerDev& L, const Shape& s, const AppendArgs& a,

@@ -99,9 +99,13 @@ int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
                    const int32_t* override_b, int32_t* budgets, int mode, int row_len,
                    int recent_len, int rho_num, int rho_den, void* stream);
 // a.k == nullptr: no append.
+// lds_cap: largest visual capacity among the launch's source segments.
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
                   int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
-                  int rs_num, int rs_den, int u, void* stream, void* ev_start, void* ev_stop);
+                  int rs_num, int rs_den, int u, int lds_cap, void* stream, void* ev_start,
+                  void* ev_stop);
+// Dynamic LDS of one update block.
+size_t update_lds_bytes(int N, int cap, int d);
 // a.k == nullptr: no append (only allowed with splits == 1 otherwise).
 // ev_start / ev_stop (hipEvent_t or nullptr) receive the attention kernel's
 // own start and end timestamps.
