@@ -46,22 +46,91 @@ def parse():
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 512 MiB device copy five times (calibrates the HBM "
                         "byte counters of a profiler run) and exit")
+    p.add_argument("--traffic-record", nargs=4, metavar="DIR",
+                   help="write the attention kernel's traffic record from four rocprofv3 --pmc "
+                        "output folders (kernel FETCH_SIZE, kernel WRITE_SIZE, copy probe "
+                        "FETCH_SIZE, copy probe WRITE_SIZE) and exit; no GPU needed")
+    p.add_argument("--traffic-kernel", default="k_attn<128, true, 1024, false>",
+                   help="kernel name the traffic record is taken for")
     return p.parse_args()
+
+
+# sources of the attention kernel: the profiler's byte counters stay valid
+# while these are unchanged
+ATTN_SOURCES = ("paper_2605_20600_amd/csrc/attn_kernels.hip",
+                "paper_2605_20600_amd/csrc/device_common.h",
+                "paper_2605_20600_amd/csrc/layout.h")
+TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_attn_lumina768_b8_rho1-8_traffic.json")
+
+
+def attn_source_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in ATTN_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic():
     """HBM bytes per dispatch of the attention kernel from the profiler's byte
-    counters (profiles/), or None once the kernel source differs from the one
+    counters (profiles/), or None once the kernel sources differ from the ones
     the counters were taken with."""
-    import hashlib
-    rec_path = os.path.join(ROOT, "profiles", "k_attn_lumina768_b8_rho1-8_traffic.json")
-    src = os.path.join(ROOT, "paper_2605_20600_amd", "csrc", "kernels.hip")
     try:
-        rec = json.load(open(rec_path))
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        rec = json.load(open(TRAFFIC_RECORD))
     except OSError:
         return None
-    return rec["traffic_bytes_per_dispatch"] if rec.get("kernels_hip_sha256") == sha else None
+    ok = rec.get("attn_source_sha256") == attn_source_sha256()
+    return rec["traffic_bytes_per_dispatch"] if ok else None
+
+
+def counter_mean(run_dir: str, kernel_substr: str):
+    """Mean value per dispatch of the one counter of a rocprofv3 --pmc run
+    (its counter_collection.csv), over the dispatches of the named kernel."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {run_dir}")
+    total, n = 0.0, 0
+    with open(files[0]) as fh:
+        for row in csv.DictReader(fh):
+            if kernel_substr in row.get("Kernel_Name", ""):
+                total += float(row["Counter_Value"])
+                n += 1
+    if n == 0:
+        raise SystemExit(f"no dispatch of {kernel_substr!r} in {files[0]}")
+    return total / n, n
+
+
+def write_traffic_record(dirs, kernel: str):
+    """Writes the traffic record from four rocprofv3 --pmc runs: FETCH_SIZE and
+    WRITE_SIZE of the attention kernel, then of the copy probe (whose bytes
+    are known), which scale the counters to bytes."""
+    fetch, n = counter_mean(dirs[0], kernel)
+    write, _ = counter_mean(dirs[1], kernel)
+    copy_fetch, _ = counter_mean(dirs[2], "copyBuffer")  # the runtime's copy kernel
+    copy_write, _ = counter_mean(dirs[3], "copyBuffer")
+    probe = 512 << 20
+    fs, ws = probe / (copy_fetch * 1024), probe / (copy_write * 1024)
+    rec = {
+        "kernel": kernel,
+        "workload": "lumina_mgpt_768_shape b8 rho=1/8",
+        "attn_source_sha256": attn_source_sha256(),
+        "dispatches_sampled": n,
+        "fetch_kib_per_dispatch": fetch,
+        "write_kib_per_dispatch": write,
+        "copy_probe_bytes": probe,
+        "copy_fetch_kib": copy_fetch,
+        "copy_write_kib": copy_write,
+        "fetch_scale": fs,
+        "write_scale": ws,
+        "traffic_bytes_per_dispatch": fetch * 1024 * fs + write * 1024 * ws,
+    }
+    with open(TRAFFIC_RECORD, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps(rec))
 
 
 def cpu_baseline(wl, seconds_target: float):
@@ -123,6 +192,9 @@ def main():
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the decode path "
               "shards by batch row or head with no communication, see DESIGN.md", file=sys.stderr)
         sys.exit(2)
+    if args.traffic_record:
+        write_traffic_record(args.traffic_record, args.traffic_kernel)
+        return
     import torch
     if args.copy_probe:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda").fill_(1)

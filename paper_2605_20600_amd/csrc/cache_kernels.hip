@@ -1,22 +1,17 @@
-// HIP kernels of the head-aware compressed-KV decode path, written for gfx950
-// (CDNA4: 64-lane wavefronts, 160 KB LDS per CU, 8 XCDs).
+// HIP kernels of the compressed cache, written for gfx950 (CDNA4: 64-lane
+// wavefronts, 160 KB LDS per CU, 8 XCDs).
 //
 //   k_prefill  Step 1 cache prefilling (Sec. 4): conditional keys/values into
 //              rows 0..C-1 of every head, layer state reset.
 //   k_append   cache append (Sec. 3, KV Cache) + running sum of the queries of
 //              the current update window (Eq. 6 is linear in the queries);
-//              also fused into k_update and k_attn.
+//              also fused into k_update and the attention kernels.
 //   k_score    head grouping (Sec. 4, Step 2), fp64.
 //   k_budgets  per-head budgets (Sec. 5.1, Implementation Details).
 //   k_update   periodic update (Eqs. 2-6): sliding window (Eq. 3) or
 //              Stratified Token Eviction (Eqs. 4-6), fused with the
 //              compaction of the head's slots or, at the grouping step, with
 //              the move into the head's own segment.
-//   k_attn     decode attention, Eq. (1): one 1024-thread block per head with
-//              all of the head's K/V loads in flight, online softmax in
-//              registers, merge through LDS; optionally fused with the append;
-//   k_merge    merge of the splits of a head, for layers with fewer heads
-//              than compute units.
 //   k_export   retained-position masks for parity checks.
 //
 // Everything that decides an index (grouping mass, eviction scores) is
@@ -29,76 +24,25 @@
 #include <cstdint>
 
 #include "../../include/headkv.h"
+#include "device_common.h"
 #include "layout.h"
 
 namespace headkv {
 namespace {
 
-template <int NW>
-struct alignas(NW * 4) Words {
-    uint32_t w[NW];
-};
-
-__device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
-__device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
-__device__ __forceinline__ double bf_f64(uint16_t b) {
-    return (double)__uint_as_float((uint32_t)b << 16);
-}
-
-// Sum over the 16 lanes of a DPP row: quad swaps, then half-row and row
-// mirrors; every lane of the row ends with the full sum.
-__device__ __forceinline__ float row16_sum(float v) {
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
-    return v;
-}
-
-// Exclusive prefix sum over a 256-thread block; *total receives the sum.
-// Every thread of the block must call it.
-__device__ int block_exclusive_scan(int x, int* total) {
-    __shared__ int wsum[kBlock / 64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int inc = x;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(inc, o);
-        if (lane >= o) inc += y;
-    }
-    if (lane == 63) wsum[wave] = inc;
-    __syncthreads();
-    int off = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < kBlock / 64; ++w) {
-        off += w < wave ? wsum[w] : 0;
-        tot += wsum[w];
-    }
-    __syncthreads();
-    *total = tot;
-    return off + inc - x;
-}
-
-struct SegPtrs {
-    uint16_t* K;
-    uint16_t* V;
-    int32_t* pos;
-};
-
-__device__ __forceinline__ SegPtrs seg_ptrs(char* seg, int C, int cap, int d) {
-    SegPtrs p;
-    p.K = reinterpret_cast<uint16_t*>(seg);
-    p.V = p.K + (size_t)(C + cap) * d;
-    p.pos = reinterpret_cast<int32_t*>(p.V + (size_t)(C + cap) * d);
-    return p;
-}
+using namespace dev;
 
 // ------------------------------------------------------------------ prefill
 __global__ __launch_bounds__(kBlock) void k_prefill(LayerDev L, int C, int d, const uint16_t* kc,
                                                     const uint16_t* vc, int64_t seg_bytes,
-                                                    int dense_cap) {
+                                                    int dense_cap, int dense_chunks) {
     const int h = blockIdx.x, tid = threadIdx.x;
+    // chunk table of the dense layout: every head has dense_chunks chunks
+    for (int c = tid; c < dense_chunks; c += kBlock)
+        L.items[(size_t)h * dense_chunks + c] = ((uint32_t)h << 8) | (uint32_t)c;
     if (tid == 0) {
+        L.item_start[h] = h * dense_chunks;
+        if (h == (int)gridDim.x - 1) L.item_start[h + 1] = (h + 1) * dense_chunks;
         L.seg_off[h] = (int64_t)h * seg_bytes;
         L.cap[h] = dense_cap;
         L.n[h] = 0;
@@ -119,51 +63,6 @@ __global__ __launch_bounds__(kBlock) void k_prefill(LayerDev L, int C, int d, co
         kd[i] = ks[i];
         vd[i] = vs[i];
     }
-}
-
-// ------------------------------------------------------------------- append
-// K <- [K, k_t], V <- [V, v_t] for head h by the threads tid < d of a block:
-// row C+n, pos[n] = step, the query sum of the update window.  Split in a
-// load half and a store half so that a caller can put other loads between
-// them; the length n is changed by append_commit once no thread reads it.
-struct AppendVals {
-    uint16_t k = 0, v = 0;
-    double qs_old = 0.0, q = 0.0;
-};
-
-__device__ __forceinline__ AppendVals append_load(const LayerDev& L, int d, int h,
-                                                  const AppendArgs& a, int tid) {
-    AppendVals r;
-    if (tid < d) {
-        r.k = a.k[(size_t)h * d + tid];
-        r.v = a.v[(size_t)h * d + tid];
-        if (a.accumulate) {
-            r.q = bf_f64(a.q[(size_t)h * d + tid]);
-            if (!a.reset) r.qs_old = L.qsum[(size_t)h * d + tid];
-        }
-    }
-    return r;
-}
-
-__device__ __forceinline__ void append_store(const LayerDev& L, int C, int d, int h, int n,
-                                             const AppendArgs& a, const AppendVals& r, int tid) {
-#pragma clang fp contract(off)
-    if (tid >= d) return;
-    SegPtrs s = seg_ptrs(L.kv + L.seg_off[h], C, L.cap[h], d);
-    const size_t row = (size_t)(C + n) * d;
-    s.K[row + tid] = r.k;
-    s.V[row + tid] = r.v;
-    if (a.accumulate) L.qsum[(size_t)h * d + tid] = r.qs_old + r.q;  // 0 + q on a reset
-    if (tid == 0) s.pos[n] = a.step;
-}
-
-__device__ __forceinline__ void append_token(const LayerDev& L, int C, int d, int h, int n,
-                                             const AppendArgs& a, int tid) {
-    append_store(L, C, d, h, n, a, append_load(L, d, h, a, tid), tid);
-}
-
-__device__ __forceinline__ void append_commit(const LayerDev& L, int h, int n, int tid) {
-    if (tid == 0) L.n[h] = n + 1;
 }
 
 __global__ void k_append(LayerDev L, int C, int d, AppendArgs a) {
@@ -541,211 +440,6 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
     if (tid == 0) L.n[h] = n_new;
 }
 
-// ---------------------------------------------------------------- attention
-// Decode attention, Eq. (1), one block per head (or per split of a head when a
-// layer has fewer heads than compute units).  1024 threads = 64 rows of 16
-// lanes; each row holds one token at a time, d/16 elements per lane (one 8- or
-// 16-byte load), so the 4 rows of a wavefront read 4 consecutive K or V rows
-// of the segment.  A pass covers 64 x kAttnTpr = 512 tokens: every load of the
-// pass is issued before the first one is used (row indices past the end are
-// clamped to the last token and their logits masked, so no load sits behind a
-// branch), which puts a whole head of up to 512 tokens in flight at once.  K/V
-// are read once per step, so the loads are non-temporal.  The softmax is
-// online per row; rows are merged with cross-lane swaps and the 16 wavefronts
-// through LDS.  With `append`, the step's token is attended from the input and
-// written into the cache by the same block.
-template <int D>
-struct AttnRegs {
-    static constexpr int VPL = D / 16;  // bf16 elements per lane
-    static constexpr int NW = VPL / 2;  // 32-bit words per lane
-    using Vec = Words<NW>;
-};
-
-template <int NW>
-__device__ __forceinline__ Words<NW> nt_load(const uint16_t* p) {
-    typedef unsigned int vec_t __attribute__((ext_vector_type(NW)));
-    const vec_t t = __builtin_nontemporal_load(reinterpret_cast<const vec_t*>(p));
-    Words<NW> w;
-#pragma unroll
-    for (int e = 0; e < NW; ++e) w.w[e] = t[e];
-    return w;
-}
-
-template <int D, bool APPEND>
-__global__ __launch_bounds__(kAttnThreads) void k_attn(LayerDev L, int C, AppendArgs a,
-                                                       const uint16_t* __restrict__ q,
-                                                       float* __restrict__ out,
-                                                       float* __restrict__ part, int splits,
-                                                       int use_order, float qscale) {
-    using Vec = typename AttnRegs<D>::Vec;
-    constexpr int VPL = AttnRegs<D>::VPL;
-    constexpr int NW = AttnRegs<D>::NW;
-    constexpr int ROWS = kAttnThreads / 16;
-    constexpr int TP = ROWS * kAttnTpr;  // tokens per pass
-    constexpr int WAVES = kAttnThreads / 64;
-    const int item = blockIdx.x / splits;
-    const int sp = blockIdx.x - item * splits;
-    const int h = use_order ? L.order[item] : item;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int row = tid >> 4, col = tid & 15;
-    const Vec qraw = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
-    const int n = L.n[h];
-    const int len = C + n + (APPEND ? 1 : 0);
-    const int span = (len + splits - 1) / splits;
-    const int t_begin = sp * span;
-    const int t_end = min(len, t_begin + span);
-    const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + L.seg_off[h]);
-    const uint16_t* V = K + (size_t)(C + L.cap[h]) * D;
-
-    // the append's loads go out before the K/V stream and its stores right
-    // after (the attention reads the new token from the input, never from row
-    // C+n); n itself changes at the end
-    AppendVals av;
-    if (APPEND) av = append_load(L, D, h, a, tid);
-    float m = -INFINITY, l = 0.f;
-    float acc[VPL];
-#pragma unroll
-    for (int e = 0; e < VPL; ++e) acc[e] = 0.f;
-    float qf[VPL];
-    bool q_ready = false;
-    for (int t0 = t_begin; t0 < t_end; t0 += TP) {
-        Vec kk[kAttnTpr], vv[kAttnTpr];
-#pragma unroll
-        for (int j = 0; j < kAttnTpr; ++j) {
-            const int tok = min(t0 + j * ROWS + row, t_end - 1);
-            const uint16_t* kp = K + (size_t)tok * D;
-            const uint16_t* vp = V + (size_t)tok * D;
-            if (APPEND && tok == len - 1) {
-                kp = a.k + (size_t)h * D;
-                vp = a.v + (size_t)h * D;
-            }
-            kk[j] = nt_load<NW>(kp + col * VPL);
-            vv[j] = nt_load<NW>(vp + col * VPL);
-        }
-        // keep every load of the pass ahead of its first use
-        __builtin_amdgcn_sched_barrier(0);
-        if (!q_ready) {
-            if (APPEND) append_store(L, C, D, h, n, a, av, tid);
-#pragma unroll
-            for (int e = 0; e < NW; ++e) {
-                qf[2 * e] = bf_lo(qraw.w[e]) * qscale;
-                qf[2 * e + 1] = bf_hi(qraw.w[e]) * qscale;
-            }
-            q_ready = true;
-        }
-        float s[kAttnTpr];
-        float mx = m;
-#pragma unroll
-        for (int j = 0; j < kAttnTpr; ++j) {
-            float dp = 0.f;
-#pragma unroll
-            for (int e = 0; e < NW; ++e) {
-                dp += qf[2 * e] * bf_lo(kk[j].w[e]);
-                dp += qf[2 * e + 1] * bf_hi(kk[j].w[e]);
-            }
-            dp = row16_sum(dp);
-            s[j] = (t0 + j * ROWS + row < t_end) ? dp : -INFINITY;
-            mx = fmaxf(mx, s[j]);
-        }
-        if (mx != -INFINITY) {
-            const float f = __builtin_amdgcn_exp2f(m - mx);  // m = -inf gives 0
-            l *= f;
-#pragma unroll
-            for (int e = 0; e < VPL; ++e) acc[e] *= f;
-#pragma unroll
-            for (int j = 0; j < kAttnTpr; ++j) {
-                const float p = __builtin_amdgcn_exp2f(s[j] - mx);
-                l += p;
-#pragma unroll
-                for (int e = 0; e < NW; ++e) {
-                    acc[2 * e] += p * bf_lo(vv[j].w[e]);
-                    acc[2 * e + 1] += p * bf_hi(vv[j].w[e]);
-                }
-            }
-            m = mx;
-        }
-    }
-    if (APPEND && !q_ready) append_store(L, C, D, h, n, a, av, tid);  // empty range
-    // merge the four rows of each wavefront
-#pragma unroll
-    for (int off = 16; off <= 32; off <<= 1) {
-        const float mo = __shfl_xor(m, off);
-        const float lo = __shfl_xor(l, off);
-        const float mn = fmaxf(m, mo);
-        const float fa = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mn);
-        const float fb = (mo == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mo - mn);
-        l = l * fa + lo * fb;
-#pragma unroll
-        for (int e = 0; e < VPL; ++e) {
-            const float ao = __shfl_xor(acc[e], off);
-            acc[e] = acc[e] * fa + ao * fb;
-        }
-        m = mn;
-    }
-    __shared__ float sm[WAVES], sl[WAVES];
-    __shared__ float sacc[WAVES][D];
-    if (lane < 16) {
-#pragma unroll
-        for (int e = 0; e < VPL; ++e) sacc[wave][col * VPL + e] = acc[e];
-        if (lane == 0) {
-            sm[wave] = m;
-            sl[wave] = l;
-        }
-    }
-    __syncthreads();  // every wavefront has read n before the append changes it
-    if (APPEND) append_commit(L, h, n, tid);
-    if (tid < D) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int w = 0; w < WAVES; ++w) mx = fmaxf(mx, sm[w]);
-        float o = 0.f, z = 0.f;
-#pragma unroll
-        for (int w = 0; w < WAVES; ++w) {
-            const float f = (sm[w] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sm[w] - mx);
-            o += f * sacc[w][tid];
-            z += f * sl[w];
-        }
-        if (splits == 1) {
-            out[(size_t)h * D + tid] = o / z;
-        } else {
-            float* pp = part + ((size_t)h * splits + sp) * (D + 2);
-            pp[tid] = o;
-            if (tid == 0) {
-                pp[D] = mx;
-                pp[D + 1] = z;
-            }
-        }
-    }
-}
-
-// Merge of the splits of every head (layers with fewer heads than compute
-// units).  A kernel of its own: plain device memory is only coherent across
-// the XCDs' L2 caches at kernel boundaries.
-template <int D>
-__global__ __launch_bounds__(D) void k_merge(float* __restrict__ out,
-                                             const float* __restrict__ part, int splits) {
-    const int h = blockIdx.x, tid = threadIdx.x;
-    constexpr int PS = D + 2;
-    const float* p0 = part + (size_t)h * splits * PS;
-    float mi[kMaxSplits];
-    float mx = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < kMaxSplits; ++i) {
-        mi[i] = i < splits ? p0[(size_t)i * PS + D] : -INFINITY;
-        mx = fmaxf(mx, mi[i]);
-    }
-    float num = 0.f, den = 0.f;
-#pragma unroll
-    for (int i = 0; i < kMaxSplits; ++i) {
-        if (i < splits && mi[i] != -INFINITY) {
-            const float f = __builtin_amdgcn_exp2f(mi[i] - mx);
-            num += f * p0[(size_t)i * PS + tid];
-            den += f * p0[(size_t)i * PS + D + 1];
-        }
-    }
-    out[(size_t)h * D + tid] = num / den;
-}
-
 // ------------------------------------------------------------------- export
 __global__ __launch_bounds__(kBlock) void k_export(LayerDev L, int C, int d, int N, uint8_t* mask,
                                                    int32_t* count) {
@@ -763,9 +457,9 @@ inline int last_error() { return (int)hipGetLastError(); }
 }  // namespace
 
 int launch_prefill(const LayerDev& L, const Shape& s, const uint16_t* kc, const uint16_t* vc,
-                   int64_t dense_seg_bytes, int dense_cap, void* stream) {
+                   int64_t dense_seg_bytes, int dense_cap, int dense_chunks, void* stream) {
     hipLaunchKernelGGL(k_prefill, dim3(s.BH), dim3(kBlock), 0, (hipStream_t)stream, L, s.C, s.d,
-                       kc, vc, dense_seg_bytes, dense_cap);
+                       kc, vc, dense_seg_bytes, dense_cap, dense_chunks);
     return last_error();
 }
 
@@ -821,36 +515,6 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
 }
 
 size_t update_lds_bytes(int N, int cap, int d) { return UpdateLds::bytes(N, cap, d); }
-
-template <int D>
-static void attn_dispatch(const LayerDev& L, const Shape& s, const AppendArgs& a,
-                          const uint16_t* q, float* out, float* partials, int splits,
-                          hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
-    const float qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
-    const dim3 grid(s.BH * splits), block(kAttnThreads);
-    // the longest-first order only matters when the blocks take more than one round
-    const int use_order = s.BH * splits > kCus ? 1 : 0;
-    // with events, they take the kernel's own start and end timestamps
-    if (a.k != nullptr)
-        hipExtLaunchKernelGGL((k_attn<D, true>), grid, block, 0, st, ev0, ev1, 0, L, s.C, a, q,
-                              out, partials, splits, use_order, qscale);
-    else
-        hipExtLaunchKernelGGL((k_attn<D, false>), grid, block, 0, st, ev0, ev1, 0, L, s.C, a, q,
-                              out, partials, splits, use_order, qscale);
-    if (splits > 1)
-        hipLaunchKernelGGL(k_merge<D>, dim3(s.BH), dim3(D), 0, st, out, partials, splits);
-}
-
-int launch_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
-                float* out, float* partials, int splits, void* stream, void* ev_start,
-                void* ev_stop) {
-    hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
-    if (s.d == 128)
-        attn_dispatch<128>(L, s, a, q, out, partials, splits, (hipStream_t)stream, e0, e1);
-    else
-        attn_dispatch<64>(L, s, a, q, out, partials, splits, (hipStream_t)stream, e0, e1);
-    return last_error();
-}
 
 int launch_export(const LayerDev& L, const Shape& s, uint8_t* mask, int32_t* count,
                   void* stream) {

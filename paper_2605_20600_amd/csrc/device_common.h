@@ -1,0 +1,120 @@
+// Device helpers shared by the cache kernels and the attention kernels:
+// bf16 unpacking, 16-lane row sums, block scans, the per-head segment view and
+// the append of a step's token.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "layout.h"
+
+namespace headkv {
+namespace dev {
+
+template <int NW>
+struct alignas(NW * 4) Words {
+    uint32_t w[NW];
+};
+
+__device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+__device__ __forceinline__ double bf_f64(uint16_t b) {
+    return (double)__uint_as_float((uint32_t)b << 16);
+}
+
+// Sum over the 16 lanes of a DPP row: quad swaps, then half-row and row
+// mirrors; every lane of the row ends with the full sum.
+__device__ __forceinline__ float row16_sum(float v) {
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
+    return v;
+}
+
+// Exclusive prefix sum over a 256-thread block; *total receives the sum.
+// Every thread of the block must call it.
+__device__ inline int block_exclusive_scan(int x, int* total) {
+    __shared__ int wsum[kBlock / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int inc = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(inc, o);
+        if (lane >= o) inc += y;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int off = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kBlock / 64; ++w) {
+        off += w < wave ? wsum[w] : 0;
+        tot += wsum[w];
+    }
+    __syncthreads();
+    *total = tot;
+    return off + inc - x;
+}
+
+struct SegPtrs {
+    uint16_t* K;
+    uint16_t* V;
+    int32_t* pos;
+};
+
+__device__ __forceinline__ SegPtrs seg_ptrs(char* seg, int C, int cap, int d) {
+    SegPtrs p;
+    p.K = reinterpret_cast<uint16_t*>(seg);
+    p.V = p.K + (size_t)(C + cap) * d;
+    p.pos = reinterpret_cast<int32_t*>(p.V + (size_t)(C + cap) * d);
+    return p;
+}
+
+// ------------------------------------------------------------------- append
+// K <- [K, k_t], V <- [V, v_t] for head h by the threads tid < d of a block:
+// row C+n, pos[n] = step, the query sum of the update window.  Split in a
+// load half and a store half so that a caller can put other loads between
+// them; the length n is changed by append_commit once no thread reads it.
+struct AppendVals {
+    uint16_t k = 0, v = 0;
+    double qs_old = 0.0, q = 0.0;
+};
+
+__device__ __forceinline__ AppendVals append_load(const LayerDev& L, int d, int h,
+                                                  const AppendArgs& a, int tid) {
+    AppendVals r;
+    if (tid < d) {
+        r.k = a.k[(size_t)h * d + tid];
+        r.v = a.v[(size_t)h * d + tid];
+        if (a.accumulate) {
+            r.q = bf_f64(a.q[(size_t)h * d + tid]);
+            if (!a.reset) r.qs_old = L.qsum[(size_t)h * d + tid];
+        }
+    }
+    return r;
+}
+
+__device__ __forceinline__ void append_store(const LayerDev& L, int C, int d, int h, int n,
+                                             const AppendArgs& a, const AppendVals& r, int tid) {
+#pragma clang fp contract(off)
+    if (tid >= d) return;
+    SegPtrs s = seg_ptrs(L.kv + L.seg_off[h], C, L.cap[h], d);
+    const size_t row = (size_t)(C + n) * d;
+    s.K[row + tid] = r.k;
+    s.V[row + tid] = r.v;
+    if (a.accumulate) L.qsum[(size_t)h * d + tid] = r.qs_old + r.q;  // 0 + q on a reset
+    if (tid == 0) s.pos[n] = a.step;
+}
+
+__device__ __forceinline__ void append_token(const LayerDev& L, int C, int d, int h, int n,
+                                             const AppendArgs& a, int tid) {
+    append_store(L, C, d, h, n, a, append_load(L, d, h, a, tid), tid);
+}
+
+__device__ __forceinline__ void append_commit(const LayerDev& L, int h, int n, int tid) {
+    if (tid == 0) L.n[h] = n + 1;
+}
+
+}  // namespace dev
+}  // namespace headkv

@@ -42,6 +42,8 @@ struct Layer {
     int last_step = -1;
     std::vector<int> n, budget, cap;
     std::vector<uint8_t> label_local;  // labels used by the updates (host copy)
+    int chunk_threads = kAttnMaxThreads;  // block size the chunk table is cut for
+    int items = 0;                        // entries of the chunk table
 };
 
 }  // namespace
@@ -97,6 +99,12 @@ headkv_status validate_config(const headkv_config* c) {
     if (c->rs_num < 0 || c->rs_den < 1 || c->rs_num > c->rs_den)
         return fail(HEADKV_ERR_INVALID_ARG, "r_s must be in [0, 1]");
     if (!(c->tau > 0.0 && c->tau <= 1.0)) return fail(HEADKV_ERR_INVALID_ARG, "tau must be in (0, 1]");
+    // chunk indices must fit the 8 bits of a chunk table entry (always true
+    // within the prefix and capacity limits)
+    const int max_cap = std::max(c->group_threshold, std::min(c->num_visual, HEADKV_MAX_CAPACITY));
+    const int tp = attn_tokens_per_pass(kAttnMinThreads);
+    if ((c->prefix_len + max_cap + 1 + tp - 1) / tp > kMaxChunksPerHead)
+        return fail(HEADKV_ERR_UNSUPPORTED, "too many attention chunks per head");
     return ok();
 }
 
@@ -107,26 +115,44 @@ struct Plan {
     MetaLayout ml;
 };
 
+// Chunks of one pass of a `threads`-thread block that cover a head of
+// capacity `cap` (prefix, slots and the token being appended).
+int chunks_of(int C, int cap, int threads) {
+    const int tp = attn_tokens_per_pass(threads);
+    return (C + cap + 1 + tp - 1) / tp;
+}
+
 Plan make_plan(const headkv_config& c) {
     Plan p;
     p.BH = c.batch * c.num_heads;
     p.dense_cap = c.group_threshold;
     p.dense_seg = (int64_t)segment_bytes(c.prefix_len, p.dense_cap, c.head_dim);
     p.dense_bytes = (size_t)p.dense_seg * p.BH;
-    p.ml.compute(p.BH, c.head_dim);
-    // partial (max, sum, weighted V) of every split of every head
-    p.ws_bytes = align_up((size_t)p.BH * kMaxSplits * (c.head_dim + 2) * sizeof(float), 256);
+    // the largest capacity any head can have, dense or after grouping
+    const int max_cap = std::max(p.dense_cap, std::min(c.num_visual, HEADKV_MAX_CAPACITY));
+    const int per_head = chunks_of(c.prefix_len, max_cap, kAttnMinThreads);
+    p.ml.compute(p.BH, c.head_dim, p.BH * per_head);
+    // partial (max, sum, weighted V) of every chunk table entry
+    p.ws_bytes = align_up((size_t)p.BH * per_head * (c.head_dim + 2) * sizeof(float), 256);
     return p;
 }
 
-// Attention splits per head: one block per head when the layer has at least
-// as many heads as compute units, else enough splits to fill the chip (each
-// split at least 256 tokens).
-int attn_splits(int BH, int max_len) {
-    if (BH >= kCus) return 1;
-    int s = (kCus + BH - 1) / BH;
-    s = std::min(s, (max_len + 255) / 256);
-    return std::max(1, std::min(s, kMaxSplits));
+// Block size of a chunk table for the given capacities: the fewest rounds of
+// resident blocks, then the largest blocks (fewest partial results).
+int pick_chunk_threads(int C, const std::vector<int>& cap) {
+    int best = kAttnMaxThreads;
+    long long best_rounds = -1;
+    for (int t = kAttnMaxThreads; t >= kAttnMinThreads; t /= 2) {
+        long long items = 0;
+        for (int x : cap) items += chunks_of(C, x, t);
+        const long long slots = attn_resident_blocks(t);
+        const long long rounds = (items + slots - 1) / slots;
+        if (best_rounds < 0 || rounds < best_rounds) {
+            best = t;
+            best_rounds = rounds;
+        }
+    }
+    return best;
 }
 
 headkv_status check_layer(headkv_t h, int32_t layer) {
@@ -211,8 +237,11 @@ headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c, con
     L.cap.assign(h->shape.BH, h->dense_cap);
     L.budget.assign(h->shape.BH, 0);
     L.label_local.assign(h->shape.BH, 0);
+    L.chunk_threads = pick_chunk_threads(c.prefix_len, L.cap);
+    const int dense_chunks = chunks_of(c.prefix_len, h->dense_cap, L.chunk_threads);
+    L.items = h->shape.BH * dense_chunks;
     st = hip_status(launch_prefill(dev_of(h, L), h->shape, k_c, v_c, h->dense_seg, h->dense_cap,
-                                   stream),
+                                   dense_chunks, stream),
                     "prefill launch");
     if (st) return st;
     L.prefilled = true;
@@ -264,8 +293,18 @@ void commit_append(headkv_t h, Layer& L, int32_t step, bool update) {
 
 int max_cap(const Layer& L) { return *std::max_element(L.cap.begin(), L.cap.end()); }
 
-int max_len(headkv_t h, const Layer& L) {
-    return h->cfg.prefix_len + *std::max_element(L.n.begin(), L.n.end());
+// How an attention launch covers the layer.
+//  - Fewer heads than CUs: the layer's chunk table, chunks of one pass
+//    balanced across heads of unequal length, merged by a second kernel.
+//  - Otherwise one block per head over all its passes (no merge, the append
+//    fused), the largest block size at which every head's block is resident
+//    at once; beyond that, 256-thread blocks, longest heads first.
+AttnPlan plan_attn(headkv_t h, const Layer& L) {
+    const int BH = h->shape.BH;
+    if (BH < kCus) return AttnPlan{L.chunk_threads, 1, L.items, 0};
+    for (int t = kAttnMaxThreads; t >= kAttnMinThreads; t /= 2)
+        if (BH <= attn_resident_blocks(t)) return AttnPlan{t, 0, BH, 0};
+    return AttnPlan{kAttnMinThreads, 0, BH, 1};
 }
 
 }  // namespace
@@ -371,7 +410,6 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
     if (!L.grouped && step == h->t_g)
         return fail(HEADKV_ERR_STATE, "the grouping step needs the separate calls");
     LayerDev D = dev_of(h, L);
-    const int splits = attn_splits(h->shape.BH, max_len(h, L) + 1);
     AppendArgs none = a;
     none.k = none.v = none.q = nullptr;
     float* ws = static_cast<float*>(h->ws);
@@ -384,24 +422,20 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
         if (st) return st;
         commit_append(h, L, step, update);
         take_events(h, time_it, HEADKV_TIMED_ATTN, attn_bytes(h, L), &e0, &e1);
-        return hip_status(launch_attn(D, h->shape, none, q, out, ws, splits, stream, e0, e1),
+        return hip_status(launch_attn(D, h->shape, none, q, out, ws, plan_attn(h, L),
+                                      stream, e0, e1),
                           "attention launch");
     }
-    if (splits == 1) {
-        take_events(h, time_it, HEADKV_TIMED_ATTN_APPEND, fused_step_bytes(h, L, a.accumulate != 0),
-                    &e0, &e1);
-        st = hip_status(launch_attn(D, h->shape, a, q, out, ws, 1, stream, e0, e1),
-                        "append + attention launch");
-        if (st) return st;
-        commit_append(h, L, step, update);
-        return ok();
-    }
-    st = hip_status(launch_append(D, h->shape, a, stream), "append launch");
+    // the append is fused into the attention (its length committed by the
+    // attention block or by the merge kernel)
+    take_events(h, time_it, HEADKV_TIMED_ATTN_APPEND, fused_step_bytes(h, L, a.accumulate != 0),
+                &e0, &e1);
+    st = hip_status(launch_attn(D, h->shape, a, q, out, ws, plan_attn(h, L),
+                                stream, e0, e1),
+                    "append + attention launch");
     if (st) return st;
     commit_append(h, L, step, update);
-    take_events(h, time_it, HEADKV_TIMED_ATTN, attn_bytes(h, L), &e0, &e1);
-    return hip_status(launch_attn(D, h->shape, none, q, out, ws, splits, stream, e0, e1),
-                      "attention launch");
+    return ok();
 }
 
 }  // namespace
@@ -529,6 +563,7 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     // segments: prefix + min(budget + P, N) slots each, in head order
     std::vector<int64_t> off(BH);
     std::vector<int32_t> cap(BH);
+    std::vector<int> cap_i(BH);
     size_t total = 0;
     for (int i = 0; i < BH; ++i) {
         if (bud[i] < 1 || bud[i] > c.num_visual)
@@ -536,6 +571,7 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
         cap[i] = std::min(bud[i] + c.period, c.num_visual);
         if (cap[i] > HEADKV_MAX_CAPACITY)
             return fail(HEADKV_ERR_UNSUPPORTED, "budget + period exceeds HEADKV_MAX_CAPACITY");
+        cap_i[i] = cap[i];
         off[i] = (int64_t)total;
         total += segment_bytes(c.prefix_len, cap[i], c.head_dim);
     }
@@ -547,12 +583,24 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     std::vector<int32_t> order(BH);
     for (int i = 0; i < BH; ++i) order[i] = i;
     std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cap[a] > cap[b]; });
+    // chunk table of the new layout, the chunks of a head contiguous
+    const int chunk_threads = pick_chunk_threads(c.prefix_len, cap_i);
+    std::vector<uint32_t> items;
+    std::vector<int32_t> item_start(BH + 1);
+    for (int i = 0; i < BH; ++i) {
+        item_start[i] = (int32_t)items.size();
+        const int nc = chunks_of(c.prefix_len, cap[i], chunk_threads);
+        for (int k = 0; k < nc; ++k) items.push_back(((uint32_t)i << 8) | (uint32_t)k);
+    }
+    item_start[BH] = (int32_t)items.size();
     // tables of the new layout (the host vectors outlive the copies: the stream
     // is waited for below on every path)
     char* mb = static_cast<char*>(L.meta);
     st = hip_status(hipMemcpyAsync(mb + h->ml.seg_off, off.data(), sizeof(int64_t) * BH, hipMemcpyHostToDevice, s), "table upload");
     if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.cap, cap.data(), sizeof(int32_t) * BH, hipMemcpyHostToDevice, s), "table upload");
     if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.order, order.data(), sizeof(int32_t) * BH, hipMemcpyHostToDevice, s), "table upload");
+    if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.items, items.data(), sizeof(uint32_t) * items.size(), hipMemcpyHostToDevice, s), "table upload");
+    if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.item_start, item_start.data(), sizeof(int32_t) * (BH + 1), hipMemcpyHostToDevice, s), "table upload");
     // first update, fused with the move from the dense buffer into the segments
     if (!st) {
         LayerDev Dnew = make_layer_dev(ragged_kv, L.meta, h->ml);
@@ -570,6 +618,8 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     L.budget.assign(bud.begin(), bud.end());
     L.label_local.assign(lab.begin(), lab.end());
     L.cap.assign(cap.begin(), cap.end());
+    L.chunk_threads = chunk_threads;
+    L.items = (int)items.size();
     for (int i = 0; i < BH; ++i) L.n[i] = std::min(L.n[i], L.budget[i]);
     return ok();
 }
@@ -585,7 +635,7 @@ headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, f
         return fail(HEADKV_ERR_STATE, "assign_budgets must run before attention at step group_threshold - 1");
     AppendArgs none{};
     return hip_status(launch_attn(dev_of(h, L), h->shape, none, q, out, static_cast<float*>(h->ws),
-                                  attn_splits(h->shape.BH, max_len(h, L)), stream),
+                                  plan_attn(h, L), stream),
                       "attention launch");
 }
 

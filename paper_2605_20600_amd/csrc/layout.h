@@ -16,11 +16,18 @@
 
 namespace headkv {
 
-constexpr int kBlock = 256;         // threads per block of the cache kernels
-constexpr int kAttnThreads = 1024;  // threads per attention block (one head or split)
-constexpr int kAttnTpr = 8;         // tokens per 16-lane row per attention pass
-constexpr int kMaxSplits = 8;       // attention splits per head (layers with few heads)
-constexpr int kCus = 256;           // MI355X compute units
+constexpr int kBlock = 256;  // threads per block of the cache kernels
+constexpr int kAttnTpr = 8;  // tokens per 16-lane row per attention pass
+constexpr int kCus = 256;    // MI355X compute units
+// Attention blocks have 1024, 512 or 256 threads; 1024 threads of at most 128
+// VGPRs fill a CU, so a CU holds 1024 / threads blocks at once.
+constexpr int kAttnMinThreads = 256;
+constexpr int kAttnMaxThreads = 1024;
+inline constexpr int attn_tokens_per_pass(int threads) { return threads / 16 * kAttnTpr; }
+inline constexpr int attn_resident_blocks(int threads) { return kCus * (kAttnMaxThreads / threads); }
+// Chunks per head in a chunk table: bounded so that the chunk index fits in
+// the 8 low bits of a table entry.
+constexpr int kMaxChunksPerHead = 255;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -29,9 +36,13 @@ inline size_t segment_bytes(int C, int cap, int d) {
 }
 
 struct MetaLayout {
-    size_t seg_off, cap, n, budget, nstar, label, order, qsum, total;
+    size_t seg_off, cap, n, budget, nstar, label, order, qsum, items, item_start, total;
+    int max_items;
 
-    void compute(int BH, int d) {
+    // max_items: largest chunk table of a layer (every head at its largest
+    // capacity, in chunks of the smallest attention pass).
+    void compute(int BH, int d, int max_items_) {
+        max_items = max_items_;
         size_t o = 0;
         auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
         seg_off = take(sizeof(int64_t) * BH);
@@ -42,6 +53,8 @@ struct MetaLayout {
         label = take(sizeof(int32_t) * BH);
         order = take(sizeof(int32_t) * BH);
         qsum = take(sizeof(double) * (size_t)BH * d);
+        items = take(sizeof(uint32_t) * (size_t)max_items);
+        item_start = take(sizeof(int32_t) * ((size_t)BH + 1));
         total = o;
     }
 };
@@ -57,6 +70,10 @@ struct LayerDev {
     int32_t* label;       // 1 = local head
     int32_t* order;       // attention dispatch order of the heads (longest first)
     double* qsum;         // [BH][d] running sum of the queries of this window
+    // chunk table: entry = head << 8 | chunk, the chunks of a head contiguous;
+    // head h owns entries item_start[h] .. item_start[h+1]-1
+    uint32_t* items;
+    int32_t* item_start;  // [BH + 1]
 };
 
 inline LayerDev make_layer_dev(void* kv, void* meta, const MetaLayout& m) {
@@ -71,10 +88,13 @@ inline LayerDev make_layer_dev(void* kv, void* meta, const MetaLayout& m) {
     L.label = reinterpret_cast<int32_t*>(b + m.label);
     L.order = reinterpret_cast<int32_t*>(b + m.order);
     L.qsum = reinterpret_cast<double*>(b + m.qsum);
+    L.items = reinterpret_cast<uint32_t*>(b + m.items);
+    L.item_start = reinterpret_cast<int32_t*>(b + m.item_start);
     return L;
 }
 
-// Launchers (kernels.hip).  All return hipGetLastError() as an int.
+// Launchers (cache_kernels.hip, attn_kernels.hip).  All return
+// hipGetLastError() as an int.
 struct Shape {
     int BH, B, H, d, C, N;
 };
@@ -89,8 +109,9 @@ struct AppendArgs {
     int reset;           // the query sum restarts with this q
 };
 
+// Also writes the dense layout's chunk table: dense_chunks chunks per head.
 int launch_prefill(const LayerDev& L, const Shape& s, const uint16_t* kc, const uint16_t* vc,
-                   int64_t dense_seg_bytes, int dense_cap, void* stream);
+                   int64_t dense_seg_bytes, int dense_cap, int dense_chunks, void* stream);
 int launch_append(const LayerDev& L, const Shape& s, const AppendArgs& a, void* stream);
 int launch_score(const LayerDev& L, const Shape& s, const uint16_t* q, int32_t* n_star,
                  uint8_t* is_local, int len, double sqrt_d, double tau, int local_window,
@@ -106,11 +127,19 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
                   void* ev_stop);
 // Dynamic LDS of one update block.
 size_t update_lds_bytes(int N, int cap, int d);
-// a.k == nullptr: no append (only allowed with splits == 1 otherwise).
+// How one attention launch covers a layer.
+struct AttnPlan {
+    int threads;    // 1024, 512 or 256
+    int chunked;    // 0: one block per head, every pass; 1: one block per entry
+                    //    of the chunk table (chunks of one pass) + merge kernel
+    int items;      // entries of the chunk table (chunked)
+    int use_order;  // one block per head: longest heads first
+};
+// a.k == nullptr: no append.  partials: (d + 2) floats per table entry.
 // ev_start / ev_stop (hipEvent_t or nullptr) receive the attention kernel's
 // own start and end timestamps.
 int launch_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
-                float* out, float* partials, int splits, void* stream,
+                float* out, float* partials, const AttnPlan& p, void* stream,
                 void* ev_start = nullptr, void* ev_stop = nullptr);
 int launch_export(const LayerDev& L, const Shape& s, uint8_t* mask, int32_t* count,
                   void* stream);

@@ -155,14 +155,20 @@ def test_lumina768_separate_calls():
     _run_and_check(wl, [5], [(5, 3)], _steps(wl), fused=False, all_heads=False)
 
 
+def test_lumina1024_separate_calls():
+    # fewer heads than CUs: the chunked attention without a fused append
+    wl = W.LUMINA1024
+    _run_and_check(wl, [7], [(7, 2)], _steps(wl), fused=False, all_heads=False)
+
+
 def test_janus7b_total_budget_sampled():
     wl = W.JANUS7B
     _run_and_check(wl, [0, 29], [(0, 0), (29, 15)], _steps(wl, extra=(200, 400)))
 
 
 def test_lumina1024_override_split_heads():
-    # 4 x 32 = 128 heads per layer < 256 compute units: each head is split over
-    # several blocks and merged
+    # 4 x 32 = 128 heads per layer < 256 compute units: each head is cut into
+    # chunks of one pass by the layer's chunk table and merged
     wl = W.LUMINA1024
     _run_and_check(wl, [0, 31], [(0, 0), (31, 3)], _steps(wl, extra=(2000, 3000)))
 
