@@ -38,6 +38,14 @@ def parse():
     p.add_argument("--workload", default="lumina_mgpt_768",
                    help="lumina_mgpt_768 (default), janus_pro_7b, lumina_mgpt_1024, "
                         "stress_768_b64_p1 or tiny")
+    p.add_argument("--attn-strategy", default="varlen", choices=["varlen", "padded", "grouped"],
+                   help="attention over heads of unequal length: per-head lengths (default), "
+                        "every head padded to the layer's longest with a mask, or one launch "
+                        "per head group")
+    p.add_argument("--method", default="headkv", choices=["headkv", "uniform", "full"],
+                   help="headkv (default); uniform: every head labelled global, budget rho*N "
+                        "for all (the line-based baseline's uniform allocation); full: every "
+                        "budget N, no eviction (full cache)")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="approximate CPU work of the oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -211,6 +219,8 @@ def main():
     wl = W.ALL[args.workload]
     if args.rho is not None:
         wl = wl.with_(rho=tuple(int(x) for x in args.rho.split("/")))
+    if args.method == "full":
+        wl = wl.with_(budget_mode=W.BUDGET_OVERRIDE)
     rho_s = f"{wl.rho[0]}/{wl.rho[1]}"
     dev = torch.cuda.current_device()
     torch.cuda.set_device(dev)
@@ -219,12 +229,20 @@ def main():
     torch.cuda.synchronize()
     print(f"# inputs: {inp.nbytes() / 1e9:.2f} GB on device in {time.perf_counter() - t0:.1f} s",
           file=sys.stderr, flush=True)
-    sess = new_session(wl)
+    labels = None
+    if args.method == "full":
+        for l in inp.layers:
+            inp.override[l] = torch.full((wl.batch * wl.heads,), wl.num_visual, dtype=torch.int32,
+                                         device="cuda")
+    elif args.method == "uniform":
+        labels = {l: torch.zeros(wl.batch * wl.heads, dtype=torch.uint8, device="cuda")
+                  for l in inp.layers}
+    sess = new_session(wl, attn_strategy=B.ATTN_STRATEGIES[args.attn_strategy])
     outs = {l: torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32, device="cuda")
             for l in inp.layers}
 
     for i in range(args.warmup):
-        run_generation_native(sess, inp, outs)
+        run_generation_native(sess, inp, outs, label_override=labels)
         torch.cuda.synchronize()
         print(f"# warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
 
@@ -237,7 +255,8 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
-        run_generation_native(sess, inp, outs, timing_every=args.timing_every)
+        run_generation_native(sess, inp, outs, timing_every=args.timing_every,
+                              label_override=labels)
         print(f"# step {i + 1}/{args.steps} issued", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
@@ -291,6 +310,7 @@ def main():
             "head_dim": wl.head_dim, "prefix_tokens": wl.prefix_len,
             "visual_tokens": wl.num_visual, "rho": rho_s,
             "budget_mode": ["paper", "override", "layer_total"][wl.budget_mode],
+            "method": args.method, "attn_strategy": args.attn_strategy,
             "period": wl.period,
             "group_threshold": wl.group_threshold, "recent_window": wl.recent_len,
             "kv_storage": "bf16", "accumulate": "fp32 (attention), fp64 (grouping, eviction)",
@@ -302,6 +322,7 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": (measured_traffic() if wl.name == "lumina_mgpt_768" and rho_s == "1/8"
+                        and args.method == "headkv" and args.attn_strategy == "varlen"
                         and dominant == names[0] else None),
             "kernel": dominant.replace("<d", f"<{wl.head_dim}"),
             "timed_every_nth_step": args.timing_every,

@@ -63,6 +63,19 @@ typedef int32_t headkv_status;
                                     local heads recent_len, global heads an
                                     equal share in whole rows, >= recent_len */
 
+/* Attention strategies for heads of unequal length, the three of Sec. 5.1
+ * (Implementation Details) and Sec. 5.3 (Efficiency Analysis).  All give the
+ * same outputs (up to fp32 summation order) and the same retained sets. */
+#define HEADKV_ATTN_VARLEN 0  /* each head attends over its own length */
+#define HEADKV_ATTN_PADDED 1  /* after grouping every head's segment has the
+                                 layer's largest capacity, and every head reads
+                                 the layer's longest length with the rows past
+                                 its own length masked (Appendix, padding-based
+                                 strategy) */
+#define HEADKV_ATTN_GROUPED 2 /* one attention launch per head group (global
+                                 heads, then local heads), written into one
+                                 output */
+
 /* Limits of this build. */
 #define HEADKV_MAX_VISUAL 16384  /* num_visual */
 #define HEADKV_MAX_PREFIX 2048   /* prefix_len */
@@ -84,6 +97,7 @@ typedef struct headkv_config {
     int32_t budget_mode;     /* HEADKV_BUDGET_* */
     int32_t rho_num, rho_den;/* rho = rho_num / rho_den in (0, 1] */
     int32_t rs_num, rs_den;  /* r_s = rs_num / rs_den in [0, 1] (Eq. 5) */
+    int32_t attn_strategy;   /* HEADKV_ATTN_*; HEADKV_ATTN_VARLEN by default */
     double tau;              /* grouping mass threshold in (0, 1], 0.9 */
 } headkv_config;
 
@@ -93,10 +107,11 @@ typedef struct headkv_ctx* headkv_t;
  *   dense_kv_bytes: per layer, the cache before grouping (every head holds
  *                   its prefix and up to group_threshold visual tokens);
  *   meta_bytes:     per layer, segment table, lengths, labels, budgets,
- *                   query sums and the attention dispatch order;
+ *                   query sums, the attention dispatch order and the
+ *                   attention chunk table;
  *   workspace_bytes: one buffer shared by all layers: attention partials of
- *                   layers with fewer heads than compute units, which split
- *                   each head over several blocks. */
+ *                   layers with fewer heads than compute units, which cut
+ *                   each head into chunks of one pass. */
 headkv_status headkv_plan(const headkv_config* cfg, size_t* dense_kv_bytes,
                           size_t* meta_bytes, size_t* workspace_bytes);
 
@@ -142,8 +157,9 @@ headkv_status headkv_score_heads(headkv_t h, int32_t layer, const uint16_t* q,
  * budget_override: [B][H] int32 (device) for HEADKV_BUDGET_OVERRIDE, else
  * NULL.  budgets: [B][H] int32 output (device), visual tokens per head, the
  * recent window included and the prefix not counted.
- * Each head then needs prefix_len + min(budget + period, N) slots; the total,
- * with alignment, is written to *ragged_bytes_needed.  If ragged_kv is NULL
+ * Each head then needs prefix_len + min(budget + period, N) slots (with
+ * HEADKV_ATTN_PADDED, the largest of these for every head of the layer); the
+ * total, with alignment, is written to *ragged_bytes_needed.  If ragged_kv is NULL
  * or ragged_bytes is smaller, the call returns HEADKV_ERR_CAPACITY after
  * setting *ragged_bytes_needed and changes no state: allocate and call again.
  * Otherwise the first update runs (Eqs. 2-6), the retained tokens are copied

@@ -23,6 +23,12 @@ HEADKV_BUDGET_PAPER = 0
 HEADKV_BUDGET_OVERRIDE = 1
 HEADKV_BUDGET_TOTAL = 2
 
+HEADKV_ATTN_VARLEN = 0
+HEADKV_ATTN_PADDED = 1
+HEADKV_ATTN_GROUPED = 2
+ATTN_STRATEGIES = {"varlen": HEADKV_ATTN_VARLEN, "padded": HEADKV_ATTN_PADDED,
+                   "grouped": HEADKV_ATTN_GROUPED}
+
 EXPORTED = (
     "headkv_plan", "headkv_create", "headkv_destroy", "headkv_prefill",
     "headkv_append_and_evict", "headkv_score_heads", "headkv_assign_budgets",
@@ -42,6 +48,7 @@ class HeadKVConfig(ctypes.Structure):
         ("group_threshold", ctypes.c_int32), ("budget_mode", ctypes.c_int32),
         ("rho_num", ctypes.c_int32), ("rho_den", ctypes.c_int32),
         ("rs_num", ctypes.c_int32), ("rs_den", ctypes.c_int32),
+        ("attn_strategy", ctypes.c_int32),
         ("tau", ctypes.c_double),
     ]
 

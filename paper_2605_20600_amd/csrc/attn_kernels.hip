@@ -4,7 +4,10 @@
 //   k_attn   one block per work item.  A work item is either a whole head
 //            (every pass over its tokens) or one chunk of a head of at most
 //            one pass, taken from the layer's chunk table; optionally fused
-//            with the step's append.
+//            with the step's append.  Whole heads may come from a range of the
+//            dispatch order (one head group per launch) and may read up to a
+//            padded length with the rows past their own length masked (the
+//            other two strategies of Sec. 5.1 for heads of unequal length).
 //   k_merge  merge of the chunks of every head of a chunked launch, and the
 //            commit of the fused append's length.
 //
@@ -54,7 +57,7 @@ __device__ __forceinline__ Words<NW> nt_load(const uint16_t* p) {
 template <int D, bool APPEND, int T, bool CHUNKED>
 __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_attn(
     LayerDev L, int C, AppendArgs a, const uint16_t* __restrict__ q, float* __restrict__ out,
-    float* __restrict__ part, int use_order, float qscale) {
+    float* __restrict__ part, int use_order, int order_base, int pad_len, float qscale) {
     using Vec = typename AttnRegs<D>::Vec;
     constexpr int VPL = AttnRegs<D>::VPL;
     constexpr int NW = AttnRegs<D>::NW;
@@ -67,7 +70,7 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
         h = (int)(it >> 8);
         t_begin = (int)(it & 255u) * TP;
     } else {
-        h = use_order ? L.order[blockIdx.x] : (int)blockIdx.x;
+        h = use_order ? L.order[order_base + (int)blockIdx.x] : (int)blockIdx.x;
         t_begin = 0;
     }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -76,6 +79,8 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
     const int n = L.n[h];
     const int len = C + n + (APPEND ? 1 : 0);
     const int t_end = CHUNKED ? min(len, t_begin + TP) : len;
+    // padding strategy: rows up to pad_len are read, those past len masked
+    const int t_stop = CHUNKED ? t_end : max(len, pad_len);
     // the block whose range holds the new token (always the one block of a head
     // that is not chunked) performs the append
     const bool owner = APPEND && (!CHUNKED || (t_begin <= len - 1 && len - 1 < t_end));
@@ -93,11 +98,11 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
     for (int e = 0; e < VPL; ++e) acc[e] = 0.f;
     float qf[VPL];
     bool q_ready = false;
-    for (int t0 = t_begin; t0 < t_end; t0 += TP) {
+    for (int t0 = t_begin; t0 < t_stop; t0 += TP) {
         Vec kk[kAttnTpr], vv[kAttnTpr];
 #pragma unroll
         for (int j = 0; j < kAttnTpr; ++j) {
-            const int tok = min(t0 + j * ROWS + row, t_end - 1);
+            const int tok = min(t0 + j * ROWS + row, t_stop - 1);
             const uint16_t* kp = K + (size_t)tok * D;
             const uint16_t* vp = V + (size_t)tok * D;
             if (APPEND && tok == len - 1) {
@@ -234,14 +239,16 @@ void attn_launch(const LayerDev& L, const Shape& s, const AppendArgs& a, const u
                  float* out, float* partials, const AttnPlan& p, hipStream_t st, hipEvent_t ev0,
                  hipEvent_t ev1) {
     const float qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
-    const dim3 grid(CHUNKED ? p.items : s.BH), block(T);
+    const dim3 grid(CHUNKED ? p.items : p.heads), block(T);
     // with events, they take the kernel's own start and end timestamps
     if (a.k != nullptr)
         hipExtLaunchKernelGGL((k_attn<D, true, T, CHUNKED>), grid, block, 0, st, ev0, ev1, 0, L,
-                              s.C, a, q, out, partials, p.use_order, qscale);
+                              s.C, a, q, out, partials, p.use_order, p.order_base, p.pad_len,
+                              qscale);
     else
         hipExtLaunchKernelGGL((k_attn<D, false, T, CHUNKED>), grid, block, 0, st, ev0, ev1, 0, L,
-                              s.C, a, q, out, partials, p.use_order, qscale);
+                              s.C, a, q, out, partials, p.use_order, p.order_base, p.pad_len,
+                              qscale);
     if (CHUNKED)
         hipLaunchKernelGGL(k_merge<D>, dim3(s.BH), dim3(D), 0, st, L, out, partials,
                            a.k != nullptr ? 1 : 0);

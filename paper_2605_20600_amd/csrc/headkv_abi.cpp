@@ -44,6 +44,8 @@ struct Layer {
     std::vector<uint8_t> label_local;  // labels used by the updates (host copy)
     int chunk_threads = kAttnMaxThreads;  // block size the chunk table is cut for
     int items = 0;                        // entries of the chunk table
+    int n_global = 0;                     // global heads (first in the dispatch
+                                          // order with HEADKV_ATTN_GROUPED)
 };
 
 }  // namespace
@@ -99,6 +101,8 @@ headkv_status validate_config(const headkv_config* c) {
     if (c->rs_num < 0 || c->rs_den < 1 || c->rs_num > c->rs_den)
         return fail(HEADKV_ERR_INVALID_ARG, "r_s must be in [0, 1]");
     if (!(c->tau > 0.0 && c->tau <= 1.0)) return fail(HEADKV_ERR_INVALID_ARG, "tau must be in (0, 1]");
+    if (c->attn_strategy < HEADKV_ATTN_VARLEN || c->attn_strategy > HEADKV_ATTN_GROUPED)
+        return fail(HEADKV_ERR_INVALID_ARG, "unknown attn_strategy");
     // chunk indices must fit the 8 bits of a chunk table entry (always true
     // within the prefix and capacity limits)
     const int max_cap = std::max(c->group_threshold, std::min(c->num_visual, HEADKV_MAX_CAPACITY));
@@ -293,18 +297,62 @@ void commit_append(headkv_t h, Layer& L, int32_t step, bool update) {
 
 int max_cap(const Layer& L) { return *std::max_element(L.cap.begin(), L.cap.end()); }
 
-// How an attention launch covers the layer.
-//  - Fewer heads than CUs: the layer's chunk table, chunks of one pass
-//    balanced across heads of unequal length, merged by a second kernel.
-//  - Otherwise one block per head over all its passes (no merge, the append
-//    fused), the largest block size at which every head's block is resident
-//    at once; beyond that, 256-thread blocks, longest heads first.
-AttnPlan plan_attn(headkv_t h, const Layer& L) {
-    const int BH = h->shape.BH;
-    if (BH < kCus) return AttnPlan{L.chunk_threads, 1, L.items, 0};
+// Largest block size at which `heads` one-block-per-head blocks are all
+// resident at once (256 beyond that; 1024 when they do not fill the CUs).
+int resident_threads(int heads) {
     for (int t = kAttnMaxThreads; t >= kAttnMinThreads; t /= 2)
-        if (BH <= attn_resident_blocks(t)) return AttnPlan{t, 0, BH, 0};
-    return AttnPlan{kAttnMinThreads, 0, BH, 1};
+        if (heads <= attn_resident_blocks(t)) return t;
+    return kAttnMinThreads;
+}
+
+// The attention launches of one layer step (appended: the step's token is
+// attended from the input).  Returns their number (1 or 2).
+//  VARLEN, fewer heads than CUs: the layer's chunk table, chunks of one pass
+//    balanced across heads of unequal length, merged by a second kernel.
+//  VARLEN otherwise: one block per head over all its passes (no merge, the
+//    append fused), at the largest block size at which every head's block is
+//    resident at once; beyond that 256-thread blocks, longest heads first.
+//  PADDED: one block per head, every head reading the layer's longest length.
+//  GROUPED (after grouping): one launch per non-empty group, global heads
+//    first, each like VARLEN's one block per head over its own heads.
+int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
+    const int BH = h->shape.BH;
+    const int strategy = h->cfg.attn_strategy;
+    if (strategy == HEADKV_ATTN_PADDED) {
+        const int n_max = *std::max_element(L.n.begin(), L.n.end());
+        out[0] = AttnPlan{resident_threads(BH), 0, 0, BH, 0, 0,
+                          h->cfg.prefix_len + n_max + (appended ? 1 : 0)};
+        return 1;
+    }
+    if (strategy == HEADKV_ATTN_GROUPED && L.grouped) {
+        int k = 0;
+        const int sizes[2] = {L.n_global, BH - L.n_global};
+        for (int g = 0, base = 0; g < 2; base += sizes[g], ++g)
+            if (sizes[g] > 0) out[k++] = AttnPlan{resident_threads(sizes[g]), 0, 0, sizes[g], 1, base, 0};
+        return k;
+    }
+    if (BH < kCus) {
+        out[0] = AttnPlan{L.chunk_threads, 1, L.items, BH, 0, 0, 0};
+        return 1;
+    }
+    const int t = resident_threads(BH);
+    out[0] = AttnPlan{t, 0, 0, BH, BH > attn_resident_blocks(t) ? 1 : 0, 0, 0};
+    return 1;
+}
+
+// Launches the attention of a layer step; the event pair brackets the first
+// kernel's start and the last kernel's end.
+int launch_attention(headkv_t h, const Layer& L, const LayerDev& D, const AppendArgs& a,
+                     const uint16_t* q, float* out, void* stream, void* e0, void* e1) {
+    AttnPlan plans[2];
+    const int np = attn_plans(h, L, a.k != nullptr, plans);
+    float* ws = static_cast<float*>(h->ws);
+    for (int i = 0; i < np; ++i) {
+        const int e = launch_attn(D, h->shape, a, q, out, ws, plans[i], stream, i == 0 ? e0 : nullptr,
+                                  i == np - 1 ? e1 : nullptr);
+        if (e) return e;
+    }
+    return 0;
 }
 
 }  // namespace
@@ -412,7 +460,6 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
     LayerDev D = dev_of(h, L);
     AppendArgs none = a;
     none.k = none.v = none.q = nullptr;
-    float* ws = static_cast<float*>(h->ws);
     void *e0, *e1;
     if (update) {
         take_events(h, time_it, HEADKV_TIMED_UPDATE, update_bytes(h, L), &e0, &e1);
@@ -422,16 +469,14 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
         if (st) return st;
         commit_append(h, L, step, update);
         take_events(h, time_it, HEADKV_TIMED_ATTN, attn_bytes(h, L), &e0, &e1);
-        return hip_status(launch_attn(D, h->shape, none, q, out, ws, plan_attn(h, L),
-                                      stream, e0, e1),
+        return hip_status(launch_attention(h, L, D, none, q, out, stream, e0, e1),
                           "attention launch");
     }
     // the append is fused into the attention (its length committed by the
     // attention block or by the merge kernel)
     take_events(h, time_it, HEADKV_TIMED_ATTN_APPEND, fused_step_bytes(h, L, a.accumulate != 0),
                 &e0, &e1);
-    st = hip_status(launch_attn(D, h->shape, a, q, out, ws, plan_attn(h, L),
-                                stream, e0, e1),
+    st = hip_status(launch_attention(h, L, D, a, q, out, stream, e0, e1),
                     "append + attention launch");
     if (st) return st;
     commit_append(h, L, step, update);
@@ -571,6 +616,12 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
         cap[i] = std::min(bud[i] + c.period, c.num_visual);
         if (cap[i] > HEADKV_MAX_CAPACITY)
             return fail(HEADKV_ERR_UNSUPPORTED, "budget + period exceeds HEADKV_MAX_CAPACITY");
+    }
+    if (c.attn_strategy == HEADKV_ATTN_PADDED) {  // every head padded to the largest
+        const int32_t cmax = *std::max_element(cap.begin(), cap.end());
+        std::fill(cap.begin(), cap.end(), cmax);
+    }
+    for (int i = 0; i < BH; ++i) {
         cap_i[i] = cap[i];
         off[i] = (int64_t)total;
         total += segment_bytes(c.prefix_len, cap[i], c.head_dim);
@@ -579,10 +630,16 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     if (!ragged_kv || ragged_bytes < total)
         return fail(HEADKV_ERR_CAPACITY, "ragged_kv is NULL or smaller than *ragged_bytes_needed");
     // attention dispatch order: longest heads first, so that when a layer
-    // needs more than one round of blocks the short heads fill the tail
+    // needs more than one round of blocks the short heads fill the tail; with
+    // HEADKV_ATTN_GROUPED the global heads, then the local heads
     std::vector<int32_t> order(BH);
     for (int i = 0; i < BH; ++i) order[i] = i;
-    std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cap[a] > cap[b]; });
+    if (c.attn_strategy == HEADKV_ATTN_GROUPED)
+        std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return lab[a] < lab[b]; });
+    else
+        std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return cap[a] > cap[b]; });
+    int n_global = 0;
+    for (int i = 0; i < BH; ++i) n_global += lab[i] ? 0 : 1;
     // chunk table of the new layout, the chunks of a head contiguous
     const int chunk_threads = pick_chunk_threads(c.prefix_len, cap_i);
     std::vector<uint32_t> items;
@@ -601,6 +658,9 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.order, order.data(), sizeof(int32_t) * BH, hipMemcpyHostToDevice, s), "table upload");
     if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.items, items.data(), sizeof(uint32_t) * items.size(), hipMemcpyHostToDevice, s), "table upload");
     if (!st) st = hip_status(hipMemcpyAsync(mb + h->ml.item_start, item_start.data(), sizeof(int32_t) * (BH + 1), hipMemcpyHostToDevice, s), "table upload");
+    // padded rows are read (and masked) by the attention: keep them finite
+    if (!st && c.attn_strategy == HEADKV_ATTN_PADDED)
+        st = hip_status(hipMemsetAsync(ragged_kv, 0, total, s), "ragged clear");
     // first update, fused with the move from the dense buffer into the segments
     if (!st) {
         LayerDev Dnew = make_layer_dev(ragged_kv, L.meta, h->ml);
@@ -620,6 +680,7 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     L.cap.assign(cap.begin(), cap.end());
     L.chunk_threads = chunk_threads;
     L.items = (int)items.size();
+    L.n_global = n_global;
     for (int i = 0; i < BH; ++i) L.n[i] = std::min(L.n[i], L.budget[i]);
     return ok();
 }
@@ -634,8 +695,7 @@ headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, f
     if (!L.grouped && L.last_step == h->t_g)
         return fail(HEADKV_ERR_STATE, "assign_budgets must run before attention at step group_threshold - 1");
     AppendArgs none{};
-    return hip_status(launch_attn(dev_of(h, L), h->shape, none, q, out, static_cast<float*>(h->ws),
-                                  plan_attn(h, L), stream),
+    return hip_status(launch_attention(h, L, dev_of(h, L), none, q, out, stream, nullptr, nullptr),
                       "attention launch");
 }
 

@@ -127,13 +127,17 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
                   void* ev_stop);
 // Dynamic LDS of one update block.
 size_t update_lds_bytes(int N, int cap, int d);
-// How one attention launch covers a layer.
+// How one attention launch covers a layer (or a group of its heads).
 struct AttnPlan {
-    int threads;    // 1024, 512 or 256
-    int chunked;    // 0: one block per head, every pass; 1: one block per entry
-                    //    of the chunk table (chunks of one pass) + merge kernel
-    int items;      // entries of the chunk table (chunked)
-    int use_order;  // one block per head: longest heads first
+    int threads;     // 1024, 512 or 256
+    int chunked;     // 0: one block per head, every pass; 1: one block per entry
+                     //    of the chunk table (chunks of one pass) + merge kernel
+    int items;       // entries of the chunk table (chunked)
+    int heads;       // blocks of a launch with one block per head
+    int use_order;   // one block per head: head = order[order_base + block]
+    int order_base;
+    int pad_len;     // one block per head: read rows up to this length, those
+                     // past the head's own length masked (0: none)
 };
 // a.k == nullptr: no append.  partials: (d + 2) floats per table entry.
 // ev_start / ev_stop (hipEvent_t or nullptr) receive the attention kernel's

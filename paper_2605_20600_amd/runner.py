@@ -99,11 +99,14 @@ def new_session(wl: Workload, layers: Optional[int] = None, **kw) -> Session:
 
 
 def run_generation_native(sess: Session, inp: DeviceInputs, outs: Dict[int, torch.Tensor],
-                          timing_every: int = 0) -> Dict:
+                          timing_every: int = 0,
+                          label_override: Optional[Dict[int, torch.Tensor]] = None) -> Dict:
     """The same generation with the step loop in the library (headkv_run_steps):
     steps before and after the grouping step run from one host call each; the
     grouping step uses the separate calls.  Needs the inputs of every layer of
-    the handle.  Returns labels, n* and budgets per layer."""
+    the handle.  label_override: per layer [B*H] uint8 labels that replace the
+    grouping's for the budgets and updates.  Returns labels, n* and budgets per
+    layer."""
     wl = inp.wl
     L = sess.cfg.num_layers
     assert inp.layers == list(range(L)), "the native loop runs every layer"
@@ -123,8 +126,10 @@ def run_generation_native(sess: Session, inp: DeviceInputs, outs: Dict[int, torc
         q = inp.q[l][t_g]
         sess.append_and_evict(l, t_g, q, inp.k[l][t_g], inp.v[l][t_g])
         n_star, is_local = sess.score_heads(l, q)
-        sess.assign_budgets(l, override=inp.override[l])
+        lab = None if label_override is None else label_override[l]
+        sess.assign_budgets(l, is_local=lab, override=inp.override[l])
         sess.decode_attn(l, q, outs[l])
-        res["n_star"][l], res["is_local"][l], res["budgets"][l] = n_star, is_local, sess.budgets[l]
+        res["n_star"][l], res["is_local"][l] = n_star, (is_local if lab is None else lab)
+        res["budgets"][l] = sess.budgets[l]
     B.headkv_run_steps(sess.h, t_g + 1, N, qp, kp, vp, stride, op, timing_every, st)
     return res

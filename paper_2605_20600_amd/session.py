@@ -14,7 +14,8 @@ from .workloads import Workload
 
 
 def make_config(wl: Workload, rho=None, budget_mode=None, r_s=None, tau=None,
-                layers: Optional[int] = None) -> B.HeadKVConfig:
+                layers: Optional[int] = None, attn_strategy: int = B.HEADKV_ATTN_VARLEN
+                ) -> B.HeadKVConfig:
     rho = wl.rho if rho is None else rho
     r_s = wl.r_s if r_s is None else r_s
     return B.HeadKVConfig(
@@ -25,7 +26,7 @@ def make_config(wl: Workload, rho=None, budget_mode=None, r_s=None, tau=None,
         group_threshold=wl.group_threshold,
         budget_mode=wl.budget_mode if budget_mode is None else budget_mode,
         rho_num=rho[0], rho_den=rho[1], rs_num=r_s[0], rs_den=r_s[1],
-        tau=wl.tau if tau is None else tau)
+        attn_strategy=attn_strategy, tau=wl.tau if tau is None else tau)
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:

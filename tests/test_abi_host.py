@@ -45,7 +45,7 @@ def test_plan_sizes_and_validation():
            dict(group_threshold=99999), dict(period=0), dict(tau=0.0), dict(tau=1.5),
            dict(rho_num=0), dict(rho_num=3, rho_den=2), dict(rs_num=3, rs_den=2),
            dict(budget_mode=7), dict(prefix_len=-1), dict(row_len=0), dict(recent_len=0),
-           dict(num_heads=2000)]
+           dict(num_heads=2000), dict(attn_strategy=3), dict(attn_strategy=-1)]
     for kw in bad:
         c = make_config(W.LUMINA768)
         for k, v in kw.items():
@@ -54,6 +54,18 @@ def test_plan_sizes_and_validation():
             B.headkv_plan(c)
         assert e.value.status in (B.HEADKV_ERR_INVALID_ARG, B.HEADKV_ERR_UNSUPPORTED), kw
         assert B.headkv_last_error() != ""
+
+
+def test_config_struct_matches_header():
+    # the binding's struct mirrors headkv_config field by field
+    src = open(HEADER).read()
+    body = src[src.index("typedef struct headkv_config {"):src.index("} headkv_config;")]
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    fields = []
+    for decl in re.findall(r"(int32_t|double)\s+([^;]+);", body):
+        fields += [(decl[0], n.strip()) for n in decl[1].split(",")]
+    ct = {"int32_t": ctypes.c_int32, "double": ctypes.c_double}
+    assert [(n, ct[t]) for t, n in fields] == list(B.HeadKVConfig._fields_)
 
 
 def _handle(wl=W.TINY):

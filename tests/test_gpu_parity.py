@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import oracle
-from paper_2605_20600_amd import synth, workloads as W
+from paper_2605_20600_amd import binding as B, synth, workloads as W
 from paper_2605_20600_amd.runner import (DeviceInputs, new_session, run_generation,
                                          run_generation_native)
 
@@ -53,16 +53,16 @@ def _steps(wl, extra=()):
     return sorted(x for x in s.union(extra) if 0 <= x < N)
 
 
-def _run_and_check(wl, layers, slices, steps, fused=True, all_heads=True):
+def _run_and_check(wl, layers, slices, steps, fused=True, all_heads=True, strategy=0):
     inp = DeviceInputs(wl, layers=layers)
-    sess = new_session(wl)
+    sess = new_session(wl, attn_strategy=strategy)
     res = run_generation(sess, inp, out_steps=steps, snap_steps=steps, fused=fused,
                          record_layers=sorted({l for l, _ in slices}))
     torch.cuda.synchronize()
     for (layer, b) in slices:
         worst, ref = _check_slice(wl, res, layer, b, steps)
         gaps = [st["min_gap"] for st in ref["stats"].values()]
-        _say(f"{wl.name} rho={wl.rho} fused={fused} layer {layer} b {b}: bit-exact; "
+        _say(f"{wl.name} rho={wl.rho} fused={fused} strategy={strategy} layer {layer} b {b}: bit-exact; "
              f"max err {worst:.2e}; min label margin "
              f"{np.abs(ref['mass_window'] - wl.tau).min():.2e}; min eviction score gap "
              f"{min(gaps):.2e}")
@@ -198,3 +198,38 @@ def test_native_step_loop(wl):
         for h in range(H):
             assert np.array_equal(mask[h].cpu().numpy(), ref["snaps"][h][0]), (l, h)
             assert np.abs(out[h] - ref["out"][h][N - 1]).max() <= ATOL
+
+
+STRATEGIES = [B.HEADKV_ATTN_PADDED, B.HEADKV_ATTN_GROUPED]
+STRATEGY_IDS = ["padded", "grouped"]
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES, ids=STRATEGY_IDS)
+@pytest.mark.parametrize("fused", [True, False])
+def test_tiny_strategies_every_step(strategy, fused):
+    # the paper's other two attention strategies give the oracle's outputs
+    wl = W.TINY
+    steps = list(range(wl.num_visual))
+    inp = DeviceInputs(wl)
+    sess = new_session(wl, attn_strategy=strategy)
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps, fused=fused)
+    torch.cuda.synchronize()
+    worst, _ = _check_slice(wl, res, 0, 0, steps)
+    _say(f"tiny strategy={strategy} fused={fused}: every step bit-exact, max err {worst:.3e}")
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES, ids=STRATEGY_IDS)
+def test_lumina768_strategies_sampled(strategy):
+    wl = W.LUMINA768
+    _run_and_check(wl, [3], [(3, 5)], _steps(wl, extra=(500,)), all_heads=False, strategy=strategy)
+
+
+@pytest.mark.parametrize("strategy", STRATEGIES, ids=STRATEGY_IDS)
+def test_lumina1024_strategies_sampled(strategy):
+    wl = W.LUMINA1024
+    _run_and_check(wl, [9], [(9, 1)], _steps(wl), all_heads=False, strategy=strategy)
+
+
+def test_janus7b_grouped_sampled():
+    wl = W.JANUS7B
+    _run_and_check(wl, [4], [(4, 9)], _steps(wl), all_heads=False, strategy=B.HEADKV_ATTN_GROUPED)
