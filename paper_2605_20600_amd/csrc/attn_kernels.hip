@@ -53,6 +53,48 @@ __device__ __forceinline__ Words<NW> nt_load(const uint16_t* p) {
     return w;
 }
 
+// Online-softmax update of one row's state with NT tokens t0 + j * ROWS + row
+// (those at or past t_end masked); k/v hold their d/16 elements of the lane.
+template <int D, int NT, int ROWS>
+__device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec (&kk)[NT],
+                                                const typename AttnRegs<D>::Vec (&vv)[NT],
+                                                int t0, int row, int t_end, const float* qf,
+                                                float& m, float& l, float* acc) {
+    constexpr int NW = AttnRegs<D>::NW;
+    constexpr int VPL = AttnRegs<D>::VPL;
+    float s[NT];
+    float mx = m;
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        float dp = 0.f;
+#pragma unroll
+        for (int e = 0; e < NW; ++e) {
+            dp += qf[2 * e] * bf_lo(kk[j].w[e]);
+            dp += qf[2 * e + 1] * bf_hi(kk[j].w[e]);
+        }
+        dp = row16_sum(dp);
+        s[j] = (t0 + j * ROWS + row < t_end) ? dp : -INFINITY;
+        mx = fmaxf(mx, s[j]);
+    }
+    if (mx != -INFINITY) {
+        const float f = __builtin_amdgcn_exp2f(m - mx);  // m = -inf gives 0
+        l *= f;
+#pragma unroll
+        for (int e = 0; e < VPL; ++e) acc[e] *= f;
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const float p = __builtin_amdgcn_exp2f(s[j] - mx);
+            l += p;
+#pragma unroll
+            for (int e = 0; e < NW; ++e) {
+                acc[2 * e] += p * bf_lo(vv[j].w[e]);
+                acc[2 * e + 1] += p * bf_hi(vv[j].w[e]);
+            }
+        }
+        m = mx;
+    }
+}
+
 // 4 wavefronts per SIMD (16 per CU) at every block size: at most 128 VGPRs.
 template <int D, bool APPEND, int T, bool CHUNKED>
 __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_attn(
@@ -86,6 +128,13 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
     const bool owner = APPEND && (!CHUNKED || (t_begin <= len - 1 && len - 1 < t_end));
     const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + L.seg_off[h]);
     const uint16_t* V = K + (size_t)(C + L.cap[h]) * D;
+    // K (or V) row of token `tok`: the step's new token comes from the input
+    auto krow = [&](int tok) {
+        return (APPEND && tok == len - 1) ? a.k + (size_t)h * D : K + (size_t)tok * D;
+    };
+    auto vrow = [&](int tok) {
+        return (APPEND && tok == len - 1) ? a.v + (size_t)h * D : V + (size_t)tok * D;
+    };
 
     // the append's loads go out before the K/V stream and its stores right
     // after (the attention reads the new token from the input, never from row
@@ -97,65 +146,38 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
 #pragma unroll
     for (int e = 0; e < VPL; ++e) acc[e] = 0.f;
     float qf[VPL];
-    bool q_ready = false;
-    for (int t0 = t_begin; t0 < t_stop; t0 += TP) {
+    // first pass: the append's store and q's conversion go between its loads
+    // and their first use
+    if (t_begin < t_stop) {  // a chunk past the head's length reads nothing
+        Vec kk[kAttnTpr], vv[kAttnTpr];
+#pragma unroll
+        for (int j = 0; j < kAttnTpr; ++j) {
+            const int tok = min(t_begin + j * ROWS + row, t_stop - 1);
+            kk[j] = nt_load<NW>(krow(tok) + col * VPL);
+            vv[j] = nt_load<NW>(vrow(tok) + col * VPL);
+        }
+        // keep every load of the pass ahead of its first use
+        __builtin_amdgcn_sched_barrier(0);
+        if (owner) append_store(L, C, D, h, n, a, av, tid);
+#pragma unroll
+        for (int e = 0; e < NW; ++e) {
+            qf[2 * e] = bf_lo(qraw.w[e]) * qscale;
+            qf[2 * e + 1] = bf_hi(qraw.w[e]) * qscale;
+        }
+        attn_accumulate<D, kAttnTpr, ROWS>(kk, vv, t_begin, row, t_end, qf, m, l, acc);
+    }
+    // further passes of a head longer than one pass
+    for (int t0 = t_begin + TP; t0 < t_stop; t0 += TP) {
         Vec kk[kAttnTpr], vv[kAttnTpr];
 #pragma unroll
         for (int j = 0; j < kAttnTpr; ++j) {
             const int tok = min(t0 + j * ROWS + row, t_stop - 1);
-            const uint16_t* kp = K + (size_t)tok * D;
-            const uint16_t* vp = V + (size_t)tok * D;
-            if (APPEND && tok == len - 1) {
-                kp = a.k + (size_t)h * D;
-                vp = a.v + (size_t)h * D;
-            }
-            kk[j] = nt_load<NW>(kp + col * VPL);
-            vv[j] = nt_load<NW>(vp + col * VPL);
+            kk[j] = nt_load<NW>(krow(tok) + col * VPL);
+            vv[j] = nt_load<NW>(vrow(tok) + col * VPL);
         }
-        // keep every load of the pass ahead of its first use
         __builtin_amdgcn_sched_barrier(0);
-        if (!q_ready) {
-            if (owner) append_store(L, C, D, h, n, a, av, tid);
-#pragma unroll
-            for (int e = 0; e < NW; ++e) {
-                qf[2 * e] = bf_lo(qraw.w[e]) * qscale;
-                qf[2 * e + 1] = bf_hi(qraw.w[e]) * qscale;
-            }
-            q_ready = true;
-        }
-        float s[kAttnTpr];
-        float mx = m;
-#pragma unroll
-        for (int j = 0; j < kAttnTpr; ++j) {
-            float dp = 0.f;
-#pragma unroll
-            for (int e = 0; e < NW; ++e) {
-                dp += qf[2 * e] * bf_lo(kk[j].w[e]);
-                dp += qf[2 * e + 1] * bf_hi(kk[j].w[e]);
-            }
-            dp = row16_sum(dp);
-            s[j] = (t0 + j * ROWS + row < t_end) ? dp : -INFINITY;
-            mx = fmaxf(mx, s[j]);
-        }
-        if (mx != -INFINITY) {
-            const float f = __builtin_amdgcn_exp2f(m - mx);  // m = -inf gives 0
-            l *= f;
-#pragma unroll
-            for (int e = 0; e < VPL; ++e) acc[e] *= f;
-#pragma unroll
-            for (int j = 0; j < kAttnTpr; ++j) {
-                const float p = __builtin_amdgcn_exp2f(s[j] - mx);
-                l += p;
-#pragma unroll
-                for (int e = 0; e < NW; ++e) {
-                    acc[2 * e] += p * bf_lo(vv[j].w[e]);
-                    acc[2 * e + 1] += p * bf_hi(vv[j].w[e]);
-                }
-            }
-            m = mx;
-        }
+        attn_accumulate<D, kAttnTpr, ROWS>(kk, vv, t0, row, t_end, qf, m, l, acc);
     }
-    if (owner && !q_ready) append_store(L, C, D, h, n, a, av, tid);  // not reached: len >= 1
     // merge the four rows of each wavefront
 #pragma unroll
     for (int off = 16; off <= 32; off <<= 1) {

@@ -318,17 +318,20 @@ int resident_threads(int heads) {
 int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
     const int BH = h->shape.BH;
     const int strategy = h->cfg.attn_strategy;
+    const int len_max = h->cfg.prefix_len + *std::max_element(L.n.begin(), L.n.end()) +
+                        (appended ? 1 : 0);
+    auto whole = [&](int t, int heads, int use_order, int base, int pad) {
+        return AttnPlan{t, 0, 0, heads, use_order, base, pad};
+    };
     if (strategy == HEADKV_ATTN_PADDED) {
-        const int n_max = *std::max_element(L.n.begin(), L.n.end());
-        out[0] = AttnPlan{resident_threads(BH), 0, 0, BH, 0, 0,
-                          h->cfg.prefix_len + n_max + (appended ? 1 : 0)};
+        out[0] = whole(resident_threads(BH), BH, 0, 0, len_max);
         return 1;
     }
     if (strategy == HEADKV_ATTN_GROUPED && L.grouped) {
         int k = 0;
         const int sizes[2] = {L.n_global, BH - L.n_global};
         for (int g = 0, base = 0; g < 2; base += sizes[g], ++g)
-            if (sizes[g] > 0) out[k++] = AttnPlan{resident_threads(sizes[g]), 0, 0, sizes[g], 1, base, 0};
+            if (sizes[g] > 0) out[k++] = whole(resident_threads(sizes[g]), sizes[g], 1, base, 0);
         return k;
     }
     if (BH < kCus) {
@@ -336,7 +339,7 @@ int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
         return 1;
     }
     const int t = resident_threads(BH);
-    out[0] = AttnPlan{t, 0, 0, BH, BH > attn_resident_blocks(t) ? 1 : 0, 0, 0};
+    out[0] = whole(t, BH, BH > attn_resident_blocks(t) ? 1 : 0, 0, 0);
     return 1;
 }
 
