@@ -54,6 +54,10 @@ def parse():
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 512 MiB device copy five times (calibrates the HBM "
                         "byte counters of a profiler run) and exit")
+    p.add_argument("--label-stability", default=None, metavar="THR,THR,...",
+                   help="print, as one JSON line, how the head labels found when grouping at the "
+                        "first threshold (visual tokens) change when grouping runs at the later "
+                        "ones, on the GPU, and exit")
     p.add_argument("--traffic-record", nargs=4, metavar="DIR",
                    help="write the attention kernel's traffic record from four rocprofv3 --pmc "
                         "output folders (kernel FETCH_SIZE, kernel WRITE_SIZE, copy probe "
@@ -194,6 +198,31 @@ def cpu_baseline(wl, seconds_target: float):
                        f"{threads} threads; scaled to all {wl.layers}x{wl.heads} heads per token")}
 
 
+def label_stability(wl, thresholds):
+    """Labels of every (layer, batch row, head) when grouping runs at each of
+    the thresholds, compared with those at the first: the synthetic analogue
+    of the paper's grouping-accuracy table (Sec. 5.4).  L->G: heads local at
+    the first threshold and global later; G->L: the reverse."""
+    import numpy as np
+    from paper_2605_20600_amd.runner import DeviceInputs, grouping_labels
+    inp = DeviceInputs(wl.with_(group_threshold=max(thresholds)))
+    ref = None
+    rows = []
+    for thr in thresholds:
+        lab = grouping_labels(wl.with_(group_threshold=thr), inp)
+        x = np.stack([lab[l].cpu().numpy() for l in sorted(lab)]).astype(np.int64)
+        if ref is None:
+            ref = x
+        loc, glo = ref == 1, ref == 0
+        rows.append({"threshold": thr, "local_fraction": float(x.mean()),
+                     "agreement": float((x == ref).mean()),
+                     "L->G": float(((x == 0) & loc).sum() / max(loc.sum(), 1)),
+                     "G->L": float(((x == 1) & glo).sum() / max(glo.sum(), 1))})
+        print(f"# threshold {thr}: {rows[-1]}", file=sys.stderr, flush=True)
+    print(json.dumps({"workload": wl.name + "_shape", "heads": int(ref.size),
+                      "reference_threshold": thresholds[0], "rows": rows}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -217,6 +246,9 @@ def main():
     from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation_native
 
     wl = W.ALL[args.workload]
+    if args.label_stability:
+        label_stability(wl, [int(x) for x in args.label_stability.split(",")])
+        return
     if args.rho is not None:
         wl = wl.with_(rho=tuple(int(x) for x in args.rho.split("/")))
     if args.method == "full":

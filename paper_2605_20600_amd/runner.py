@@ -133,3 +133,30 @@ def run_generation_native(sess: Session, inp: DeviceInputs, outs: Dict[int, torc
         res["budgets"][l] = sess.budgets[l]
     B.headkv_run_steps(sess.h, t_g + 1, N, qp, kp, vp, stride, op, timing_every, st)
     return res
+
+
+def grouping_labels(wl: Workload, inp: DeviceInputs) -> Dict[int, torch.Tensor]:
+    """Head labels (1 = local) of every layer when grouping runs at step
+    wl.group_threshold - 1: the decode steps before it through the library's
+    step loop, then the append and headkv_score_heads.  Returns [B*H] uint8
+    per layer."""
+    L = wl.layers
+    t_g = wl.group_threshold - 1
+    sess = new_session(wl)
+    outs = {l: torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32,
+                           device=sess.device) for l in range(L)}
+    stride = wl.batch * wl.heads * wl.head_dim
+    ptr = lambda d: [d[l].data_ptr() for l in range(L)]
+    for l in range(L):
+        sess.prefill(l, inp.kc[l], inp.vc[l])
+    B.headkv_run_steps(sess.h, 0, t_g, ptr(inp.q), ptr(inp.k), ptr(inp.v), stride, ptr(outs), 0,
+                       sess.stream())
+    labels = {}
+    for l in range(L):
+        q = inp.q[l][t_g]
+        sess.append_and_evict(l, t_g, q, inp.k[l][t_g], inp.v[l][t_g])
+        _, is_local = sess.score_heads(l, q)
+        labels[l] = is_local.clone()
+    torch.cuda.synchronize()
+    sess.close()
+    return labels

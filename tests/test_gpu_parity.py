@@ -53,11 +53,12 @@ def _steps(wl, extra=()):
     return sorted(x for x in s.union(extra) if 0 <= x < N)
 
 
-def _run_and_check(wl, layers, slices, steps, fused=True, all_heads=True, strategy=0):
+def _run_and_check(wl, layers, slices, steps, fused=True, all_heads=True, strategy=0,
+                   n_steps=None):
     inp = DeviceInputs(wl, layers=layers)
     sess = new_session(wl, attn_strategy=strategy)
     res = run_generation(sess, inp, out_steps=steps, snap_steps=steps, fused=fused,
-                         record_layers=sorted({l for l, _ in slices}))
+                         record_layers=sorted({l for l, _ in slices}), steps=n_steps)
     torch.cuda.synchronize()
     for (layer, b) in slices:
         worst, ref = _check_slice(wl, res, layer, b, steps)
@@ -233,3 +234,43 @@ def test_lumina1024_strategies_sampled(strategy):
 def test_janus7b_grouped_sampled():
     wl = W.JANUS7B
     _run_and_check(wl, [4], [(4, 9)], _steps(wl), all_heads=False, strategy=B.HEADKV_ATTN_GROUPED)
+
+
+# ---- grouping and eviction variants: other tau, r_s and grouping points ----
+
+@pytest.mark.parametrize("tau", [0.85, 0.95])
+def test_lumina768_tau_sweep(tau):
+    # labels, n* and budgets of every head of two layers, retained sets of one
+    # slice through the first updates, at another grouping threshold tau
+    wl = W.LUMINA768.with_(tau=tau)
+    t_g, P = wl.group_threshold - 1, wl.period
+    steps = [t_g - 1, t_g, t_g + 1, t_g + P, t_g + 2 * P]
+    _run_and_check(wl, [0, 20], [(20, 6)], steps, n_steps=t_g + 2 * P + 1)
+
+
+@pytest.mark.parametrize("r_s", [(0, 1), (1, 4), (3, 4), (1, 1)], ids=["0", "1/4", "3/4", "1"])
+def test_tiny_rs_sweep(r_s):
+    # r_s = 0 or 1 leaves one part: plain bottom-M eviction over the history
+    wl = W.TINY.with_(r_s=r_s)
+    steps = list(range(wl.num_visual))
+    inp = DeviceInputs(wl)
+    sess = new_session(wl)
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps)
+    torch.cuda.synchronize()
+    _check_slice(wl, res, 0, 0, steps)
+
+
+@pytest.mark.parametrize("r_s", [(0, 1), (1, 1)], ids=["0", "1"])
+def test_lumina768_rs_extremes(r_s):
+    wl = W.LUMINA768.with_(rho=(1, 4), r_s=r_s)
+    _run_and_check(wl, [2], [(2, 4)], _steps(wl), all_heads=False)
+
+
+@pytest.mark.parametrize("thr", [100, 1200])
+def test_lumina768_other_grouping_points(thr):
+    # grouping at an earlier or later step (the labels' stability across
+    # positions is read from these)
+    wl = W.LUMINA768.with_(group_threshold=thr)
+    t_g, P = thr - 1, wl.period
+    steps = [t_g, t_g + 1, t_g + P]
+    _run_and_check(wl, [11], [(11, 1)], steps, n_steps=t_g + P + 1)
