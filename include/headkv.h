@@ -98,6 +98,11 @@ typedef struct headkv_config {
     int32_t rho_num, rho_den;/* rho = rho_num / rho_den in (0, 1] */
     int32_t rs_num, rs_den;  /* r_s = rs_num / rs_den in [0, 1] (Eq. 5) */
     int32_t attn_strategy;   /* HEADKV_ATTN_*; HEADKV_ATTN_VARLEN by default */
+    int32_t cfg_pairs;       /* 1: batch rows 2i and 2i+1 are the conditional and
+                                unconditional sequences of one classifier-free-
+                                guidance pair, and both take the head labels of
+                                row 2i (batch must be even); 0: every row is
+                                grouped on its own */
     double tau;              /* grouping mass threshold in (0, 1], 0.9 */
 } headkv_config;
 
@@ -153,7 +158,8 @@ headkv_status headkv_score_heads(headkv_t h, int32_t layer, const uint16_t* q,
 
 /* Budgets (Sec. 5.1) and the move into per-head segments, at step t_g after
  * score_heads.  is_local: [B][H] uint8 labels (device; usually the array
- * score_heads wrote; all zero gives the uniform-budget LineAR layout).
+ * score_heads wrote; all zero gives the uniform-budget LineAR layout; with
+ * cfg_pairs, row 2i+1 takes the labels of row 2i).
  * budget_override: [B][H] int32 (device) for HEADKV_BUDGET_OVERRIDE, else
  * NULL.  budgets: [B][H] int32 output (device), visual tokens per head, the
  * recent window included and the prefix not counted.

@@ -145,7 +145,10 @@ def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
 
     Grouping runs for every head of the slice (budgets of the layer-total mode
     depend on all labels), then each requested head is run through the
-    generation.  Inputs come from the shared seeded generator."""
+    generation.  Inputs come from the shared seeded generator.  With
+    wl.cfg_pairs the row's budgets and update policies follow the labels of
+    its pair's conditional row (b rounded down to even); "labels" and
+    "n_star" stay the row's own grouping result."""
     from paper_2605_20600_amd import synth
     kw = {} if seed is None else {"seed": seed}
     H = wl.heads
@@ -163,20 +166,23 @@ def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
         g = group_head(q[t_g], K, wl.tau, wl.local_window)
         labels[h], n_star[h], margins[h], mass[h] = (g["is_local"], g["n_star"],
                                                      g["margin"], g["mass_window"])
+    used = labels
     if label_override is not None:
-        labels = np.asarray(label_override, dtype=np.int32)
+        labels = used = np.asarray(label_override, dtype=np.int32)
+    elif getattr(wl, "cfg_pairs", False) and b % 2 == 1:
+        used = group_layer_row(wl, layer, b - 1, **kw)
     if budget_override is not None:
         ov_slice = np.asarray(budget_override, dtype=np.int32)
     else:
         ov = synth.budget_override(wl)
         ov_slice = None if ov is None else ov[layer, b]
-    bud = budgets(wl.budget_mode, labels, wl.num_visual, wl.row_len, wl.recent_len,
+    bud = budgets(wl.budget_mode, used, wl.num_visual, wl.row_len, wl.recent_len,
                   wl.rho, ov_slice)
     res = {"labels": labels, "n_star": n_star, "margin": margins, "mass_window": mass,
-           "budgets": bud, "out": {}, "snaps": {}, "stats": {}}
+           "budgets": bud, "labels_used": used, "out": {}, "snaps": {}, "stats": {}}
     def one(h):
         q, k, v, kc, vc = inputs[h]
-        return h, run_head(q, k, v, kc, vc, t_g, wl.period, bool(labels[h]), int(bud[h]),
+        return h, run_head(q, k, v, kc, vc, t_g, wl.period, bool(used[h]), int(bud[h]),
                            wl.recent_len, wl.r_s, want_out, snap_steps)
 
     # heads are independent; the C code runs without the GIL
@@ -189,8 +195,22 @@ def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
     return res
 
 
+def group_layer_row(wl, layer: int, b: int, seed: Optional[int] = None) -> np.ndarray:
+    """Labels of every head of one (layer, batch row): int32 [H]."""
+    from paper_2605_20600_amd import synth
+    kw = {} if seed is None else {"seed": seed}
+    t_g = wl.group_threshold - 1
+    lab = np.zeros(wl.heads, np.int32)
+    for h in range(wl.heads):
+        q, k, _, kc, _ = synth.head_inputs(wl, layer, b, h, **kw)
+        lab[h] = group_head(q[t_g], torch.cat([kc, k[: t_g + 1]], dim=0), wl.tau,
+                            wl.local_window)["is_local"]
+    return lab
+
+
 def group_layer(wl, layer: int, seed: Optional[int] = None) -> Dict[str, np.ndarray]:
-    """Grouping and budgets for every (b, h) of one layer: arrays [B][H]."""
+    """Grouping and budgets for every (b, h) of one layer: arrays [B][H].  With
+    wl.cfg_pairs, row 2i+1's budgets follow row 2i's labels."""
     from paper_2605_20600_amd import synth
     kw = {} if seed is None else {"seed": seed}
     t_g = wl.group_threshold - 1
@@ -208,6 +228,8 @@ def group_layer(wl, layer: int, seed: Optional[int] = None) -> Dict[str, np.ndar
             g = group_head(q[t_g, b, h], K, wl.tau, wl.local_window)
             out["labels"][b, h], out["n_star"][b, h] = g["is_local"], g["n_star"]
             out["margin"][b, h], out["mass_window"][b, h] = g["margin"], g["mass_window"]
-        out["budgets"][b] = budgets(wl.budget_mode, out["labels"][b], wl.num_visual, wl.row_len,
+    for b in range(B):
+        src = b - (b % 2) if getattr(wl, "cfg_pairs", False) else b
+        out["budgets"][b] = budgets(wl.budget_mode, out["labels"][src], wl.num_visual, wl.row_len,
                                     wl.recent_len, wl.rho, None if ov is None else ov[layer, b])
     return out

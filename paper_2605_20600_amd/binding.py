@@ -48,7 +48,7 @@ class HeadKVConfig(ctypes.Structure):
         ("group_threshold", ctypes.c_int32), ("budget_mode", ctypes.c_int32),
         ("rho_num", ctypes.c_int32), ("rho_den", ctypes.c_int32),
         ("rs_num", ctypes.c_int32), ("rs_den", ctypes.c_int32),
-        ("attn_strategy", ctypes.c_int32),
+        ("attn_strategy", ctypes.c_int32), ("cfg_pairs", ctypes.c_int32),
         ("tau", ctypes.c_double),
     ]
 

@@ -11,10 +11,11 @@
 //   k_merge  merge of the chunks of every head of a chunked launch, and the
 //            commit of the fused append's length.
 //
-// A block of T threads is T/16 rows of 16 lanes; each row holds one token at a
-// time, d/16 elements per lane (one 8- or 16-byte load), so the 4 rows of a
-// wavefront read 4 consecutive K or V rows of the segment.  A pass covers
-// T/16 x kAttnTpr tokens (512 at T = 1024): every load of the pass is issued
+// A block of T threads is rows of d/8 lanes (16 at d = 128, 8 at d = 64); each
+// row holds one token at a time, 8 elements per lane (one 16-byte load), so the
+// rows of a wavefront read consecutive K or V rows of the segment (1 KB).  A
+// pass covers T/(d/8) x kAttnTpr tokens (512 at T = 1024 and d = 128, 1024 at
+// d = 64): every load of the pass is issued
 // before the first one is used (row indices past the end are clamped to the
 // last token and their logits masked, so no load sits behind a branch).  K/V
 // are read once per step, so the loads are non-temporal.  The softmax is
@@ -38,7 +39,8 @@ using namespace dev;
 
 template <int D>
 struct AttnRegs {
-    static constexpr int VPL = D / 16;  // bf16 elements per lane
+    static constexpr int LPR = D / 8;   // lanes per token row
+    static constexpr int VPL = 8;       // bf16 elements per lane
     static constexpr int NW = VPL / 2;  // 32-bit words per lane
     using Vec = Words<NW>;
 };
@@ -72,7 +74,7 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
             dp += qf[2 * e] * bf_lo(kk[j].w[e]);
             dp += qf[2 * e + 1] * bf_hi(kk[j].w[e]);
         }
-        dp = row16_sum(dp);
+        dp = lanes_sum<AttnRegs<D>::LPR>(dp);
         s[j] = (t0 + j * ROWS + row < t_end) ? dp : -INFINITY;
         mx = fmaxf(mx, s[j]);
     }
@@ -96,15 +98,17 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
 }
 
 // 4 wavefronts per SIMD (16 per CU) at every block size: at most 128 VGPRs.
-template <int D, bool APPEND, int T, bool CHUNKED>
+// TPR tokens per row and pass: 8, or 4 when every head fits in half a pass.
+template <int D, bool APPEND, int T, bool CHUNKED, int TPR>
 __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_attn(
     LayerDev L, int C, AppendArgs a, const uint16_t* __restrict__ q, float* __restrict__ out,
     float* __restrict__ part, int use_order, int order_base, int pad_len, float qscale) {
     using Vec = typename AttnRegs<D>::Vec;
     constexpr int VPL = AttnRegs<D>::VPL;
     constexpr int NW = AttnRegs<D>::NW;
-    constexpr int ROWS = T / 16;
-    constexpr int TP = ROWS * kAttnTpr;  // tokens per pass
+    constexpr int LPR = AttnRegs<D>::LPR;
+    constexpr int ROWS = T / LPR;
+    constexpr int TP = ROWS * TPR;  // tokens per pass
     constexpr int WAVES = T / 64;
     int h, t_begin;
     if (CHUNKED) {
@@ -116,7 +120,7 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
         t_begin = 0;
     }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int row = tid >> 4, col = tid & 15;
+    const int row = tid / LPR, col = tid % LPR;
     const Vec qraw = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
     const int n = L.n[h];
     const int len = C + n + (APPEND ? 1 : 0);
@@ -149,9 +153,9 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
     // first pass: the append's store and q's conversion go between its loads
     // and their first use
     if (t_begin < t_stop) {  // a chunk past the head's length reads nothing
-        Vec kk[kAttnTpr], vv[kAttnTpr];
+        Vec kk[TPR], vv[TPR];
 #pragma unroll
-        for (int j = 0; j < kAttnTpr; ++j) {
+        for (int j = 0; j < TPR; ++j) {
             const int tok = min(t_begin + j * ROWS + row, t_stop - 1);
             kk[j] = nt_load<NW>(krow(tok) + col * VPL);
             vv[j] = nt_load<NW>(vrow(tok) + col * VPL);
@@ -164,23 +168,23 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
             qf[2 * e] = bf_lo(qraw.w[e]) * qscale;
             qf[2 * e + 1] = bf_hi(qraw.w[e]) * qscale;
         }
-        attn_accumulate<D, kAttnTpr, ROWS>(kk, vv, t_begin, row, t_end, qf, m, l, acc);
+        attn_accumulate<D, TPR, ROWS>(kk, vv, t_begin, row, t_end, qf, m, l, acc);
     }
     // further passes of a head longer than one pass
     for (int t0 = t_begin + TP; t0 < t_stop; t0 += TP) {
-        Vec kk[kAttnTpr], vv[kAttnTpr];
+        Vec kk[TPR], vv[TPR];
 #pragma unroll
-        for (int j = 0; j < kAttnTpr; ++j) {
+        for (int j = 0; j < TPR; ++j) {
             const int tok = min(t0 + j * ROWS + row, t_stop - 1);
             kk[j] = nt_load<NW>(krow(tok) + col * VPL);
             vv[j] = nt_load<NW>(vrow(tok) + col * VPL);
         }
         __builtin_amdgcn_sched_barrier(0);
-        attn_accumulate<D, kAttnTpr, ROWS>(kk, vv, t0, row, t_end, qf, m, l, acc);
+        attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, t_end, qf, m, l, acc);
     }
-    // merge the four rows of each wavefront
+    // merge the rows of each wavefront
 #pragma unroll
-    for (int off = 16; off <= 32; off <<= 1) {
+    for (int off = LPR; off <= 32; off <<= 1) {
         const float mo = __shfl_xor(m, off);
         const float lo = __shfl_xor(l, off);
         const float mn = fmaxf(m, mo);
@@ -196,7 +200,7 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
     }
     __shared__ float sm[WAVES], sl[WAVES];
     __shared__ float sacc[WAVES][D];
-    if (lane < 16) {
+    if (lane < LPR) {
 #pragma unroll
         for (int e = 0; e < VPL; ++e) sacc[wave][col * VPL + e] = acc[e];
         if (lane == 0) {
@@ -256,7 +260,7 @@ __global__ __launch_bounds__(D) void k_merge(LayerDev L, float* __restrict__ out
 
 inline int last_error() { return (int)hipGetLastError(); }
 
-template <int D, int T, bool CHUNKED>
+template <int D, int T, bool CHUNKED, int TPR>
 void attn_launch(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
                  float* out, float* partials, const AttnPlan& p, hipStream_t st, hipEvent_t ev0,
                  hipEvent_t ev1) {
@@ -264,11 +268,11 @@ void attn_launch(const LayerDev& L, const Shape& s, const AppendArgs& a, const u
     const dim3 grid(CHUNKED ? p.items : p.heads), block(T);
     // with events, they take the kernel's own start and end timestamps
     if (a.k != nullptr)
-        hipExtLaunchKernelGGL((k_attn<D, true, T, CHUNKED>), grid, block, 0, st, ev0, ev1, 0, L,
+        hipExtLaunchKernelGGL((k_attn<D, true, T, CHUNKED, TPR>), grid, block, 0, st, ev0, ev1, 0, L,
                               s.C, a, q, out, partials, p.use_order, p.order_base, p.pad_len,
                               qscale);
     else
-        hipExtLaunchKernelGGL((k_attn<D, false, T, CHUNKED>), grid, block, 0, st, ev0, ev1, 0, L,
+        hipExtLaunchKernelGGL((k_attn<D, false, T, CHUNKED, TPR>), grid, block, 0, st, ev0, ev1, 0, L,
                               s.C, a, q, out, partials, p.use_order, p.order_base, p.pad_len,
                               qscale);
     if (CHUNKED)
@@ -281,9 +285,11 @@ void attn_dispatch_t(const LayerDev& L, const Shape& s, const AppendArgs& a, con
                      float* out, float* partials, const AttnPlan& p, hipStream_t st,
                      hipEvent_t ev0, hipEvent_t ev1) {
     if (p.chunked)
-        attn_launch<D, T, true>(L, s, a, q, out, partials, p, st, ev0, ev1);
+        attn_launch<D, T, true, kAttnTpr>(L, s, a, q, out, partials, p, st, ev0, ev1);
+    else if (p.tpr == kAttnTpr)
+        attn_launch<D, T, false, kAttnTpr>(L, s, a, q, out, partials, p, st, ev0, ev1);
     else
-        attn_launch<D, T, false>(L, s, a, q, out, partials, p, st, ev0, ev1);
+        attn_launch<D, T, false, kAttnTpr / 2>(L, s, a, q, out, partials, p, st, ev0, ev1);
 }
 
 template <int D>

@@ -135,14 +135,16 @@ __global__ __launch_bounds__(kBlock) void k_score(LayerDev L, int d, const uint1
 }
 
 // ------------------------------------------------------------------ budgets
+// With cfg_pairs, batch rows 2i (conditional) and 2i+1 (unconditional) form a
+// guidance pair and both take the labels of row 2i.
 __global__ void k_budgets(LayerDev L, int H, int N, const uint8_t* is_local,
                           const int32_t* override_b, int32_t* budgets, int mode, int row_len,
-                          int recent_len, int rho_num, int rho_den) {
+                          int recent_len, int rho_num, int rho_den, int cfg_pairs) {
     __shared__ int n_local;
     const int b = blockIdx.x, h = threadIdx.x, idx = b * H + h;
     if (h == 0) n_local = 0;
     __syncthreads();
-    const int loc = is_local[idx] ? 1 : 0;
+    const int loc = is_local[cfg_pairs ? (b & ~1) * H + h : idx] ? 1 : 0;
     if (loc) atomicAdd(&n_local, 1);
     __syncthreads();
     const long long rhoN = (long long)N * rho_num / rho_den;
@@ -479,9 +481,10 @@ int launch_score(const LayerDev& L, const Shape& s, const uint16_t* q, int32_t* 
 
 int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
                    const int32_t* override_b, int32_t* budgets, int mode, int row_len,
-                   int recent_len, int rho_num, int rho_den, void* stream) {
+                   int recent_len, int rho_num, int rho_den, int cfg_pairs, void* stream) {
     hipLaunchKernelGGL(k_budgets, dim3(s.B), dim3(s.H), 0, (hipStream_t)stream, L, s.H, s.N,
-                       is_local, override_b, budgets, mode, row_len, recent_len, rho_num, rho_den);
+                       is_local, override_b, budgets, mode, row_len, recent_len, rho_num, rho_den,
+                       cfg_pairs);
     return last_error();
 }
 

@@ -23,13 +23,17 @@ __device__ __forceinline__ double bf_f64(uint16_t b) {
     return (double)__uint_as_float((uint32_t)b << 16);
 }
 
-// Sum over the 16 lanes of a DPP row: quad swaps, then half-row and row
-// mirrors; every lane of the row ends with the full sum.
-__device__ __forceinline__ float row16_sum(float v) {
+// Sum over groups of N = 8 or 16 lanes (half or whole DPP rows): quad swaps,
+// then the half-row mirror and, for 16, the row mirror; every lane of the
+// group ends with the group's sum.
+template <int N>
+__device__ __forceinline__ float lanes_sum(float v) {
+    static_assert(N == 8 || N == 16, "8 or 16 lanes");
     v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
     v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
     v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
-    v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
+    if (N == 16)
+        v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
     return v;
 }
 

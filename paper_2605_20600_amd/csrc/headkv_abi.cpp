@@ -103,10 +103,13 @@ headkv_status validate_config(const headkv_config* c) {
     if (!(c->tau > 0.0 && c->tau <= 1.0)) return fail(HEADKV_ERR_INVALID_ARG, "tau must be in (0, 1]");
     if (c->attn_strategy < HEADKV_ATTN_VARLEN || c->attn_strategy > HEADKV_ATTN_GROUPED)
         return fail(HEADKV_ERR_INVALID_ARG, "unknown attn_strategy");
+    if (c->cfg_pairs != 0 && c->cfg_pairs != 1) return fail(HEADKV_ERR_INVALID_ARG, "cfg_pairs must be 0 or 1");
+    if (c->cfg_pairs && c->batch % 2 != 0)
+        return fail(HEADKV_ERR_INVALID_ARG, "cfg_pairs needs an even batch");
     // chunk indices must fit the 8 bits of a chunk table entry (always true
     // within the prefix and capacity limits)
     const int max_cap = std::max(c->group_threshold, std::min(c->num_visual, HEADKV_MAX_CAPACITY));
-    const int tp = attn_tokens_per_pass(kAttnMinThreads);
+    const int tp = attn_tokens_per_pass(kAttnMinThreads, c->head_dim);
     if ((c->prefix_len + max_cap + 1 + tp - 1) / tp > kMaxChunksPerHead)
         return fail(HEADKV_ERR_UNSUPPORTED, "too many attention chunks per head");
     return ok();
@@ -121,8 +124,8 @@ struct Plan {
 
 // Chunks of one pass of a `threads`-thread block that cover a head of
 // capacity `cap` (prefix, slots and the token being appended).
-int chunks_of(int C, int cap, int threads) {
-    const int tp = attn_tokens_per_pass(threads);
+int chunks_of(int C, int cap, int threads, int d) {
+    const int tp = attn_tokens_per_pass(threads, d);
     return (C + cap + 1 + tp - 1) / tp;
 }
 
@@ -134,7 +137,7 @@ Plan make_plan(const headkv_config& c) {
     p.dense_bytes = (size_t)p.dense_seg * p.BH;
     // the largest capacity any head can have, dense or after grouping
     const int max_cap = std::max(p.dense_cap, std::min(c.num_visual, HEADKV_MAX_CAPACITY));
-    const int per_head = chunks_of(c.prefix_len, max_cap, kAttnMinThreads);
+    const int per_head = chunks_of(c.prefix_len, max_cap, kAttnMinThreads, c.head_dim);
     p.ml.compute(p.BH, c.head_dim, p.BH * per_head);
     // partial (max, sum, weighted V) of every chunk table entry
     p.ws_bytes = align_up((size_t)p.BH * per_head * (c.head_dim + 2) * sizeof(float), 256);
@@ -143,12 +146,12 @@ Plan make_plan(const headkv_config& c) {
 
 // Block size of a chunk table for the given capacities: the fewest rounds of
 // resident blocks, then the largest blocks (fewest partial results).
-int pick_chunk_threads(int C, const std::vector<int>& cap) {
+int pick_chunk_threads(int C, int d, const std::vector<int>& cap) {
     int best = kAttnMaxThreads;
     long long best_rounds = -1;
     for (int t = kAttnMaxThreads; t >= kAttnMinThreads; t /= 2) {
         long long items = 0;
-        for (int x : cap) items += chunks_of(C, x, t);
+        for (int x : cap) items += chunks_of(C, x, t, d);
         const long long slots = attn_resident_blocks(t);
         const long long rounds = (items + slots - 1) / slots;
         if (best_rounds < 0 || rounds < best_rounds) {
@@ -241,8 +244,8 @@ headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c, con
     L.cap.assign(h->shape.BH, h->dense_cap);
     L.budget.assign(h->shape.BH, 0);
     L.label_local.assign(h->shape.BH, 0);
-    L.chunk_threads = pick_chunk_threads(c.prefix_len, L.cap);
-    const int dense_chunks = chunks_of(c.prefix_len, h->dense_cap, L.chunk_threads);
+    L.chunk_threads = pick_chunk_threads(c.prefix_len, c.head_dim, L.cap);
+    const int dense_chunks = chunks_of(c.prefix_len, h->dense_cap, L.chunk_threads, c.head_dim);
     L.items = h->shape.BH * dense_chunks;
     st = hip_status(launch_prefill(dev_of(h, L), h->shape, k_c, v_c, h->dense_seg, h->dense_cap,
                                    dense_chunks, stream),
@@ -320,8 +323,11 @@ int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
     const int strategy = h->cfg.attn_strategy;
     const int len_max = h->cfg.prefix_len + *std::max_element(L.n.begin(), L.n.end()) +
                         (appended ? 1 : 0);
+    const int d = h->cfg.head_dim;
     auto whole = [&](int t, int heads, int use_order, int base, int pad) {
-        return AttnPlan{t, 0, 0, heads, use_order, base, pad};
+        const int read = std::max(len_max, pad);
+        const int tpr = read <= attn_tokens_per_pass(t, d, kAttnTpr / 2) ? kAttnTpr / 2 : kAttnTpr;
+        return AttnPlan{t, 0, 0, heads, use_order, base, pad, tpr};
     };
     if (strategy == HEADKV_ATTN_PADDED) {
         out[0] = whole(resident_threads(BH), BH, 0, 0, len_max);
@@ -335,7 +341,7 @@ int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
         return k;
     }
     if (BH < kCus) {
-        out[0] = AttnPlan{L.chunk_threads, 1, L.items, BH, 0, 0, 0};
+        out[0] = AttnPlan{L.chunk_threads, 1, L.items, BH, 0, 0, 0, kAttnTpr};
         return 1;
     }
     const int t = resident_threads(BH);
@@ -593,14 +599,15 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     hipStream_t s = (hipStream_t)stream;
     LayerDev Dold = dev_of(h, L);
     st = hip_status(launch_budgets(Dold, h->shape, is_local, budget_override, budgets, c.budget_mode,
-                                   c.row_len, c.recent_len, c.rho_num, c.rho_den, stream),
+                                   c.row_len, c.recent_len, c.rho_num, c.rho_den, c.cfg_pairs, stream),
                     "budget launch");
     if (st) return st;
     std::vector<int32_t> bud(BH);
-    std::vector<uint8_t> lab(BH);
+    std::vector<int32_t> lab(BH);  // the labels the budgets used (cfg pairs applied)
     st = hip_status(hipMemcpyAsync(bud.data(), budgets, sizeof(int32_t) * BH, hipMemcpyDeviceToHost, s),
                     "budget read-back");
-    if (!st) st = hip_status(hipMemcpyAsync(lab.data(), is_local, BH, hipMemcpyDeviceToHost, s),
+    if (!st) st = hip_status(hipMemcpyAsync(lab.data(), Dold.label, sizeof(int32_t) * BH,
+                                            hipMemcpyDeviceToHost, s),
                              "label read-back");
     if (st) {
         (void)hipStreamSynchronize(s);
@@ -644,12 +651,12 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     int n_global = 0;
     for (int i = 0; i < BH; ++i) n_global += lab[i] ? 0 : 1;
     // chunk table of the new layout, the chunks of a head contiguous
-    const int chunk_threads = pick_chunk_threads(c.prefix_len, cap_i);
+    const int chunk_threads = pick_chunk_threads(c.prefix_len, c.head_dim, cap_i);
     std::vector<uint32_t> items;
     std::vector<int32_t> item_start(BH + 1);
     for (int i = 0; i < BH; ++i) {
         item_start[i] = (int32_t)items.size();
-        const int nc = chunks_of(c.prefix_len, cap[i], chunk_threads);
+        const int nc = chunks_of(c.prefix_len, cap[i], chunk_threads, c.head_dim);
         for (int k = 0; k < nc; ++k) items.push_back(((uint32_t)i << 8) | (uint32_t)k);
     }
     item_start[BH] = (int32_t)items.size();

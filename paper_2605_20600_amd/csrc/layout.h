@@ -20,10 +20,13 @@ constexpr int kBlock = 256;  // threads per block of the cache kernels
 constexpr int kAttnTpr = 8;  // tokens per 16-lane row per attention pass
 constexpr int kCus = 256;    // MI355X compute units
 // Attention blocks have 1024, 512 or 256 threads; 1024 threads of at most 128
-// VGPRs fill a CU, so a CU holds 1024 / threads blocks at once.
+// VGPRs fill a CU, so a CU holds 1024 / threads blocks at once.  A token row
+// of d bf16 is read by d/8 lanes, 16 bytes each.
 constexpr int kAttnMinThreads = 256;
 constexpr int kAttnMaxThreads = 1024;
-inline constexpr int attn_tokens_per_pass(int threads) { return threads / 16 * kAttnTpr; }
+inline constexpr int attn_tokens_per_pass(int threads, int d, int tpr = kAttnTpr) {
+    return threads / (d / 8) * tpr;
+}
 inline constexpr int attn_resident_blocks(int threads) { return kCus * (kAttnMaxThreads / threads); }
 // Chunks per head in a chunk table: bounded so that the chunk index fits in
 // the 8 low bits of a table entry.
@@ -116,9 +119,10 @@ int launch_append(const LayerDev& L, const Shape& s, const AppendArgs& a, void* 
 int launch_score(const LayerDev& L, const Shape& s, const uint16_t* q, int32_t* n_star,
                  uint8_t* is_local, int len, double sqrt_d, double tau, int local_window,
                  void* stream);
+// Writes budgets and the labels the updates use (L.label) for every head.
 int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
                    const int32_t* override_b, int32_t* budgets, int mode, int row_len,
-                   int recent_len, int rho_num, int rho_den, void* stream);
+                   int recent_len, int rho_num, int rho_den, int cfg_pairs, void* stream);
 // a.k == nullptr: no append.
 // lds_cap: largest visual capacity among the launch's source segments.
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
@@ -138,6 +142,8 @@ struct AttnPlan {
     int order_base;
     int pad_len;     // one block per head: read rows up to this length, those
                      // past the head's own length masked (0: none)
+    int tpr;         // tokens per row and pass: kAttnTpr, or half of it (one
+                     // block per head, every head within half a pass)
 };
 // a.k == nullptr: no append.  partials: (d + 2) floats per table entry.
 // ev_start / ev_stop (hipEvent_t or nullptr) receive the attention kernel's

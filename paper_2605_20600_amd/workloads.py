@@ -10,7 +10,8 @@ Hyper-parameters of the method and where they come from:
   * rho -- budget ratio of global heads, B = rho*N (Sec. 5.1, Implementation
     Details; the B column of the efficiency table).
   * w = two image rows -- recent window (Sec. 5.1, Implementation Details).
-  * thr -- visual-token count at which heads are grouped: 100 for Janus-Pro,
+  * thr -- visual-token count at which heads are grouped: 100 for Janus-Pro
+    and LlamaGen,
     300 for Lumina-mGPT-768, 500 for Lumina-mGPT-1024 (Appendix, More
     Implementation Details).
   * P -- update period of the efficient cache update (Sec. 4, Efficient Cache
@@ -46,6 +47,7 @@ class Workload:
     override: Optional[str] = None  # None, "rows_1_16" or "loguniform_64_1024"
     r_s: Tuple[int, int] = (1, 2)
     tau: float = 0.9
+    cfg_pairs: bool = False    # rows 2i / 2i+1: cond / uncond of one guidance pair
 
     @property
     def row_len(self) -> int:          # R, including the row-end token
@@ -94,4 +96,12 @@ STRESS = Workload(
     group_threshold=300, rho=(1, 8), budget_mode=BUDGET_OVERRIDE,
     amp_mode="lumina", override="loguniform_64_1024")
 
-ALL = {w.name: w for w in (TINY, JANUS7B, LUMINA768, LUMINA1024, STRESS)}
+# LlamaGen-XL (class-conditional, 36 layers, 20 heads of 64, one class token)
+# at 384 px: a 24 x 24 grid, 128 images with classifier-free guidance = 256
+# sequences in 128 cond/uncond pairs that share their head labels.
+LLAMAGEN_XL = Workload(
+    name="llamagen_xl", batch=256, layers=36, heads=20, head_dim=64, prefix_len=1,
+    grid_rows=24, grid_cols=24, row_end=False, period=24, group_threshold=100,
+    rho=(1, 4), budget_mode=BUDGET_PAPER, amp_mode="lumina", cfg_pairs=True)
+
+ALL = {w.name: w for w in (TINY, JANUS7B, LUMINA768, LUMINA1024, STRESS, LLAMAGEN_XL)}

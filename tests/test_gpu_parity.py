@@ -274,3 +274,23 @@ def test_lumina768_other_grouping_points(thr):
     t_g, P = thr - 1, wl.period
     steps = [t_g, t_g + 1, t_g + P]
     _run_and_check(wl, [11], [(11, 1)], steps, n_steps=t_g + P + 1)
+
+
+# ---- classifier-free-guidance pairs and the LlamaGen-XL shape (d = 64) ----
+
+def test_tiny_cfg_pairs_every_step():
+    # row 1 (unconditional) takes row 0's labels: budgets, policies and
+    # retained sets follow them
+    wl = W.TINY.with_(batch=2, cfg_pairs=True)
+    steps = list(range(wl.num_visual))
+    inp = DeviceInputs(wl)
+    sess = new_session(wl)
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps)
+    torch.cuda.synchronize()
+    for b in (0, 1):
+        _check_slice(wl, res, 0, b, steps)
+
+
+def test_llamagen_xl_cfg_sampled():
+    wl = W.LLAMAGEN_XL
+    _run_and_check(wl, [0, 35], [(0, 0), (35, 255)], _steps(wl, extra=(250,)))

@@ -366,3 +366,20 @@ def test_ste_query_window_is_the_last_P_queries():
         kept = set(np.flatnonzero(snaps[0]).tolist())
         assert len(kept) == B
         assert (kept == oldest_first) == (not inside), step
+
+
+def test_cfg_pairs_follow_the_conditional_row():
+    # a guidance pair's unconditional row runs with its conditional row's
+    # labels: the same as overriding its labels with them
+    from paper_2605_20600_amd import workloads as W
+    wl = W.TINY.with_(batch=2, cfg_pairs=True)
+    plain = W.TINY.with_(batch=2)
+    lab0 = oracle.simulate(plain, 0, 0, want_out=False)["labels"]
+    a = oracle.simulate(wl, 0, 1, snap_steps=[255])
+    b = oracle.simulate(plain, 0, 1, snap_steps=[255], label_override=lab0)
+    assert np.array_equal(a["budgets"], b["budgets"])
+    assert np.array_equal(a["labels_used"], lab0)
+    for h in range(wl.heads):
+        assert np.array_equal(a["snaps"][h], b["snaps"][h])
+    g = oracle.group_layer(wl, 0)
+    assert np.array_equal(g["budgets"][1], g["budgets"][0])
