@@ -272,35 +272,44 @@ def main():
     sess = new_session(wl, attn_strategy=B.ATTN_STRATEGIES[args.attn_strategy])
     outs = {l: torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32, device="cuda")
             for l in inp.layers}
+    pre_out = {l: torch.empty((wl.batch, wl.heads, wl.prefix_len, wl.head_dim),
+                              dtype=torch.float32, device="cuda") for l in inp.layers}
 
     for i in range(args.warmup):
-        run_generation_native(sess, inp, outs, label_override=labels)
+        run_generation_native(sess, inp, outs, label_override=labels, prefill_out=pre_out)
         torch.cuda.synchronize()
         print(f"# warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
 
     # timed region: K whole generations, the step loop in the library.  Every
     # `timing_every`-th step's fused append + attention launch (one kernel) is
     # timed with HIP events that take the kernel's own start and end.
-    per_gen = (wl.num_visual + args.timing_every - 1) // args.timing_every * wl.layers * 2
+    per_gen = ((wl.num_visual + args.timing_every - 1) // args.timing_every * 2 + 1) * wl.layers
     B.headkv_timing_reserve(sess.h, per_gen * args.steps)
     B.headkv_timing_collect(sess.h)              # discard warm-up records
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
         run_generation_native(sess, inp, outs, timing_every=args.timing_every,
-                              label_override=labels)
+                              label_override=labels, prefill_out=pre_out)
         print(f"# step {i + 1}/{args.steps} issued", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     per_kind, dropped = B.headkv_timing_collect(sess.h)
+    C, d = wl.prefix_len, wl.head_dim
+    pre_flops = wl.batch * wl.heads * 4 * d * C * (C + 1) / 2  # causal QK^T and PV
     names = ["k_attn<d, append> (headkv_decode_step)", "k_attn<d> (after an update)",
-             "k_update<d> (append + periodic update)"]
+             "k_update<d> (append + periodic update)",
+             "k_prefill_attn<d> (prefix store + causal attention, headkv_prefill_attn)"]
     kinds = {}
     for name, (kms, kn, kb) in zip(names, per_kind):
         if kn:
             kinds[name] = {"launches": kn, "avg_us": kms / kn * 1e3, "alg_bytes_per_launch": kb / kn,
                            "achieved_gbps": kb / kn / (kms / kn * 1e-3) / 1e9,
                            "share_of_timed_ms": kms}
+    if names[3] in kinds:
+        k = kinds[names[3]]
+        k["causal_flops_per_launch"] = pre_flops
+        k["achieved_tflops"] = pre_flops / (k["avg_us"] * 1e-6) / 1e12
     total_ms = sum(v["share_of_timed_ms"] for v in kinds.values())
     for v in kinds.values():
         v["share_of_timed_ms"] = v["share_of_timed_ms"] / total_ms

@@ -133,6 +133,16 @@ void headkv_destroy(headkv_t h);
 headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c,
                              const uint16_t* v_c, void* stream);
 
+/* Step 1 with its attention: headkv_prefill, and the causal self-attention of
+ * the C conditional tokens, out_c[b][h][i] = softmax(q_i K_c^T / sqrt(d) over
+ * keys 0..i) V_c (Eq. 1 over the prefix, token by token).  q_c, k_c, v_c:
+ * [B][H][C][d] bf16; out_c: [B][H][C][d] fp32; all device, 16-byte aligned.
+ * Needs C >= 1.  bf16 storage, fp32 accumulation (the attention weights enter
+ * the weighted sum of V in bf16, on the matrix cores). */
+headkv_status headkv_prefill_attn(headkv_t h, int32_t layer, const uint16_t* q_c,
+                                  const uint16_t* k_c, const uint16_t* v_c, float* out_c,
+                                  void* stream);
+
 /* Cache append K <- [K, k_t], V <- [V, v_t] (Sec. 3, KV Cache) for visual
  * step `step` of `layer`; q, k, v: [B][H][d] bf16, device.  q_t is added to
  * the head's sum of the past-P queries (Eq. 6).  When the layer is grouped and
@@ -209,14 +219,16 @@ headkv_status headkv_run_steps(headkv_t h, int32_t step_begin, int32_t step_end,
                                const uint16_t* const* v, int64_t step_stride,
                                float* const* out, int32_t timing_every, void* stream);
 
-/* Creates events for `launches` timed attention launches (host call). */
+/* Creates events for `launches` timed launches (host call).  While reserved
+ * events are left, every headkv_prefill_attn launch is timed as well. */
 headkv_status headkv_timing_reserve(headkv_t h, int64_t launches);
 
 /* Kinds of timed launches. */
 #define HEADKV_TIMED_ATTN_APPEND 0 /* fused append + attention (one kernel) */
 #define HEADKV_TIMED_ATTN 1        /* attention after an update or a split append */
 #define HEADKV_TIMED_UPDATE 2      /* append + periodic update */
-#define HEADKV_TIMED_KINDS 3
+#define HEADKV_TIMED_PREFILL 3     /* prefix store + causal prefix attention */
+#define HEADKV_TIMED_KINDS 4
 
 /* Waits for the timed launches since the last collect and returns, per kind
  * (arrays of HEADKV_TIMED_KINDS), the sum of their kernel durations (ms), their
@@ -224,7 +236,9 @@ headkv_status headkv_timing_reserve(headkv_t h, int64_t launches);
  * launches that found no free event.  Algorithmic bytes: K/V of every attended
  * token, q and the output for attention; the appended row, its position and
  * the query-sum update for the append; positions, the history keys of
- * evicting global heads and at most M moved rows for the update. */
+ * evicting global heads and at most M moved rows for the update; q, k, v of
+ * the prefix read, its k, v stored and the fp32 output written for the
+ * prefill. */
 headkv_status headkv_timing_collect(headkv_t h, double* kernel_ms, int64_t* launches,
                                     double* alg_bytes, int64_t* dropped);
 

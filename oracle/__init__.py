@@ -79,6 +79,13 @@ def attention(q, K, V) -> np.ndarray:
     return out
 
 
+def prefill_attention(qc, kc, vc) -> np.ndarray:
+    """Causal attention over the prefix, Eq. (1) token by token: row i attends
+    over keys 0..i.  qc, kc, vc: [C][d]; returns fp64 [C][d]."""
+    qc, kc, vc = _f64(qc), _f64(kc), _f64(vc)
+    return np.stack([attention(qc[i], kc[: i + 1], vc[: i + 1]) for i in range(qc.shape[0])])
+
+
 def group_head(q, K, tau: float, local_window: int) -> Dict[str, float]:
     """Head grouping of Sec. 4 Step 2 for one head (K in cache order)."""
     q, K = _f64(q), _f64(K)

@@ -30,7 +30,7 @@ ATTN_STRATEGIES = {"varlen": HEADKV_ATTN_VARLEN, "padded": HEADKV_ATTN_PADDED,
                    "grouped": HEADKV_ATTN_GROUPED}
 
 EXPORTED = (
-    "headkv_plan", "headkv_create", "headkv_destroy", "headkv_prefill",
+    "headkv_plan", "headkv_create", "headkv_destroy", "headkv_prefill", "headkv_prefill_attn",
     "headkv_append_and_evict", "headkv_score_heads", "headkv_assign_budgets",
     "headkv_decode_attn", "headkv_decode_step", "headkv_export_retained",
     "headkv_run_steps", "headkv_timing_reserve", "headkv_timing_collect",
@@ -76,6 +76,7 @@ def load() -> ctypes.CDLL:
         "headkv_plan": [cfgp, ctypes.POINTER(Z), ctypes.POINTER(Z), ctypes.POINTER(Z)],
         "headkv_create": [cfgp, P, P, P, ctypes.POINTER(P)],
         "headkv_prefill": [P, I, P, P, P],
+        "headkv_prefill_attn": [P, I, P, P, P, P, P],
         "headkv_append_and_evict": [P, I, I, P, P, P, P],
         "headkv_score_heads": [P, I, P, P, P, P],
         "headkv_assign_budgets": [P, I, P, P, P, P, Z, ctypes.POINTER(Z), P],
@@ -134,6 +135,11 @@ def headkv_prefill(h: int, layer: int, k_c: int, v_c: int, stream: int = 0) -> N
     _check(load().headkv_prefill(h, layer, k_c, v_c, stream), "headkv_prefill")
 
 
+def headkv_prefill_attn(h: int, layer: int, q_c: int, k_c: int, v_c: int, out_c: int,
+                        stream: int = 0) -> None:
+    _check(load().headkv_prefill_attn(h, layer, q_c, k_c, v_c, out_c, stream), "headkv_prefill_attn")
+
+
 def headkv_append_and_evict(h: int, layer: int, step: int, q: int, k: int, v: int,
                             stream: int = 0) -> None:
     _check(load().headkv_append_and_evict(h, layer, step, q, k, v, stream),
@@ -185,9 +191,10 @@ def headkv_timing_reserve(h: int, launches: int) -> None:
 
 
 def headkv_timing_collect(h: int):
-    """Returns per kind (fused append + attention, attention, append + update)
-    a list of (kernel ms, launches, algorithmic bytes), and the dropped count."""
-    K = 3
+    """Returns per kind (fused append + attention, attention, append + update,
+    prefill) a list of (kernel ms, launches, algorithmic bytes), and the
+    dropped count."""
+    K = 4
     ms = (ctypes.c_double * K)()
     n = (ctypes.c_int64 * K)()
     b = (ctypes.c_double * K)()

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libheadkv.so")
-SOURCES = ["cache_kernels.hip", "attn_kernels.hip", "headkv_abi.cpp"]
+SOURCES = ["cache_kernels.hip", "attn_kernels.hip", "prefill_attn.hip", "headkv_abi.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra",

@@ -36,33 +36,8 @@ using namespace dev;
 __global__ __launch_bounds__(kBlock) void k_prefill(LayerDev L, int C, int d, const uint16_t* kc,
                                                     const uint16_t* vc, int64_t seg_bytes,
                                                     int dense_cap, int dense_chunks) {
-    const int h = blockIdx.x, tid = threadIdx.x;
-    // chunk table of the dense layout: every head has dense_chunks chunks
-    for (int c = tid; c < dense_chunks; c += kBlock)
-        L.items[(size_t)h * dense_chunks + c] = ((uint32_t)h << 8) | (uint32_t)c;
-    if (tid == 0) {
-        L.item_start[h] = h * dense_chunks;
-        if (h == (int)gridDim.x - 1) L.item_start[h + 1] = (h + 1) * dense_chunks;
-        L.seg_off[h] = (int64_t)h * seg_bytes;
-        L.cap[h] = dense_cap;
-        L.n[h] = 0;
-        L.budget[h] = 0;
-        L.nstar[h] = 0;
-        L.label[h] = 0;
-        L.order[h] = h;
-    }
-    for (int i = tid; i < d; i += kBlock) L.qsum[(size_t)h * d + i] = 0.0;
-    if (C == 0) return;
-    SegPtrs s = seg_ptrs(L.kv + (int64_t)h * seg_bytes, C, dense_cap, d);
-    const int n16 = C * d / 8;
-    const uint4* ks = reinterpret_cast<const uint4*>(kc + (size_t)h * C * d);
-    const uint4* vs = reinterpret_cast<const uint4*>(vc + (size_t)h * C * d);
-    uint4* kd = reinterpret_cast<uint4*>(s.K);
-    uint4* vd = reinterpret_cast<uint4*>(s.V);
-    for (int i = tid; i < n16; i += kBlock) {
-        kd[i] = ks[i];
-        vd[i] = vs[i];
-    }
+    prefill_head(L, blockIdx.x, gridDim.x, C, d, kc, vc, seg_bytes, dense_cap, dense_chunks, 0, C,
+                 true, threadIdx.x, kBlock);
 }
 
 __global__ void k_append(LayerDev L, int C, int d, AppendArgs a) {

@@ -120,5 +120,42 @@ __device__ __forceinline__ void append_commit(const LayerDev& L, int h, int n, i
     if (tid == 0) L.n[h] = n + 1;
 }
 
+// Step 1 for head h of the dense layout, by the nthreads threads of a block:
+// layer state reset (segment, capacity, length 0, labels, query sum, the
+// dense chunk table) and, for prefix rows [r0, r1), the copy of the
+// conditional keys and values into the head's first rows.
+__device__ inline void prefill_head(const LayerDev& L, int h, int nheads, int C, int d,
+                                    const uint16_t* kc, const uint16_t* vc, int64_t seg_bytes,
+                                    int dense_cap, int dense_chunks, int r0, int r1,
+                                    bool reset, int tid, int nthreads) {
+    if (reset) {
+        for (int c = tid; c < dense_chunks; c += nthreads)
+            L.items[(size_t)h * dense_chunks + c] = ((uint32_t)h << 8) | (uint32_t)c;
+        if (tid == 0) {
+            L.item_start[h] = h * dense_chunks;
+            if (h == nheads - 1) L.item_start[h + 1] = (h + 1) * dense_chunks;
+            L.seg_off[h] = (int64_t)h * seg_bytes;
+            L.cap[h] = dense_cap;
+            L.n[h] = 0;
+            L.budget[h] = 0;
+            L.nstar[h] = 0;
+            L.label[h] = 0;
+            L.order[h] = h;
+        }
+        for (int i = tid; i < d; i += nthreads) L.qsum[(size_t)h * d + i] = 0.0;
+    }
+    if (r1 <= r0) return;
+    SegPtrs s = seg_ptrs(L.kv + (int64_t)h * seg_bytes, C, dense_cap, d);
+    const int w = d / 8;  // 16-byte pieces per row
+    const uint4* ks = reinterpret_cast<const uint4*>(kc + (size_t)h * C * d);
+    const uint4* vs = reinterpret_cast<const uint4*>(vc + (size_t)h * C * d);
+    uint4* kd = reinterpret_cast<uint4*>(s.K);
+    uint4* vd = reinterpret_cast<uint4*>(s.V);
+    for (int i = r0 * w + tid; i < r1 * w; i += nthreads) {
+        kd[i] = ks[i];
+        vd[i] = vs[i];
+    }
+}
+
 }  // namespace dev
 }  // namespace headkv

@@ -177,6 +177,21 @@ LayerDev dev_of(headkv_t h, const Layer& L) {
     return make_layer_dev(L.grouped ? L.ragged : L.dense, L.meta, h->ml);
 }
 
+// Event pair for a sampled launch of `kind`, or nullptrs.
+void take_events(headkv_t h, bool time_it, int kind, double bytes, void** e0, void** e1) {
+    *e0 = *e1 = nullptr;
+    if (!time_it) return;
+    if (2 * (h->timed + 1) > h->events.size()) {
+        ++h->timing_dropped;
+        return;
+    }
+    *e0 = h->events[2 * h->timed];
+    *e1 = h->events[2 * h->timed + 1];
+    h->timed_bytes[h->timed] = bytes;
+    h->timed_kind[h->timed] = kind;
+    ++h->timed;
+}
+
 }  // namespace
 
 extern "C" {
@@ -227,14 +242,26 @@ headkv_status headkv_create(const headkv_config* cfg, void* const* dense_kv, voi
 
 void headkv_destroy(headkv_t h) { delete h; }
 
-headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c, const uint16_t* v_c,
-                             void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Step 1 of `layer`: host mirror reset and one launch that resets the device
+// state and stores the prefix (with q_c, also the prefix attention).
+headkv_status prefill_impl(headkv_t h, int32_t layer, const uint16_t* q_c, const uint16_t* k_c,
+                           const uint16_t* v_c, float* out_c, void* stream) {
     headkv_status st = check_layer(h, layer);
     if (st) return st;
     const headkv_config& c = h->cfg;
     if (c.prefix_len > 0 && (!k_c || !v_c)) return fail(HEADKV_ERR_INVALID_ARG, "k_c / v_c is NULL");
     if (c.prefix_len > 0 && (!aligned(k_c, 16) || !aligned(v_c, 16)))
         return fail(HEADKV_ERR_INVALID_ARG, "k_c / v_c not 16-byte aligned");
+    if (q_c || out_c) {
+        if (c.prefix_len < 1) return fail(HEADKV_ERR_INVALID_ARG, "prefill attention needs prefix_len >= 1");
+        if (!q_c || !out_c) return fail(HEADKV_ERR_INVALID_ARG, "q_c / out_c is NULL");
+        if (!aligned(q_c, 16) || !aligned(out_c, 16))
+            return fail(HEADKV_ERR_INVALID_ARG, "q_c / out_c not 16-byte aligned");
+    }
     Layer& L = h->layers[layer];
     L.grouped = false;
     L.prefilled = false;
@@ -247,12 +274,40 @@ headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c, con
     L.chunk_threads = pick_chunk_threads(c.prefix_len, c.head_dim, L.cap);
     const int dense_chunks = chunks_of(c.prefix_len, h->dense_cap, L.chunk_threads, c.head_dim);
     L.items = h->shape.BH * dense_chunks;
-    st = hip_status(launch_prefill(dev_of(h, L), h->shape, k_c, v_c, h->dense_seg, h->dense_cap,
-                                   dense_chunks, stream),
-                    "prefill launch");
+    if (q_c) {
+        // timed whenever events are reserved: q, k, v read, k, v stored, fp32 out
+        const double Cd = (double)c.prefix_len * c.head_dim;
+        void *e0, *e1;
+        take_events(h, !h->events.empty(), HEADKV_TIMED_PREFILL,
+                    h->shape.BH * (3 * Cd * 2 + 2 * Cd * 2 + Cd * 4), &e0, &e1);
+        st = hip_status(launch_prefill_attn(dev_of(h, L), h->shape, q_c, k_c, v_c, out_c,
+                                            h->dense_seg, h->dense_cap, dense_chunks, stream,
+                                            e0, e1),
+                        "prefill attention launch");
+    }
+    else
+        st = hip_status(launch_prefill(dev_of(h, L), h->shape, k_c, v_c, h->dense_seg,
+                                       h->dense_cap, dense_chunks, stream),
+                        "prefill launch");
     if (st) return st;
     L.prefilled = true;
     return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+headkv_status headkv_prefill(headkv_t h, int32_t layer, const uint16_t* k_c, const uint16_t* v_c,
+                             void* stream) {
+    return prefill_impl(h, layer, nullptr, k_c, v_c, nullptr, stream);
+}
+
+headkv_status headkv_prefill_attn(headkv_t h, int32_t layer, const uint16_t* q_c,
+                                  const uint16_t* k_c, const uint16_t* v_c, float* out_c,
+                                  void* stream) {
+    if (!q_c || !out_c) return fail(HEADKV_ERR_INVALID_ARG, "q_c / out_c is NULL");
+    return prefill_impl(h, layer, q_c, k_c, v_c, out_c, stream);
 }
 
 }  // extern "C"
@@ -436,21 +491,6 @@ double update_bytes(headkv_t h, const Layer& L) {
         }
     }
     return b;
-}
-
-// Event pair for a sampled launch of `kind`, or nullptrs.
-void take_events(headkv_t h, bool time_it, int kind, double bytes, void** e0, void** e1) {
-    *e0 = *e1 = nullptr;
-    if (!time_it) return;
-    if (2 * (h->timed + 1) > h->events.size()) {
-        ++h->timing_dropped;
-        return;
-    }
-    *e0 = h->events[2 * h->timed];
-    *e1 = h->events[2 * h->timed + 1];
-    h->timed_bytes[h->timed] = bytes;
-    h->timed_kind[h->timed] = kind;
-    ++h->timed;
 }
 
 headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,

@@ -116,6 +116,12 @@ struct AppendArgs {
 int launch_prefill(const LayerDev& L, const Shape& s, const uint16_t* kc, const uint16_t* vc,
                    int64_t dense_seg_bytes, int dense_cap, int dense_chunks, void* stream);
 int launch_append(const LayerDev& L, const Shape& s, const AppendArgs& a, void* stream);
+// Causal attention over the C >= 1 prefix tokens of every head, fused with
+// launch_prefill's work (prefill_attn.hip).
+int launch_prefill_attn(const LayerDev& L, const Shape& s, const uint16_t* qc, const uint16_t* kc,
+                        const uint16_t* vc, float* out, int64_t dense_seg_bytes, int dense_cap,
+                        int dense_chunks, void* stream, void* ev_start = nullptr,
+                        void* ev_stop = nullptr);
 int launch_score(const LayerDev& L, const Shape& s, const uint16_t* q, int32_t* n_star,
                  uint8_t* is_local, int len, double sqrt_d, double tau, int local_window,
                  void* stream);

@@ -24,6 +24,7 @@ class DeviceInputs:
         self.wl = wl
         self.layers = list(range(wl.layers)) if layers is None else list(layers)
         self.q, self.k, self.v, self.kc, self.vc, self.override = {}, {}, {}, {}, {}, {}
+        self.qc = {}
         ov = synth.budget_override(wl)
         N = wl.num_visual
         for l in self.layers:
@@ -36,11 +37,13 @@ class DeviceInputs:
                 q[t0:t1], k[t0:t1], v[t0:t1] = synth.visual_qkv(wl, l, t0, t1, device, seed)
             self.q[l], self.k[l], self.v[l] = q, k, v
             self.kc[l], self.vc[l] = synth.prefix_kv(wl, l, device, seed)
+            self.qc[l] = synth.prefix_q(wl, l, device, seed)
             self.override[l] = (None if ov is None else
                                 torch.from_numpy(ov[l].reshape(-1).copy()).to(device))
 
     def nbytes(self) -> int:
-        return sum(t.numel() * t.element_size() for d in (self.q, self.k, self.v, self.kc, self.vc)
+        return sum(t.numel() * t.element_size()
+                   for d in (self.q, self.k, self.v, self.kc, self.vc, self.qc)
                    for t in d.values())
 
 
@@ -100,13 +103,15 @@ def new_session(wl: Workload, layers: Optional[int] = None, **kw) -> Session:
 
 def run_generation_native(sess: Session, inp: DeviceInputs, outs: Dict[int, torch.Tensor],
                           timing_every: int = 0,
-                          label_override: Optional[Dict[int, torch.Tensor]] = None) -> Dict:
+                          label_override: Optional[Dict[int, torch.Tensor]] = None,
+                          prefill_out: Optional[Dict[int, torch.Tensor]] = None) -> Dict:
     """The same generation with the step loop in the library (headkv_run_steps):
     steps before and after the grouping step run from one host call each; the
-    grouping step uses the separate calls.  Needs the inputs of every layer of
-    the handle.  label_override: per layer [B*H] uint8 labels that replace the
-    grouping's for the budgets and updates.  Returns labels, n* and budgets per
-    layer."""
+    grouping step uses the separate calls; the prefix goes through the prefill
+    attention (headkv_prefill_attn, whose outputs land in `prefill_out` when
+    given).  Needs the inputs of every layer of the handle.  label_override: per
+    layer [B*H] uint8 labels that replace the grouping's for the budgets and
+    updates.  Returns labels, n* and budgets per layer."""
     wl = inp.wl
     L = sess.cfg.num_layers
     assert inp.layers == list(range(L)), "the native loop runs every layer"
@@ -120,7 +125,11 @@ def run_generation_native(sess: Session, inp: DeviceInputs, outs: Dict[int, torc
     st = sess.stream()
     res = {"n_star": {}, "is_local": {}, "budgets": {}}
     for l in range(L):
-        sess.prefill(l, inp.kc[l], inp.vc[l])
+        if wl.prefix_len > 0:
+            po = None if prefill_out is None else prefill_out[l]
+            sess.prefill_attn(l, inp.qc[l], inp.kc[l], inp.vc[l], po)
+        else:
+            sess.prefill(l, inp.kc[l], inp.vc[l])
     B.headkv_run_steps(sess.h, 0, t_g, qp, kp, vp, stride, op, timing_every, st)
     for l in range(L):
         q = inp.q[l][t_g]

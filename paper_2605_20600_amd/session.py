@@ -75,6 +75,13 @@ class Session:
     def prefill(self, layer: int, k_c: Optional[torch.Tensor], v_c: Optional[torch.Tensor]):
         B.headkv_prefill(self.h, layer, _ptr(k_c), _ptr(v_c), self.stream())
 
+    def prefill_attn(self, layer: int, q_c, k_c, v_c, out: Optional[torch.Tensor] = None):
+        if out is None:
+            out = torch.empty(q_c.shape, dtype=torch.float32, device=self.device)
+        B.headkv_prefill_attn(self.h, layer, q_c.data_ptr(), k_c.data_ptr(), v_c.data_ptr(),
+                              out.data_ptr(), self.stream())
+        return out
+
     def append_and_evict(self, layer: int, step: int, q, k, v):
         B.headkv_append_and_evict(self.h, layer, step, q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                   self.stream())

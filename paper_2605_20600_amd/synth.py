@@ -35,7 +35,7 @@ SEED_AMP = 2606
 SEED_BUDGET = 2607
 POS_BASE = 10.0
 
-T_Q, T_K, T_V, T_KC, T_VC = 0, 1, 2, 3, 4
+T_Q, T_K, T_V, T_KC, T_VC, T_QC = 0, 1, 2, 3, 4, 5
 _M32 = 0xFFFFFFFF
 
 
@@ -193,6 +193,15 @@ def prefix_kv(wl: Workload, layer: int, device: str = "cpu",
     kc = _noise(wl, T_KC, layer, t, b, h, seed, device).to(torch.bfloat16)
     vc = _noise(wl, T_VC, layer, t, b, h, seed, device).to(torch.bfloat16)
     return kc.permute(1, 2, 0, 3).contiguous(), vc.permute(1, 2, 0, 3).contiguous()
+
+
+def prefix_q(wl: Workload, layer: int, device: str = "cpu",
+             seed: int = SEED_DATA) -> torch.Tensor:
+    """Conditional-token queries (for the prefill attention): bf16 [B][H][C][d]."""
+    t, b, h = _grid(0, wl.prefix_len, range(wl.batch), range(wl.heads), device)
+    t = t + wl.num_visual
+    qc = _noise(wl, T_QC, layer, t, b, h, seed, device).to(torch.bfloat16)
+    return qc.permute(1, 2, 0, 3).contiguous()
 
 
 def head_inputs(wl: Workload, layer: int, b: int, h: int, seed: int = SEED_DATA):

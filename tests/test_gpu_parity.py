@@ -294,3 +294,43 @@ def test_tiny_cfg_pairs_every_step():
 def test_llamagen_xl_cfg_sampled():
     wl = W.LLAMAGEN_XL
     _run_and_check(wl, [0, 35], [(0, 0), (35, 255)], _steps(wl, extra=(250,)))
+
+
+# ---- prefill: causal attention over the conditional tokens (MFMA) ----
+
+@pytest.mark.parametrize("wl", [W.TINY, W.JANUS7B.with_(layers=1), W.LUMINA768.with_(layers=1),
+                                W.LLAMAGEN_XL.with_(layers=1, batch=4),
+                                W.LUMINA768.with_(layers=1, prefix_len=77, batch=2),
+                                W.LUMINA768.with_(layers=1, prefix_len=300, batch=1)],
+                         ids=["tiny", "janus", "lumina768", "llamagen", "c77", "c300"])
+def test_prefill_attention(wl):
+    qc = synth.prefix_q(wl, 0, "cuda")
+    kc, vc = synth.prefix_kv(wl, 0, "cuda")
+    sess = new_session(wl)
+    out = sess.prefill_attn(0, qc, kc, vc)
+    torch.cuda.synchronize()
+    out = out.cpu().double().numpy()
+    qh, kh, vh = qc.cpu(), kc.cpu(), vc.cpu()
+    BH = wl.batch * wl.heads
+    worst = 0.0
+    for i in sorted({0, BH // 3, BH - 1}):
+        b, h = divmod(i, wl.heads)
+        ref = oracle.prefill_attention(qh[b, h], kh[b, h], vh[b, h])
+        err = float(np.abs(out[b, h] - ref).max())
+        worst = max(worst, err)
+        assert err <= ATOL, (b, h, err)
+    _say(f"prefill attention {wl.name} C={wl.prefix_len} d={wl.head_dim}: max err {worst:.2e}")
+
+
+def test_prefill_attention_then_decode():
+    # headkv_prefill_attn leaves the cache as headkv_prefill does
+    wl = W.TINY
+    inp = DeviceInputs(wl)
+    sess = new_session(wl)
+    sess.prefill_attn(0, inp.qc[0], inp.kc[0], inp.vc[0])
+    out = sess.decode_step(0, 0, inp.q[0][0], inp.k[0][0], inp.v[0][0])
+    torch.cuda.synchronize()
+    for h in range(wl.heads):
+        q, k, v, kc, vc = synth.head_inputs(wl, 0, 0, h)
+        ref = oracle.attention(q[0], torch.cat([kc, k[:1]]), torch.cat([vc, v[:1]]))
+        assert np.abs(out[0, h].cpu().double().numpy() - ref).max() <= ATOL

@@ -383,3 +383,24 @@ def test_cfg_pairs_follow_the_conditional_row():
         assert np.array_equal(a["snaps"][h], b["snaps"][h])
     g = oracle.group_layer(wl, 0)
     assert np.array_equal(g["budgets"][1], g["budgets"][0])
+
+
+def test_prefill_attention_pins():
+    # causal attention over the prefix: the first token sees only itself, and
+    # with identical keys every token averages the values up to itself
+    rng = np.random.default_rng(5)
+    C, d = 9, 16
+    qc = torch.from_numpy(rng.standard_normal((C, d)))
+    kc = torch.from_numpy(rng.standard_normal((C, d)))
+    vc = torch.from_numpy(rng.standard_normal((C, d)))
+    o = oracle.prefill_attention(qc, kc, vc)
+    assert np.allclose(o[0], vc[0].numpy(), rtol=0, atol=1e-15)
+    same = kc[:1].repeat(C, 1)
+    o = oracle.prefill_attention(qc, same, vc)
+    for i in range(C):
+        assert np.allclose(o[i], vc[: i + 1].numpy().mean(axis=0), rtol=0, atol=1e-12)
+    # a key far ahead of the others takes all the weight once it is visible
+    kc2 = kc.clone()
+    kc2[4] = 50.0 * qc[6] / qc[6].norm()
+    o = oracle.prefill_attention(qc, kc2, vc)
+    assert np.allclose(o[6], vc[4].numpy(), atol=1e-6)
