@@ -62,7 +62,7 @@ def parse():
                    help="write the attention kernel's traffic record from four rocprofv3 --pmc "
                         "output folders (kernel FETCH_SIZE, kernel WRITE_SIZE, copy probe "
                         "FETCH_SIZE, copy probe WRITE_SIZE) and exit; no GPU needed")
-    p.add_argument("--traffic-kernel", default="k_attn<128, true, 1024, false>",
+    p.add_argument("--traffic-kernel", default="k_attn<128, true, 1024, false, 8>",
                    help="kernel name the traffic record is taken for")
     return p.parse_args()
 
@@ -297,9 +297,11 @@ def main():
     per_kind, dropped = B.headkv_timing_collect(sess.h)
     C, d = wl.prefix_len, wl.head_dim
     pre_flops = wl.batch * wl.heads * 4 * d * C * (C + 1) / 2  # causal QK^T and PV
-    names = ["k_attn<d, append> (headkv_decode_step)", "k_attn<d> (after an update)",
+    names = ["k_attn<d, append> (headkv_decode_step, compressed cache)",
+             "k_attn<d> (after an update)",
              "k_update<d> (append + periodic update)",
-             "k_prefill_attn<d> (prefix store + causal attention, headkv_prefill_attn)"]
+             "k_prefill_attn<d> (prefix store + causal attention, headkv_prefill_attn)",
+             "k_attn<d, append> (headkv_decode_step, full cache before grouping)"]
     kinds = {}
     for name, (kms, kn, kb) in zip(names, per_kind):
         if kn:

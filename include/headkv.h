@@ -224,11 +224,14 @@ headkv_status headkv_run_steps(headkv_t h, int32_t step_begin, int32_t step_end,
 headkv_status headkv_timing_reserve(headkv_t h, int64_t launches);
 
 /* Kinds of timed launches. */
-#define HEADKV_TIMED_ATTN_APPEND 0 /* fused append + attention (one kernel) */
-#define HEADKV_TIMED_ATTN 1        /* attention after an update or a split append */
+#define HEADKV_TIMED_ATTN_APPEND 0 /* fused append + attention over the
+                                      compressed cache (after grouping) */
+#define HEADKV_TIMED_ATTN 1        /* attention after an update */
 #define HEADKV_TIMED_UPDATE 2      /* append + periodic update */
 #define HEADKV_TIMED_PREFILL 3     /* prefix store + causal prefix attention */
-#define HEADKV_TIMED_KINDS 4
+#define HEADKV_TIMED_ATTN_APPEND_DENSE 4 /* fused append + attention before
+                                            grouping (full cache) */
+#define HEADKV_TIMED_KINDS 5
 
 /* Waits for the timed launches since the last collect and returns, per kind
  * (arrays of HEADKV_TIMED_KINDS), the sum of their kernel durations (ms), their

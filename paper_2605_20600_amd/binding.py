@@ -191,10 +191,11 @@ def headkv_timing_reserve(h: int, launches: int) -> None:
 
 
 def headkv_timing_collect(h: int):
-    """Returns per kind (fused append + attention, attention, append + update,
-    prefill) a list of (kernel ms, launches, algorithmic bytes), and the
+    """Returns per kind (fused append + attention after grouping, attention
+    after an update, append + update, prefill, fused append + attention before
+    grouping) a list of (kernel ms, launches, algorithmic bytes), and the
     dropped count."""
-    K = 4
+    K = 5
     ms = (ctypes.c_double * K)()
     n = (ctypes.c_int64 * K)()
     b = (ctypes.c_double * K)()

@@ -523,8 +523,8 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
     }
     // the append is fused into the attention (its length committed by the
     // attention block or by the merge kernel)
-    take_events(h, time_it, HEADKV_TIMED_ATTN_APPEND, fused_step_bytes(h, L, a.accumulate != 0),
-                &e0, &e1);
+    take_events(h, time_it, L.grouped ? HEADKV_TIMED_ATTN_APPEND : HEADKV_TIMED_ATTN_APPEND_DENSE,
+                fused_step_bytes(h, L, a.accumulate != 0), &e0, &e1);
     st = hip_status(launch_attention(h, L, D, a, q, out, stream, e0, e1),
                     "append + attention launch");
     if (st) return st;
