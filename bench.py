@@ -58,6 +58,11 @@ def parse():
                    help="print, as one JSON line, how the head labels found when grouping at the "
                         "first threshold (visual tokens) change when grouping runs at the later "
                         "ones, on the GPU, and exit")
+    p.add_argument("--all-layer-launch", action="store_true",
+                   help="after one generation, time the attention of the last step over every "
+                        "layer as one launch (headkv_decode_attn_layers) and as one launch per "
+                        "layer, print one JSON line and exit (a kernel-efficiency bound: a decoder "
+                        "cannot launch its layers together)")
     p.add_argument("--traffic-record", nargs=4, metavar="DIR",
                    help="write the attention kernel's traffic record from four rocprofv3 --pmc "
                         "output folders (kernel FETCH_SIZE, kernel WRITE_SIZE, copy probe "
@@ -223,6 +228,59 @@ def label_stability(wl, thresholds):
                       "reference_threshold": thresholds[0], "rows": rows}), flush=True)
 
 
+def all_layer_launch(wl, reps: int = 20):
+    """Attention of the last step of a generation, over all layers: one launch
+    per layer (as a decoder runs it) vs one launch for all layers, same
+    results; times from events on the launch stream, per layer."""
+    import numpy as np
+    import torch
+    from paper_2605_20600_amd import binding as B
+    from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation_native
+    inp = DeviceInputs(wl)
+    sess = new_session(wl)
+    L = wl.layers
+    outs = {l: torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32, device="cuda")
+            for l in range(L)}
+    run_generation_native(sess, inp, outs)
+    q = [inp.q[l][wl.num_visual - 1] for l in range(L)]
+    o1 = [torch.empty_like(outs[l]) for l in range(L)]
+    o2 = [torch.empty_like(outs[l]) for l in range(L)]
+    st = sess.stream()
+
+    def per_layer():
+        for l in range(L):
+            B.headkv_decode_attn(sess.h, l, q[l].data_ptr(), o1[l].data_ptr(), st)
+
+    def together():
+        B.headkv_decode_attn_layers(sess.h, 0, L, [x.data_ptr() for x in q],
+                                    [x.data_ptr() for x in o2], st)
+
+    res = {}
+    for name, fn in (("per_layer", per_layer), ("all_layers", together)):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        res[name] = e0.elapsed_time(e1) / reps / L * 1e3  # us per layer
+    same = max(float((a - b).abs().max()) for a, b in zip(o1, o2))
+    C, d = wl.prefix_len, wl.head_dim
+    tokens = 0
+    for l in range(L):
+        _, count = sess.export_retained(l)
+        tokens += int(count.sum()) + C * wl.batch * wl.heads
+    per_layer_bytes = (tokens * 2 * d * 2 + L * wl.batch * wl.heads * (2 * d + 4 * d)) / L
+    line = {"workload": wl.name + "_shape", "step": wl.num_visual - 1, "layers": L,
+            "alg_bytes_per_layer": per_layer_bytes, "max_abs_diff": same,
+            "per_layer_launch_us": res["per_layer"], "all_layers_launch_us_per_layer": res["all_layers"],
+            "per_layer_launch_gbps": per_layer_bytes / (res["per_layer"] * 1e-6) / 1e9,
+            "all_layers_launch_gbps": per_layer_bytes / (res["all_layers"] * 1e-6) / 1e9}
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -248,6 +306,9 @@ def main():
     wl = W.ALL[args.workload]
     if args.label_stability:
         label_stability(wl, [int(x) for x in args.label_stability.split(",")])
+        return
+    if args.all_layer_launch:
+        all_layer_launch(wl)
         return
     if args.rho is not None:
         wl = wl.with_(rho=tuple(int(x) for x in args.rho.split("/")))

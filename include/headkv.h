@@ -193,6 +193,17 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
 headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q,
                                  float* out, void* stream);
 
+/* Decode attention of layers [layer_begin, layer_end) in one launch, with the
+ * results of headkv_decode_attn on each.  q, out: host arrays (indexed by
+ * layer - layer_begin) of device pointers as for headkv_decode_attn.  For
+ * callers that hold several layers' queries at once; a decoder whose next
+ * layer needs this one's output calls headkv_decode_attn per layer.  At most
+ * 64 layers; needs at least 256 (batch x heads) and HEADKV_ATTN_VARLEN
+ * (HEADKV_ERR_UNSUPPORTED otherwise). */
+headkv_status headkv_decode_attn_layers(headkv_t h, int32_t layer_begin, int32_t layer_end,
+                                        const uint16_t* const* q, float* const* out,
+                                        void* stream);
+
 /* One whole decode step of `layer` in the fewest launches: the append of
  * headkv_append_and_evict (with its periodic update when due) followed by the
  * attention of headkv_decode_attn, with identical results.  Without an update

@@ -32,7 +32,8 @@ ATTN_STRATEGIES = {"varlen": HEADKV_ATTN_VARLEN, "padded": HEADKV_ATTN_PADDED,
 EXPORTED = (
     "headkv_plan", "headkv_create", "headkv_destroy", "headkv_prefill", "headkv_prefill_attn",
     "headkv_append_and_evict", "headkv_score_heads", "headkv_assign_budgets",
-    "headkv_decode_attn", "headkv_decode_step", "headkv_export_retained",
+    "headkv_decode_attn", "headkv_decode_attn_layers", "headkv_decode_step",
+    "headkv_export_retained",
     "headkv_run_steps", "headkv_timing_reserve", "headkv_timing_collect",
     "headkv_last_error",
 )
@@ -82,6 +83,7 @@ def load() -> ctypes.CDLL:
         "headkv_assign_budgets": [P, I, P, P, P, P, Z, ctypes.POINTER(Z), P],
         "headkv_decode_attn": [P, I, P, P, P],
         "headkv_decode_step": [P, I, I, P, P, P, P, P],
+        "headkv_decode_attn_layers": [P, I, I, P, P, P],
         "headkv_export_retained": [P, I, P, P, P],
         "headkv_run_steps": [P, I, I, P, P, P, ctypes.c_int64, P, I, P],
         "headkv_timing_reserve": [P, ctypes.c_int64],
@@ -166,6 +168,15 @@ def headkv_assign_budgets(h: int, layer: int, is_local: int, budget_override: Op
 
 def headkv_decode_attn(h: int, layer: int, q: int, out: int, stream: int = 0) -> None:
     _check(load().headkv_decode_attn(h, layer, q, out, stream), "headkv_decode_attn")
+
+
+def headkv_decode_attn_layers(h: int, layer_begin: int, layer_end: int, q: Sequence[int],
+                              out: Sequence[int], stream: int = 0) -> None:
+    n = layer_end - layer_begin
+    qa = (ctypes.c_void_p * n)(*q)
+    oa = (ctypes.c_void_p * n)(*out)
+    _check(load().headkv_decode_attn_layers(h, layer_begin, layer_end, qa, oa, stream),
+           "headkv_decode_attn_layers")
 
 
 def headkv_decode_step(h: int, layer: int, step: int, q: int, k: int, v: int, out: int,

@@ -97,12 +97,15 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
     }
 }
 
-// 4 wavefronts per SIMD (16 per CU) at every block size: at most 128 VGPRs.
-// TPR tokens per row and pass: 8, or 4 when every head fits in half a pass.
+// The work of one attention block; `item` is its index among the blocks of
+// the layer.  TPR tokens per row and pass: 8, or 4 when every head fits in
+// half a pass.
 template <int D, bool APPEND, int T, bool CHUNKED, int TPR>
-__global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_attn(
-    LayerDev L, int C, AppendArgs a, const uint16_t* __restrict__ q, float* __restrict__ out,
-    float* __restrict__ part, int use_order, int order_base, int pad_len, float qscale) {
+__device__ __forceinline__ void attn_block(const LayerDev& L, int C, const AppendArgs& a,
+                                           const uint16_t* __restrict__ q,
+                                           float* __restrict__ out, float* __restrict__ part,
+                                           int use_order, int order_base, int pad_len,
+                                           float qscale, int item) {
     using Vec = typename AttnRegs<D>::Vec;
     constexpr int VPL = AttnRegs<D>::VPL;
     constexpr int NW = AttnRegs<D>::NW;
@@ -112,11 +115,11 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
     constexpr int WAVES = T / 64;
     int h, t_begin;
     if (CHUNKED) {
-        const uint32_t it = L.items[blockIdx.x];
+        const uint32_t it = L.items[item];
         h = (int)(it >> 8);
         t_begin = (int)(it & 255u) * TP;
     } else {
-        h = use_order ? L.order[order_base + (int)blockIdx.x] : (int)blockIdx.x;
+        h = use_order ? L.order[order_base + item] : item;
         t_begin = 0;
     }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -224,7 +227,7 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
         if (!CHUNKED) {
             out[(size_t)h * D + tid] = o / z;
         } else {
-            float* pp = part + (size_t)blockIdx.x * (D + 2);
+            float* pp = part + (size_t)item * (D + 2);
             pp[tid] = o;
             if (tid == 0) {
                 pp[D] = mx;
@@ -232,6 +235,26 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
             }
         }
     }
+}
+
+// 4 wavefronts per SIMD (16 per CU) at every block size: at most 128 VGPRs.
+template <int D, bool APPEND, int T, bool CHUNKED, int TPR>
+__global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_attn(
+    LayerDev L, int C, AppendArgs a, const uint16_t* __restrict__ q, float* __restrict__ out,
+    float* __restrict__ part, int use_order, int order_base, int pad_len, float qscale) {
+    attn_block<D, APPEND, T, CHUNKED, TPR>(L, C, a, q, out, part, use_order, order_base, pad_len,
+                                           qscale, (int)blockIdx.x);
+}
+
+// Several layers in one launch: layer blockIdx.x / BH, head blockIdx.x % BH.
+template <int D, int T, int TPR>
+__global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_attn_layers(
+    LayersArg args, MetaLayout ml, int BH, int C, float qscale) {
+    const int layer = (int)blockIdx.x / BH;
+    const LayerDev L = make_layer_dev(args.kv[layer], args.meta[layer], ml);
+    const AppendArgs none{};
+    attn_block<D, false, T, false, TPR>(L, C, none, args.q[layer], args.out[layer], nullptr, 0, 0,
+                                        0, qscale, (int)blockIdx.x - layer * BH);
 }
 
 // Merge of the chunks of every head: a kernel of its own, since plain device
@@ -306,6 +329,30 @@ void attn_dispatch(const LayerDev& L, const Shape& s, const AppendArgs& a, const
 
 }  // namespace
 
+template <int D, int T>
+void layers_launch(const LayersArg& a, int layers, const MetaLayout& ml, const Shape& s, int tpr,
+                   hipStream_t st) {
+    const float qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
+    const dim3 grid((unsigned)layers * (unsigned)s.BH), block(T);
+    if (tpr == kAttnTpr)
+        hipLaunchKernelGGL((k_attn_layers<D, T, kAttnTpr>), grid, block, 0, st, a, ml, s.BH, s.C,
+                           qscale);
+    else
+        hipLaunchKernelGGL((k_attn_layers<D, T, kAttnTpr / 2>), grid, block, 0, st, a, ml, s.BH,
+                           s.C, qscale);
+}
+
+template <int D>
+void layers_dispatch(const LayersArg& a, int layers, const MetaLayout& ml, const Shape& s,
+                     int threads, int tpr, hipStream_t st) {
+    if (threads == 1024)
+        layers_launch<D, 1024>(a, layers, ml, s, tpr, st);
+    else if (threads == 512)
+        layers_launch<D, 512>(a, layers, ml, s, tpr, st);
+    else
+        layers_launch<D, 256>(a, layers, ml, s, tpr, st);
+}
+
 int launch_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
                 float* out, float* partials, const AttnPlan& p, void* stream, void* ev_start,
                 void* ev_stop) {
@@ -314,6 +361,15 @@ int launch_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, const ui
         attn_dispatch<128>(L, s, a, q, out, partials, p, (hipStream_t)stream, e0, e1);
     else
         attn_dispatch<64>(L, s, a, q, out, partials, p, (hipStream_t)stream, e0, e1);
+    return last_error();
+}
+
+int launch_attn_layers(const LayersArg& a, int layers, const MetaLayout& ml, const Shape& s,
+                       int threads, int tpr, void* stream) {
+    if (s.d == 128)
+        layers_dispatch<128>(a, layers, ml, s, threads, tpr, (hipStream_t)stream);
+    else
+        layers_dispatch<64>(a, layers, ml, s, threads, tpr, (hipStream_t)stream);
     return last_error();
 }
 

@@ -749,6 +749,42 @@ headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, f
                       "attention launch");
 }
 
+headkv_status headkv_decode_attn_layers(headkv_t h, int32_t layer_begin, int32_t layer_end,
+                                        const uint16_t* const* q, float* const* out,
+                                        void* stream) {
+    if (!h) return fail(HEADKV_ERR_INVALID_ARG, "handle is NULL");
+    if (!q || !out) return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer array");
+    const int n = layer_end - layer_begin;
+    if (layer_begin < 0 || layer_end > h->cfg.num_layers || n < 1)
+        return fail(HEADKV_ERR_INVALID_ARG, "bad layer range");
+    if (n > kMaxLayersPerLaunch) return fail(HEADKV_ERR_UNSUPPORTED, "more than 64 layers");
+    const int BH = h->shape.BH;
+    if (BH < kCus || h->cfg.attn_strategy != HEADKV_ATTN_VARLEN)
+        return fail(HEADKV_ERR_UNSUPPORTED, "multi-layer attention needs >= 256 heads and the varlen strategy");
+    LayersArg args{};
+    int len_max = 0;
+    for (int i = 0; i < n; ++i) {
+        Layer& L = h->layers[layer_begin + i];
+        if (!q[i] || !out[i]) return fail(HEADKV_ERR_INVALID_ARG, "NULL layer pointer");
+        if (!L.prefilled || L.last_step < 0)
+            return fail(HEADKV_ERR_STATE, "decode_attn before the first append");
+        if (!L.grouped && L.last_step == h->t_g)
+            return fail(HEADKV_ERR_STATE, "assign_budgets must run before attention at step group_threshold - 1");
+        args.kv[i] = L.grouped ? L.ragged : L.dense;
+        args.meta[i] = L.meta;
+        args.q[i] = q[i];
+        args.out[i] = out[i];
+        len_max = std::max(len_max, h->cfg.prefix_len + *std::max_element(L.n.begin(), L.n.end()));
+    }
+    const int t = resident_threads(BH);
+    if (BH > attn_resident_blocks(t))
+        return fail(HEADKV_ERR_UNSUPPORTED, "multi-layer attention needs every head resident");
+    const int tpr = len_max <= attn_tokens_per_pass(t, h->cfg.head_dim, kAttnTpr / 2) ? kAttnTpr / 2
+                                                                                      : kAttnTpr;
+    return hip_status(launch_attn_layers(args, n, h->ml, h->shape, t, tpr, stream),
+                      "multi-layer attention launch");
+}
+
 headkv_status headkv_export_retained(headkv_t h, int32_t layer, uint8_t* mask, int32_t* count,
                                      void* stream) {
     headkv_status st = check_layer(h, layer);

@@ -79,6 +79,9 @@ struct LayerDev {
     int32_t* item_start;  // [BH + 1]
 };
 
+#if defined(__HIPCC__)
+__host__ __device__
+#endif
 inline LayerDev make_layer_dev(void* kv, void* meta, const MetaLayout& m) {
     char* b = static_cast<char*>(meta);
     LayerDev L;
@@ -151,6 +154,18 @@ struct AttnPlan {
     int tpr;         // tokens per row and pass: kAttnTpr, or half of it (one
                      // block per head, every head within half a pass)
 };
+// Per-layer pointers of a multi-layer attention launch (up to kMaxLayersPerLaunch).
+constexpr int kMaxLayersPerLaunch = 64;
+struct LayersArg {
+    void* kv[kMaxLayersPerLaunch];
+    void* meta[kMaxLayersPerLaunch];
+    const uint16_t* q[kMaxLayersPerLaunch];
+    float* out[kMaxLayersPerLaunch];
+};
+// Attention of `layers` layers (no append, one block per head, every head
+// resident): heads of layer i are blocks i*BH .. i*BH + BH - 1.
+int launch_attn_layers(const LayersArg& a, int layers, const MetaLayout& ml, const Shape& s,
+                       int threads, int tpr, void* stream);
 // a.k == nullptr: no append.  partials: (d + 2) floats per table entry.
 // ev_start / ev_stop (hipEvent_t or nullptr) receive the attention kernel's
 // own start and end timestamps.

@@ -334,3 +334,25 @@ def test_prefill_attention_then_decode():
         q, k, v, kc, vc = synth.head_inputs(wl, 0, 0, h)
         ref = oracle.attention(q[0], torch.cat([kc, k[:1]]), torch.cat([vc, v[:1]]))
         assert np.abs(out[0, h].cpu().double().numpy() - ref).max() <= ATOL
+
+
+def test_decode_attn_layers_matches_per_layer():
+    # one launch for several layers gives the per-layer results
+    wl = W.LUMINA768.with_(layers=3)
+    inp = DeviceInputs(wl)
+    sess = new_session(wl)
+    t_end = wl.group_threshold + 2 * wl.period + 5
+    run_generation(sess, inp, steps=t_end)
+    t = t_end - 1
+    q = [inp.q[l][t] for l in range(3)]
+    per = [sess.decode_attn(l, q[l]) for l in range(3)]
+    together = [torch.empty_like(p) for p in per]
+    B.headkv_decode_attn_layers(sess.h, 0, 3, [x.data_ptr() for x in q],
+                                [x.data_ptr() for x in together], sess.stream())
+    torch.cuda.synchronize()
+    for l in range(3):
+        assert float((per[l] - together[l]).abs().max()) <= 1e-5
+    ref = oracle.simulate(wl, 1, 4, snap_steps=[t])
+    got = together[1][4].cpu().double().numpy()
+    for h in range(wl.heads):
+        assert np.abs(got[h] - ref["out"][h][t]).max() <= ATOL
