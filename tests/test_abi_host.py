@@ -127,3 +127,37 @@ def test_override_mode_requires_budgets():
                        ctypes.byref(need), None) == B.HEADKV_ERR_INVALID_ARG
     finally:
         B.headkv_destroy(h)
+
+
+def test_prefill_attention_and_multi_layer_arguments():
+    h, cfg = _handle()
+    try:
+        I, U, S = B.HEADKV_ERR_INVALID_ARG, B.HEADKV_ERR_UNSUPPORTED, B.HEADKV_ERR_STATE
+        assert _status("headkv_prefill_attn", h, 0, None, FAKE, FAKE, FAKE, None) == I
+        assert _status("headkv_prefill_attn", h, 0, FAKE, FAKE, FAKE, None, None) == I
+        assert _status("headkv_prefill_attn", h, 0, FAKE + 2, FAKE, FAKE, FAKE, None) == I
+        arr = (ctypes.c_void_p * 1)(FAKE)
+        assert _status("headkv_decode_attn_layers", h, 0, 2, arr, arr, None) == I   # range
+        assert _status("headkv_decode_attn_layers", h, 0, 1, None, arr, None) == I
+        # Tiny has 4 heads: fewer than the CUs the one-launch plan needs
+        assert _status("headkv_decode_attn_layers", h, 0, 1, arr, arr, None) == U
+    finally:
+        B.headkv_destroy(h)
+    wl = W.LUMINA768.with_(layers=2)
+    cfg = make_config(wl)
+    h = B.headkv_create(cfg, [FAKE] * 2, [FAKE + 4096] * 2, FAKE)
+    try:
+        arr = (ctypes.c_void_p * 2)(FAKE, FAKE)
+        assert _status("headkv_decode_attn_layers", h, 0, 2, arr, arr, None) == B.HEADKV_ERR_STATE
+    finally:
+        B.headkv_destroy(h)
+
+
+def test_cfg_pairs_need_an_even_batch():
+    cfg = make_config(W.TINY)
+    cfg.cfg_pairs = 1
+    with pytest.raises(B.HeadKVError) as e:
+        B.headkv_plan(cfg)
+    assert e.value.status == B.HEADKV_ERR_INVALID_ARG
+    cfg.batch = 2
+    B.headkv_plan(cfg)
