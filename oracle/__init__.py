@@ -21,6 +21,7 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 BUDGET_PAPER, BUDGET_OVERRIDE, BUDGET_TOTAL = 0, 1, 2
+SCORE_MEAN_LOGIT, SCORE_ATTN_SUM = 0, 1
 
 
 def build(force: bool = True) -> str:
@@ -46,10 +47,11 @@ def lib():
         L.orc_group_head.argtypes = [P, P, i, i, ctypes.c_double, i, P, P, P, P]
         L.orc_budgets.argtypes = [i, i, P, P, i, i, i, i, i, P]
         L.orc_update.argtypes = [P, P, P, i, P, i, i, i, i, i, i, P, P]
+        L.orc_update_ex.argtypes = [P, P, P, i, P, i, i, i, i, i, i, i, P, i, i, P, i, P, P]
         L.orc_run_head.argtypes = [P, P, P, P, P, i, i, i, i, i, i, i, i, i, i,
-                                   P, P, i, P, P]
+                                   P, P, i, P, P, i]
         for f in (L.orc_attention, L.orc_group_head, L.orc_budgets, L.orc_update,
-                  L.orc_run_head):
+                  L.orc_update_ex, L.orc_run_head):
             f.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -111,24 +113,31 @@ def budgets(mode: int, labels: Sequence[int], N: int, row_len: int, recent_len: 
 
 
 def update(ret: Sequence[int], Kvis, qsum, budget: int, is_local: bool, recent_len: int,
-           r_s=(1, 2), u: int = 0):
-    """One periodic update (Eqs. 2-6).  Returns (new retained positions, gap)."""
+           r_s=(1, 2), u: int = 0, score_mode: int = SCORE_MEAN_LOGIT, Qwin=None,
+           first_step: int = 0, Kc=None):
+    """One periodic update (Eqs. 2-6).  Returns (new retained positions, gap).
+    score_mode SCORE_ATTN_SUM scores with the window queries Qwin (steps
+    first_step ..) over the prefix keys Kc and the retained keys."""
     r = np.zeros(max(len(ret), 1), np.int32)
     r[: len(ret)] = np.asarray(ret, dtype=np.int32)
     n = np.array([len(ret)], np.int32)
     Kv = _f64(Kvis)
     qs = None if qsum is None else _f64(qsum)
+    Qw = None if Qwin is None else _f64(Qwin)
+    Kc_ = None if Kc is None else _f64(Kc)
     ev = np.zeros(1, np.int32)
     gap = np.zeros(1, np.float64)
-    _check(lib().orc_update(_p(r), _p(n), _p(Kv), Kv.shape[1], _p(qs), int(budget),
-                            int(bool(is_local)), int(recent_len), int(r_s[0]), int(r_s[1]),
-                            int(u), _p(ev), _p(gap)), "update")
+    _check(lib().orc_update_ex(_p(r), _p(n), _p(Kv), Kv.shape[1], _p(qs), int(budget),
+                               int(bool(is_local)), int(recent_len), int(r_s[0]), int(r_s[1]),
+                               int(u), int(score_mode), _p(Qw), 0 if Qw is None else Qw.shape[0],
+                               int(first_step), _p(Kc_), 0 if Kc_ is None else Kc_.shape[0],
+                               _p(ev), _p(gap)), "update")
     return r[: n[0]].copy(), float(gap[0])
 
 
 def run_head(q, k, v, kc, vc, t_g: int, P: int, is_local: bool, budget: int,
              recent_len: int, r_s=(1, 2), want_out: bool = True,
-             snap_steps: Sequence[int] = ()):
+             snap_steps: Sequence[int] = (), score_mode: int = SCORE_MEAN_LOGIT):
     """A whole generation of one head; returns (out [N][d] or None, snaps, stats)."""
     q, k, v, kc, vc = _f64(q), _f64(k), _f64(v), _f64(kc), _f64(vc)
     N, d = q.shape
@@ -140,7 +149,8 @@ def run_head(q, k, v, kc, vc, t_g: int, P: int, is_local: bool, budget: int,
     _check(lib().orc_run_head(_p(q), _p(k), _p(v), _p(kc), _p(vc), C, N, d, int(t_g), int(P),
                               int(bool(is_local)), int(budget), int(recent_len), int(r_s[0]),
                               int(r_s[1]), _p(out), _p(ss) if len(ss) else None, len(ss),
-                              _p(masks) if len(ss) else None, _p(stats)), "run_head")
+                              _p(masks) if len(ss) else None, _p(stats), int(score_mode)),
+           "run_head")
     return out, masks[: len(ss)], {"updates": int(stats[0]), "evicted": int(stats[1]),
                                     "min_gap": float(stats[2])}
 
@@ -190,7 +200,8 @@ def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
     def one(h):
         q, k, v, kc, vc = inputs[h]
         return h, run_head(q, k, v, kc, vc, t_g, wl.period, bool(used[h]), int(bud[h]),
-                           wl.recent_len, wl.r_s, want_out, snap_steps)
+                           wl.recent_len, wl.r_s, want_out, snap_steps,
+                           getattr(wl, "score_mode", SCORE_MEAN_LOGIT))
 
     # heads are independent; the C code runs without the GIL
     from concurrent.futures import ThreadPoolExecutor

@@ -153,11 +153,60 @@ static int int_cmp(const void* x, const void* y) {
     return (a > b) - (a < b);
 }
 
+/* Attention weight of each history token (positions ret[0..T-1]) summed over
+ * the window queries: query p (step first_step + p) attends over the cache it
+ * saw at its step -- the prefix, then the retained visual tokens with position
+ * <= its step, in position order -- with weights exp(l - max) / Z, Z summed in
+ * that cache order; the weights are added to the scores query by query. */
+static int window_attention_scores(const int32_t* ret, int n, int T, const double* Kvis,
+                                   int d, const double* Qwin, int n_win, int first_step,
+                                   const double* Kc, int C, double* score) {
+    const double sd = sqrt((double)d);
+    double* e = malloc(sizeof(double) * (size_t)(C + n));
+    if (!e) return -2;
+    for (int j = 0; j < T; ++j) score[j] = 0.0;
+    for (int p = 0; p < n_win; ++p) {
+        const double* qp = Qwin + (size_t)p * d;
+        const int step = first_step + p;
+        int nv = 0;  /* visible visual tokens: positions <= step (ret is sorted) */
+        while (nv < n && ret[nv] <= step) ++nv;
+        double m = -INFINITY;
+        for (int j = 0; j < C + nv; ++j) {
+            const double* kr = j < C ? Kc + (size_t)j * d : Kvis + (size_t)ret[j - C] * d;
+            e[j] = dot(qp, kr, d) / sd;
+            if (e[j] > m) m = e[j];
+        }
+        double Z = 0.0;
+        for (int j = 0; j < C + nv; ++j) {
+            e[j] = exp(e[j] - m);
+            Z += e[j];
+        }
+        for (int j = 0; j < T && j < nv; ++j) score[j] += e[C + j] / Z;
+    }
+    free(e);
+    return 0;
+}
+
 int orc_update(int32_t* ret, int32_t* n_ret, const double* Kvis, int d,
                const double* qsum, int budget, int is_local, int recent_len,
                int rs_num, int rs_den, int u, int32_t* n_evicted, double* min_gap) {
+    return orc_update_ex(ret, n_ret, Kvis, d, qsum, budget, is_local, recent_len, rs_num,
+                         rs_den, u, ORC_SCORE_MEAN_LOGIT, NULL, 0, 0, NULL, 0, n_evicted,
+                         min_gap);
+}
+
+int orc_update_ex(int32_t* ret, int32_t* n_ret, const double* Kvis, int d,
+                  const double* qsum, int budget, int is_local, int recent_len,
+                  int rs_num, int rs_den, int u, int score_mode, const double* Qwin,
+                  int n_win, int first_step, const double* Kc, int C, int32_t* n_evicted,
+                  double* min_gap) {
     if (!ret || !n_ret || !Kvis || d < 1 || budget < 1 || recent_len < 1) return -1;
-    if (!is_local && (!qsum || rs_den < 1 || rs_num < 0 || rs_num > rs_den)) return -1;
+    if (score_mode != ORC_SCORE_MEAN_LOGIT && score_mode != ORC_SCORE_ATTN_SUM) return -1;
+    if (!is_local && (rs_den < 1 || rs_num < 0 || rs_num > rs_den)) return -1;
+    if (!is_local && score_mode == ORC_SCORE_MEAN_LOGIT && !qsum) return -1;
+    if (!is_local && score_mode == ORC_SCORE_ATTN_SUM &&
+        (!Qwin || n_win < 1 || first_step < 0 || C < 0 || (C > 0 && !Kc)))
+        return -1;
     const int n = *n_ret;
     const int w_eff = recent_len < budget ? recent_len : budget;
     double gap = INFINITY;
@@ -182,13 +231,23 @@ int orc_update(int32_t* ret, int32_t* n_ret, const double* Kvis, int d,
             if (m_near > n_near) { m_long += m_near - n_near; m_near = n_near; }
             /* Eq. (6): score = mean over the past-P queries of the raw logit;
              * 1/(P sqrt(d)) is a positive constant, so the order is that of
-             * qsum . k */
+             * qsum . k.  The variant sums those queries' attention weights. */
             cand_t* c = malloc(sizeof(cand_t) * (size_t)T);
-            if (!c) { free(gone); return -2; }
+            double* ws = score_mode == ORC_SCORE_ATTN_SUM ? malloc(sizeof(double) * (size_t)T) : NULL;
+            if (!c || (score_mode == ORC_SCORE_ATTN_SUM && !ws)) {
+                free(c); free(ws); free(gone);
+                return -2;
+            }
+            if (ws && window_attention_scores(ret, n, T, Kvis, d, Qwin, n_win, first_step, Kc, C,
+                                              ws)) {
+                free(c); free(ws); free(gone);
+                return -2;
+            }
             for (int j = 0; j < T; ++j) {
                 c[j].pos = ret[j];
-                c[j].s = dot(qsum, Kvis + (size_t)ret[j] * d, d);
+                c[j].s = ws ? ws[j] : dot(qsum, Kvis + (size_t)ret[j] * d, d);
             }
+            free(ws);
             const int lo[2] = {0, n_long}, cnt[2] = {n_long, n_near}, mm[2] = {m_long, m_near};
             for (int part = 0; part < 2; ++part) {
                 if (mm[part] == 0) continue;
@@ -223,7 +282,7 @@ int orc_run_head(const double* q, const double* k, const double* v,
                  const double* kc, const double* vc, int C, int N, int d,
                  int t_g, int P, int is_local, int budget, int recent_len,
                  int rs_num, int rs_den, double* out, const int32_t* snap_steps,
-                 int n_snap, uint8_t* snap_mask, double* stats) {
+                 int n_snap, uint8_t* snap_mask, double* stats, int score_mode) {
     if (!q || !k || !v || C < 0 || (C > 0 && (!kc || !vc)) || N < 1 || d < 1 ||
         t_g < 0 || P < 1 || budget < 1 || recent_len < 1 || n_snap < 0 ||
         (n_snap > 0 && (!snap_steps || !snap_mask)))
@@ -251,8 +310,9 @@ int orc_run_head(const double* q, const double* k, const double* v,
                 for (int i = 0; i < d; ++i) qsum[i] += q[(size_t)p * d + i];
             int32_t ev = 0;
             double g = INFINITY;
-            int rc = orc_update(ret, &n_ret, k, d, qsum, budget, is_local, recent_len,
-                                rs_num, rs_den, u, &ev, &g);
+            int rc = orc_update_ex(ret, &n_ret, k, d, qsum, budget, is_local, recent_len,
+                                   rs_num, rs_den, u, score_mode, q + (size_t)p0 * d, t - p0 + 1,
+                                   p0, kc, C, &ev, &g);
             if (rc) { free(ret); free(kr); free(vr); free(s); free(qsum); return rc; }
             ++updates;
             evicted_total += ev;

@@ -23,7 +23,8 @@
  *                      the history is split at floor(T*r_s) into long-range
  *                      (older) and near-range parts, each token is scored by
  *                      the mean raw logit of the past-P queries, and M/2 lowest
- *                      scores are evicted from each part.
+ *                      scores are evicted from each part.  A variant scores a
+ *                      token by the attention weights those queries gave it.
  *   orc_run_head       One head through a whole generation: append every step,
  *                      update every P steps from the grouping step on (Sec. 4,
  *                      Efficient Cache Update), attend over prefix + retained.
@@ -65,6 +66,13 @@ int orc_budgets(int mode, int H, const int32_t* labels, const int32_t* override_
                 int N, int row_len, int recent_len, int rho_num, int rho_den,
                 int32_t* out);
 
+/* Scores of the global-head update (Eq. 6 and a variant). */
+#define ORC_SCORE_MEAN_LOGIT 0 /* Eq. (6): mean raw logit of the past-P queries */
+#define ORC_SCORE_ATTN_SUM 1   /* variant: each past-P query's attention weight
+                                  on the token, over the cache that query
+                                  attended (prefix + retained tokens up to its
+                                  step), summed over the queries in step order */
+
 /* One periodic update of one head.  ret: [*n_ret] retained visual positions in
  * ascending order, rewritten in place; Kvis: [N][d] visual keys by position;
  * qsum: [d] sum of the past-P queries, added in step order starting from 0.
@@ -76,6 +84,15 @@ int orc_update(int32_t* ret, int32_t* n_ret, const double* Kvis, int d,
                const double* qsum, int budget, int is_local, int recent_len,
                int rs_num, int rs_den, int u, int32_t* n_evicted, double* min_gap);
 
+/* The same with a score mode.  For ORC_SCORE_ATTN_SUM: Qwin [n_win][d] are the
+ * queries of steps first_step .. first_step + n_win - 1 (the last of them the
+ * current step) and Kc [C][d] the conditional keys; qsum is not used. */
+int orc_update_ex(int32_t* ret, int32_t* n_ret, const double* Kvis, int d,
+                  const double* qsum, int budget, int is_local, int recent_len,
+                  int rs_num, int rs_den, int u, int score_mode, const double* Qwin,
+                  int n_win, int first_step, const double* Kc, int C, int32_t* n_evicted,
+                  double* min_gap);
+
 /* A whole generation of one head.
  *   q, k, v: [N][d] visual tokens by step; kc, vc: [C][d] conditional tokens.
  *   t_g: grouping step (updates at t_g, t_g+P, ...); is_local, budget: the
@@ -83,12 +100,13 @@ int orc_update(int32_t* ret, int32_t* n_ret, const double* Kvis, int d,
  *   out: [N][d] attention output of every step, or NULL.
  *   snap_steps: [n_snap] steps after whose attention the retained set is
  *   recorded into snap_mask [n_snap][N] (1 = retained), or NULL.
- *   stats: [4] = {updates, tokens evicted, min score gap, unused}. */
+ *   stats: [4] = {updates, tokens evicted, min score gap, unused}.
+ *   score_mode: ORC_SCORE_* of the global-head updates. */
 int orc_run_head(const double* q, const double* k, const double* v,
                  const double* kc, const double* vc, int C, int N, int d,
                  int t_g, int P, int is_local, int budget, int recent_len,
                  int rs_num, int rs_den, double* out, const int32_t* snap_steps,
-                 int n_snap, uint8_t* snap_mask, double* stats);
+                 int n_snap, uint8_t* snap_mask, double* stats, int score_mode);
 
 #ifdef __cplusplus
 }

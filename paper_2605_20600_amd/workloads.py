@@ -48,6 +48,7 @@ class Workload:
     r_s: Tuple[int, int] = (1, 2)
     tau: float = 0.9
     cfg_pairs: bool = False    # rows 2i / 2i+1: cond / uncond of one guidance pair
+    score_mode: int = 0        # 0: Eq. 6 mean logit; 1: summed window attention weights
 
     @property
     def row_len(self) -> int:          # R, including the row-end token

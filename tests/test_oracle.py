@@ -404,3 +404,59 @@ def test_prefill_attention_pins():
     kc2[4] = 50.0 * qc[6] / qc[6].norm()
     o = oracle.prefill_attention(qc, kc2, vc)
     assert np.allclose(o[6], vc[4].numpy(), atol=1e-6)
+
+
+def test_attention_sum_scores_are_window_attention_weights():
+    # the variant score of a history token is the sum, over the window's
+    # queries, of the weight each gave it at its own step: computed here with
+    # the attention function and one-hot values, then the lowest per part must
+    # be the ones the update evicts
+    rng = np.random.default_rng(11)
+    d, C, N = 8, 3, 14
+    Kvis = rng.standard_normal((N, d))
+    Kc = rng.standard_normal((C, d))
+    Q = rng.standard_normal((N, d))
+    ret = [0, 2, 3, 5, 6, 7, 8, 9, 10, 11, 12, 13]
+    t, P, w = 13, 4, 3
+    first = t - P + 1
+    T = len(ret) - w
+    exp_score = np.zeros(T)
+    for p in range(first, t + 1):
+        vis = [x for x in ret if x <= p]
+        K = np.concatenate([Kc, Kvis[vis]])
+        for j in range(T):
+            if ret[j] <= p:
+                V = np.zeros((K.shape[0], d))
+                V[C + j, 0] = 1.0        # one-hot value: the output is j's weight
+                exp_score[j] += oracle.attention(Q[p], K, V)[0]
+    for budget in (w + T - 1, w + T - 3, w + 2):
+        M = T - (budget - w)
+        n_long = T // 2
+        for u in (0, 1):
+            m_long = (M + (u & 1)) >> 1
+            m_near = M - m_long
+            m_long, m_near = min(m_long, n_long), m_near + max(0, m_long - n_long)
+            want = set()
+            for lo, hi, m in ((0, n_long, m_long), (n_long, T, m_near)):
+                order = sorted(range(lo, hi), key=lambda j: (exp_score[j], ret[j]))
+                want |= {ret[j] for j in order[:m]}
+            new, _ = oracle.update(ret, Kvis, None, budget, False, w, (1, 2), u,
+                                   oracle.SCORE_ATTN_SUM, Q[first:t + 1], first, Kc)
+            assert set(ret) - set(new.tolist()) == want, (budget, u)
+
+
+def test_attention_sum_with_one_query_ranks_like_eq6():
+    # with a window of one query the weights are a softmax of that query's
+    # logits over one cache: the same order as Eq. (6)'s raw logits
+    rng = np.random.default_rng(12)
+    d, C, N = 16, 4, 40
+    Kvis = rng.standard_normal((N, d))
+    Kc = rng.standard_normal((C, d))
+    Q = rng.standard_normal((N, d))
+    ret = list(range(0, N, 1))
+    t, w = N - 1, 5
+    for budget in (30, 20, 9):
+        a, _ = oracle.update(ret, Kvis, Q[t], budget, False, w, (1, 2), 1)
+        b, _ = oracle.update(ret, Kvis, None, budget, False, w, (1, 2), 1,
+                             oracle.SCORE_ATTN_SUM, Q[t:t + 1], t, Kc)
+        assert np.array_equal(a, b), budget
