@@ -42,6 +42,9 @@ def parse():
                    help="attention over heads of unequal length: per-head lengths (default), "
                         "every head padded to the layer's longest with a mask, or one launch "
                         "per head group")
+    p.add_argument("--score-mode", default="mean_logit", choices=["mean_logit", "attn_sum"],
+                   help="eviction score of global heads: Eq. 6's mean raw logit (default) or the "
+                        "summed attention weights of the past-P queries")
     p.add_argument("--method", default="headkv", choices=["headkv", "uniform", "full"],
                    help="headkv (default); uniform: every head labelled global, budget rho*N "
                         "for all (the line-based baseline's uniform allocation); full: every "
@@ -314,6 +317,8 @@ def main():
         wl = wl.with_(rho=tuple(int(x) for x in args.rho.split("/")))
     if args.method == "full":
         wl = wl.with_(budget_mode=W.BUDGET_OVERRIDE)
+    if args.score_mode == "attn_sum":
+        wl = wl.with_(score_mode=B.HEADKV_SCORE_ATTN_SUM)
     rho_s = f"{wl.rho[0]}/{wl.rho[1]}"
     dev = torch.cuda.current_device()
     torch.cuda.set_device(dev)
@@ -415,6 +420,7 @@ def main():
             "visual_tokens": wl.num_visual, "rho": rho_s,
             "budget_mode": ["paper", "override", "layer_total"][wl.budget_mode],
             "method": args.method, "attn_strategy": args.attn_strategy,
+            "score_mode": args.score_mode,
             "period": wl.period,
             "group_threshold": wl.group_threshold, "recent_window": wl.recent_len,
             "kv_storage": "bf16", "accumulate": "fp32 (attention), fp64 (grouping, eviction)",

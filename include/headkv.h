@@ -76,6 +76,15 @@ typedef int32_t headkv_status;
                                  heads, then local heads), written into one
                                  output */
 
+/* Eviction scores of global heads. */
+#define HEADKV_SCORE_MEAN_LOGIT 0 /* Eq. (6): mean raw logit of the past-P queries */
+#define HEADKV_SCORE_ATTN_SUM 1   /* variant (multi-query attention aggregation):
+                                     each past-P query's attention weight on the
+                                     token over the cache it attended (prefix +
+                                     retained tokens up to its step), summed
+                                     over the queries; keeps the last P queries
+                                     of every head in the metadata buffer */
+
 /* Limits of this build. */
 #define HEADKV_MAX_VISUAL 16384  /* num_visual */
 #define HEADKV_MAX_PREFIX 2048   /* prefix_len */
@@ -98,6 +107,8 @@ typedef struct headkv_config {
     int32_t rho_num, rho_den;/* rho = rho_num / rho_den in (0, 1] */
     int32_t rs_num, rs_den;  /* r_s = rs_num / rs_den in [0, 1] (Eq. 5) */
     int32_t attn_strategy;   /* HEADKV_ATTN_*; HEADKV_ATTN_VARLEN by default */
+    int32_t score_mode;      /* HEADKV_SCORE_*: how global heads score the
+                                history for eviction */
     int32_t cfg_pairs;       /* 1: batch rows 2i and 2i+1 are the conditional and
                                 unconditional sequences of one classifier-free-
                                 guidance pair, and both take the head labels of

@@ -23,6 +23,9 @@ HEADKV_BUDGET_PAPER = 0
 HEADKV_BUDGET_OVERRIDE = 1
 HEADKV_BUDGET_TOTAL = 2
 
+HEADKV_SCORE_MEAN_LOGIT = 0
+HEADKV_SCORE_ATTN_SUM = 1
+
 HEADKV_ATTN_VARLEN = 0
 HEADKV_ATTN_PADDED = 1
 HEADKV_ATTN_GROUPED = 2
@@ -49,7 +52,8 @@ class HeadKVConfig(ctypes.Structure):
         ("group_threshold", ctypes.c_int32), ("budget_mode", ctypes.c_int32),
         ("rho_num", ctypes.c_int32), ("rho_den", ctypes.c_int32),
         ("rs_num", ctypes.c_int32), ("rs_den", ctypes.c_int32),
-        ("attn_strategy", ctypes.c_int32), ("cfg_pairs", ctypes.c_int32),
+        ("attn_strategy", ctypes.c_int32), ("score_mode", ctypes.c_int32),
+        ("cfg_pairs", ctypes.c_int32),
         ("tau", ctypes.c_double),
     ]
 

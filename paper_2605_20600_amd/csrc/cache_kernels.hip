@@ -150,14 +150,18 @@ struct UpdateLds {
     static __host__ __device__ int words(int N) { return (N + 31) >> 5; }
     static __host__ __device__ size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
     // bitmap | word prefix | order (u16) | evict (u8) | positions (i32) |
-    // scores (f64, also two int lists) | query sum (f64 [d])
+    // scores (f64, also two int lists) | query sum (f64 [d]) | with
+    // attention-sum scores: weights of the cache (f64 [C + cap])
     static __host__ __device__ size_t off_wpre(int N) { return a16(4 * (size_t)words(N)); }
     static __host__ __device__ size_t off_order(int N) { return off_wpre(N) + a16(4 * (size_t)words(N)); }
     static __host__ __device__ size_t off_evict(int N, int cap) { return off_order(N) + a16(2 * (size_t)cap); }
     static __host__ __device__ size_t off_pos(int N, int cap) { return off_evict(N, cap) + a16((size_t)cap); }
     static __host__ __device__ size_t off_sig(int N, int cap) { return off_pos(N, cap) + a16(4 * (size_t)cap); }
     static __host__ __device__ size_t off_qs(int N, int cap) { return off_sig(N, cap) + a16(8 * (size_t)cap); }
-    static __host__ __device__ size_t bytes(int N, int cap, int d) { return off_qs(N, cap) + a16(8 * (size_t)d); }
+    static __host__ __device__ size_t off_w(int N, int cap, int d) { return off_qs(N, cap) + a16(8 * (size_t)d); }
+    static __host__ __device__ size_t bytes(int N, int cap, int d, int C, bool attn) {
+        return off_w(N, cap, d) + (attn ? a16(8 * ((size_t)C + cap)) : 0);
+    }
 };
 
 // fp64 score -> unsigned key with the same order (-0 and +0 map to one key,
@@ -228,6 +232,85 @@ __device__ void select_lowest(const double* sig, const uint16_t* order, uint8_t*
     }
 }
 
+// q . k of a cached row in fp64, the dims summed in order, without FMA.
+template <int D>
+__device__ __forceinline__ double dot_row(const double* qd, const uint16_t* row) {
+#pragma clang fp contract(off)
+    const uint4* kr = reinterpret_cast<const uint4*>(row);
+    uint4 v[D / 8];
+#pragma unroll
+    for (int c = 0; c < D / 8; ++c) v[c] = kr[c];
+    double acc = 0.0;
+#pragma unroll
+    for (int c = 0; c < D / 8; ++c) {
+        const uint32_t wv[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            acc = acc + qd[8 * c + 2 * e] * (double)bf_lo(wv[e]);
+            acc = acc + qd[8 * c + 2 * e + 1] * (double)bf_hi(wv[e]);
+        }
+    }
+    return acc;
+}
+
+// The attention-sum variant of the eviction score (the oracle's
+// ORC_SCORE_ATTN_SUM): for each window query p (steps max(0, step-P+1) ..
+// step, from the query ring), its softmax over the cache it attended -- the
+// prefix rows, then the retained tokens with position <= p in position order
+// -- with logits q.k / sqrt(d) in fp64, exp(l - max) summed in that order by
+// one thread; sig[r] for the history ranks [r_lo, r_hi) accumulates the
+// weights query by query.  w: LDS scratch of C + cap fp64.
+template <int D>
+__device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C, int h, int n,
+                                     int r_lo, int r_hi, int step,
+                                     const uint16_t* order, const int32_t* pos, double* qd,
+                                     double* sig, double* w, double sqrt_d, int tid) {
+#pragma clang fp contract(off)
+    __shared__ double red[kBlock / 64];
+    __shared__ double zsh;
+    __shared__ int nv_sh;
+    const int P = L.ring_len;
+    const int p0 = step - P + 1 > 0 ? step - P + 1 : 0;
+    for (int r = r_lo + tid; r < r_hi; r += kBlock) sig[r] = 0.0;
+    for (int p = p0; p <= step; ++p) {
+        const uint16_t* qp = L.qring + ((size_t)h * P + p % P) * D;
+        for (int i = tid; i < D; i += kBlock) qd[i] = bf_f64(qp[i]);
+        if (tid == 0) {  // visible visual tokens: ranks with position <= p
+            int lo = 0, hi = n;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (pos[order[mid]] <= p) lo = mid + 1; else hi = mid;
+            }
+            nv_sh = lo;
+        }
+        __syncthreads();
+        const int nv = nv_sh;
+        double m = -INFINITY;
+        for (int j = tid; j < C + nv; j += kBlock) {
+            const uint16_t* row = j < C ? S.K + (size_t)j * D : S.K + (size_t)(C + order[j - C]) * D;
+            w[j] = dot_row<D>(qd, row) / sqrt_d;
+            m = fmax(m, w[j]);
+        }
+        for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+        if ((tid & 63) == 0) red[tid >> 6] = m;
+        __syncthreads();
+        m = red[0];
+        for (int i = 1; i < kBlock / 64; ++i) m = fmax(m, red[i]);
+        for (int j = tid; j < C + nv; j += kBlock) w[j] = exp(w[j] - m);
+        __syncthreads();
+        if (tid == 0) {  // normaliser, summed over the cache in order
+            double z = 0.0;
+            for (int j = 0; j < C + nv; ++j) z += w[j];
+            zsh = z;
+        }
+        __syncthreads();
+        const double z = zsh;
+        for (int r = r_lo + tid; r < r_hi; r += kBlock)
+            if (r < nv) sig[r] = sig[r] + w[C + r] / z;
+        __syncthreads();  // w, qd, red and zsh are rewritten for the next query
+    }
+}
+
 // One block per head: optional append, then the periodic update of Eqs. 2-6
 // (or, with `relayout`, the first update fused with the move into the head's
 // new segment).
@@ -236,7 +319,7 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
                                                    const char* src_kv, int relayout,
                                                    int64_t dense_seg_bytes, int dense_cap,
                                                    int recent_len, int rs_num, int rs_den, int u,
-                                                   int lds_cap) {
+                                                   int step, int lds_cap, double sqrt_d) {
 #pragma clang fp contract(off)
     constexpr int kRow16 = D / 8;  // 16-byte chunks per row
     extern __shared__ __align__(16) unsigned char lds[];
@@ -321,6 +404,12 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
             const bool sel_near = m_near > 0 && m_near < n_near;
             const int r_lo = sel_long ? 0 : n_long;
             const int r_hi = sel_near ? T : n_long;
+            if (L.qring) {
+                attention_sum_scores<D>(L, S, C, h, n, r_lo, r_hi, step, order, pos, qs, sig,
+                                        reinterpret_cast<double*>(
+                                            lds + UpdateLds::off_w(N, lds_cap, D)),
+                                        sqrt_d, tid);
+            } else {
             // Eq. (6): mean raw logit of the past-P queries; the positive factor
             // 1/(P sqrt(d)) is dropped, the order is that of (sum q) . k, summed
             // over the dims in order in fp64.  Each thread reads its row's 16-byte
@@ -343,6 +432,7 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
                     }
                 }
                 sig[r] = acc;
+            }
             }
             __syncthreads();
             // per part, evict the m lowest by (score, position)
@@ -465,11 +555,11 @@ int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
 
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
                   int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
-                  int rs_num, int rs_den, int u, int lds_cap, void* stream, void* ev_start,
-                  void* ev_stop) {
+                  int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
+                  void* stream, void* ev_start, void* ev_stop) {
     hipStream_t st = (hipStream_t)stream;
     hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
-    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d);
+    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, L.qring != nullptr);
     // allow the update block more than 64 KB of dynamic LDS (gfx950: 160 KB)
     static const bool lds_ok = [] {
         const int max_lds = 160 * 1024;
@@ -484,15 +574,17 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
     if (s.d == 128)
         hipExtLaunchKernelGGL(k_update<128>, dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, s.C,
                               s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
-                              rs_num, rs_den, u, lds_cap);
+                              rs_num, rs_den, u, step, lds_cap, sqrt_d);
     else
         hipExtLaunchKernelGGL(k_update<64>, dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, s.C,
                               s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
-                              rs_num, rs_den, u, lds_cap);
+                              rs_num, rs_den, u, step, lds_cap, sqrt_d);
     return last_error();
 }
 
-size_t update_lds_bytes(int N, int cap, int d) { return UpdateLds::bytes(N, cap, d); }
+size_t update_lds_bytes(int N, int cap, int d, int C, bool attn_scores) {
+    return UpdateLds::bytes(N, cap, d, C, attn_scores);
+}
 
 int launch_export(const LayerDev& L, const Shape& s, uint8_t* mask, int32_t* count,
                   void* stream) {

@@ -104,6 +104,12 @@ headkv_status validate_config(const headkv_config* c) {
     if (c->attn_strategy < HEADKV_ATTN_VARLEN || c->attn_strategy > HEADKV_ATTN_GROUPED)
         return fail(HEADKV_ERR_INVALID_ARG, "unknown attn_strategy");
     if (c->cfg_pairs != 0 && c->cfg_pairs != 1) return fail(HEADKV_ERR_INVALID_ARG, "cfg_pairs must be 0 or 1");
+    if (c->score_mode != HEADKV_SCORE_MEAN_LOGIT && c->score_mode != HEADKV_SCORE_ATTN_SUM)
+        return fail(HEADKV_ERR_INVALID_ARG, "unknown score_mode");
+    if (c->score_mode == HEADKV_SCORE_ATTN_SUM &&
+        update_lds_bytes(c->num_visual, std::min(c->num_visual, HEADKV_MAX_CAPACITY), c->head_dim,
+                         c->prefix_len, true) > 160 * 1024)
+        return fail(HEADKV_ERR_UNSUPPORTED, "attention-sum scores: prefix + capacity too large for LDS");
     if (c->cfg_pairs && c->batch % 2 != 0)
         return fail(HEADKV_ERR_INVALID_ARG, "cfg_pairs needs an even batch");
     // chunk indices must fit the 8 bits of a chunk table entry (always true
@@ -138,7 +144,8 @@ Plan make_plan(const headkv_config& c) {
     // the largest capacity any head can have, dense or after grouping
     const int max_cap = std::max(p.dense_cap, std::min(c.num_visual, HEADKV_MAX_CAPACITY));
     const int per_head = chunks_of(c.prefix_len, max_cap, kAttnMinThreads, c.head_dim);
-    p.ml.compute(p.BH, c.head_dim, p.BH * per_head);
+    p.ml.compute(p.BH, c.head_dim, p.BH * per_head,
+                 c.score_mode == HEADKV_SCORE_ATTN_SUM ? c.period : 0);
     // partial (max, sum, weighted V) of every chunk table entry
     p.ws_bytes = align_up((size_t)p.BH * per_head * (c.head_dim + 2) * sizeof(float), 256);
     return p;
@@ -172,6 +179,8 @@ headkv_status hip_status(int e, const char* what) {
     if (e != 0) return fail(HEADKV_ERR_HIP, std::string(what) + ": " + hipGetErrorString((hipError_t)e));
     return ok();
 }
+
+double sqrt_d(headkv_t h) { return std::sqrt((double)h->cfg.head_dim); }
 
 LayerDev dev_of(headkv_t h, const Layer& L) {
     return make_layer_dev(L.grouped ? L.ragged : L.dense, L.meta, h->ml);
@@ -435,7 +444,8 @@ headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step, c
     LayerDev D = dev_of(h, L);
     if (update)
         st = hip_status(launch_update(D, h->shape, a, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
-                                      c.rs_den, u, max_cap(L), stream, nullptr, nullptr),
+                                      c.rs_den, u, step, max_cap(L), sqrt_d(h), stream, nullptr,
+                                      nullptr),
                         "append + update launch");
     else
         st = hip_status(launch_append(D, h->shape, a, stream), "append launch");
@@ -513,7 +523,7 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
     if (update) {
         take_events(h, time_it, HEADKV_TIMED_UPDATE, update_bytes(h, L), &e0, &e1);
         st = hip_status(launch_update(D, h->shape, a, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
-                                      c.rs_den, u, max_cap(L), stream, e0, e1),
+                                      c.rs_den, u, step, max_cap(L), sqrt_d(h), stream, e0, e1),
                         "append + update launch");
         if (st) return st;
         commit_append(h, L, step, update);
@@ -717,7 +727,7 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
         AppendArgs none{};
         st = hip_status(launch_update(Dnew, h->shape, none, static_cast<const char*>(L.dense), 1,
                                       h->dense_seg, h->dense_cap, c.recent_len, c.rs_num, c.rs_den,
-                                      0, h->dense_cap, stream, nullptr, nullptr),
+                                      0, h->t_g, h->dense_cap, sqrt_d(h), stream, nullptr, nullptr),
                         "relayout launch");
     }
     headkv_status st_wait = hip_status(hipStreamSynchronize(s), "stream wait");

@@ -39,13 +39,15 @@ inline size_t segment_bytes(int C, int cap, int d) {
 }
 
 struct MetaLayout {
-    size_t seg_off, cap, n, budget, nstar, label, order, qsum, items, item_start, total;
-    int max_items;
+    size_t seg_off, cap, n, budget, nstar, label, order, qsum, items, item_start, qring, total;
+    int max_items, ring_len;
 
     // max_items: largest chunk table of a layer (every head at its largest
-    // capacity, in chunks of the smallest attention pass).
-    void compute(int BH, int d, int max_items_) {
+    // capacity, in chunks of the smallest attention pass); ring_len: queries
+    // kept per head for the attention-sum eviction scores (0: none).
+    void compute(int BH, int d, int max_items_, int ring_len_) {
         max_items = max_items_;
+        ring_len = ring_len_;
         size_t o = 0;
         auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
         seg_off = take(sizeof(int64_t) * BH);
@@ -58,6 +60,7 @@ struct MetaLayout {
         qsum = take(sizeof(double) * (size_t)BH * d);
         items = take(sizeof(uint32_t) * (size_t)max_items);
         item_start = take(sizeof(int32_t) * ((size_t)BH + 1));
+        qring = take(sizeof(uint16_t) * (size_t)BH * ring_len * d);
         total = o;
     }
 };
@@ -77,6 +80,10 @@ struct LayerDev {
     // head h owns entries item_start[h] .. item_start[h+1]-1
     uint32_t* items;
     int32_t* item_start;  // [BH + 1]
+    // attention-sum scores only: the queries of the last ring_len steps,
+    // [BH][ring_len][d] bf16, step t in slot t % ring_len (else nullptr)
+    uint16_t* qring;
+    int ring_len;
 };
 
 #if defined(__HIPCC__)
@@ -96,6 +103,8 @@ inline LayerDev make_layer_dev(void* kv, void* meta, const MetaLayout& m) {
     L.qsum = reinterpret_cast<double*>(b + m.qsum);
     L.items = reinterpret_cast<uint32_t*>(b + m.items);
     L.item_start = reinterpret_cast<int32_t*>(b + m.item_start);
+    L.qring = m.ring_len > 0 ? reinterpret_cast<uint16_t*>(b + m.qring) : nullptr;
+    L.ring_len = m.ring_len;
     return L;
 }
 
@@ -132,14 +141,15 @@ int launch_score(const LayerDev& L, const Shape& s, const uint16_t* q, int32_t* 
 int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
                    const int32_t* override_b, int32_t* budgets, int mode, int row_len,
                    int recent_len, int rho_num, int rho_den, int cfg_pairs, void* stream);
-// a.k == nullptr: no append.
+// a.k == nullptr: no append.  step: the visual step of the update.
 // lds_cap: largest visual capacity among the launch's source segments.
+// With L.qring, global heads are scored by the window's attention weights.
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
                   int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
-                  int rs_num, int rs_den, int u, int lds_cap, void* stream, void* ev_start,
-                  void* ev_stop);
-// Dynamic LDS of one update block.
-size_t update_lds_bytes(int N, int cap, int d);
+                  int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
+                  void* stream, void* ev_start, void* ev_stop);
+// Dynamic LDS of one update block (C: prefix rows, with attention-sum scores).
+size_t update_lds_bytes(int N, int cap, int d, int C, bool attn_scores);
 // How one attention launch covers a layer (or a group of its heads).
 struct AttnPlan {
     int threads;     // 1024, 512 or 256

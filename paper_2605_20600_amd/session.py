@@ -26,7 +26,7 @@ def make_config(wl: Workload, rho=None, budget_mode=None, r_s=None, tau=None,
         group_threshold=wl.group_threshold,
         budget_mode=wl.budget_mode if budget_mode is None else budget_mode,
         rho_num=rho[0], rho_den=rho[1], rs_num=r_s[0], rs_den=r_s[1],
-        attn_strategy=attn_strategy, cfg_pairs=1 if wl.cfg_pairs else 0,
+        attn_strategy=attn_strategy, score_mode=wl.score_mode, cfg_pairs=1 if wl.cfg_pairs else 0,
         tau=wl.tau if tau is None else tau)
 
 

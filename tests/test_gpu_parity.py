@@ -356,3 +356,26 @@ def test_decode_attn_layers_matches_per_layer():
     got = together[1][4].cpu().double().numpy()
     for h in range(wl.heads):
         assert np.abs(got[h] - ref["out"][h][t]).max() <= ATOL
+
+
+# ---- attention-sum eviction scores (variant of Eq. 6) ----
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_tiny_attention_sum_scores_every_step(fused):
+    wl = W.TINY.with_(score_mode=B.HEADKV_SCORE_ATTN_SUM)
+    steps = list(range(wl.num_visual))
+    inp = DeviceInputs(wl)
+    sess = new_session(wl)
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps, fused=fused)
+    torch.cuda.synchronize()
+    _check_slice(wl, res, 0, 0, steps)
+
+
+@pytest.mark.parametrize("wl", [W.LUMINA768.with_(score_mode=1),
+                                W.STRESS.with_(score_mode=1, batch=4),
+                                W.LUMINA1024.with_(score_mode=1)],
+                         ids=["lumina768", "stress_b4", "lumina1024"])
+def test_attention_sum_scores_sampled(wl):
+    t_g, P = wl.group_threshold - 1, wl.period
+    steps = [t_g, t_g + 1, t_g + P, t_g + 3 * P, t_g + 3 * P + 1]
+    _run_and_check(wl, [1], [(1, 2)], steps, all_heads=False, n_steps=steps[-1] + 1)
