@@ -313,8 +313,10 @@ __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C,
 
 // One block per head: optional append, then the periodic update of Eqs. 2-6
 // (or, with `relayout`, the first update fused with the move into the head's
-// new segment).
-template <int D>
+// new segment).  ATTN_SUM: the attention-sum scores instead of Eq. 6; a
+// separate instantiation, since its fp64 exp needs about twice the registers
+// (the Eq. 6 kernel stays under 64 VGPRs: eight 256-thread blocks per CU).
+template <int D, bool ATTN_SUM>
 __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, AppendArgs a,
                                                    const char* src_kv, int relayout,
                                                    int64_t dense_seg_bytes, int dense_cap,
@@ -404,7 +406,7 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
             const bool sel_near = m_near > 0 && m_near < n_near;
             const int r_lo = sel_long ? 0 : n_long;
             const int r_hi = sel_near ? T : n_long;
-            if (L.qring) {
+            if (ATTN_SUM) {
                 attention_sum_scores<D>(L, S, C, h, n, r_lo, r_hi, step, order, pos, qs, sig,
                                         reinterpret_cast<double*>(
                                             lds + UpdateLds::off_w(N, lds_cap, D)),
@@ -412,23 +414,31 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
             } else {
             // Eq. (6): mean raw logit of the past-P queries; the positive factor
             // 1/(P sqrt(d)) is dropped, the order is that of (sum q) . k, summed
-            // over the dims in order in fp64.  Each thread reads its row's 16-byte
-            // chunks together and then walks them in order.
+            // over the dims in order in fp64.  Each thread reads half of its row's
+            // 16-byte chunks together and then walks them in order.
             for (int i = tid; i < D; i += kBlock) qs[i] = L.qsum[(size_t)h * D + i];
             __syncthreads();
             for (int r = r_lo + tid; r < r_hi; r += kBlock) {
                 const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + order[r]) * D);
-                uint4 v[kRow16];
-#pragma unroll
-                for (int c = 0; c < kRow16; ++c) v[c] = kr[c];
                 double acc = 0.0;
+                // half a row in flight at a time keeps the kernel under 64
+                // VGPRs (eight blocks per CU), which pays more than one
+                // round trip per row
+                constexpr int HR = kRow16 / 2;
 #pragma unroll
-                for (int c = 0; c < kRow16; ++c) {
-                    const uint32_t wv[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+                for (int half = 0; half < 2; ++half) {
+                    uint4 v[HR];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        acc = acc + qs[8 * c + 2 * e] * (double)bf_lo(wv[e]);
-                        acc = acc + qs[8 * c + 2 * e + 1] * (double)bf_hi(wv[e]);
+                    for (int c = 0; c < HR; ++c) v[c] = kr[half * HR + c];
+#pragma unroll
+                    for (int c = 0; c < HR; ++c) {
+                        const uint32_t wv[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+                        const int i0 = 8 * (half * HR + c);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            acc = acc + qs[i0 + 2 * e] * (double)bf_lo(wv[e]);
+                            acc = acc + qs[i0 + 2 * e + 1] * (double)bf_hi(wv[e]);
+                        }
                     }
                 }
                 sig[r] = acc;
@@ -563,22 +573,31 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
     // allow the update block more than 64 KB of dynamic LDS (gfx950: 160 KB)
     static const bool lds_ok = [] {
         const int max_lds = 160 * 1024;
-        bool ok = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_update<128>),
-                                      hipFuncAttributeMaxDynamicSharedMemorySize, max_lds) == hipSuccess;
-        ok = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_update<64>),
-                                 hipFuncAttributeMaxDynamicSharedMemorySize, max_lds) == hipSuccess && ok;
+        const void* fns[4] = {reinterpret_cast<const void*>(&k_update<128, false>),
+                              reinterpret_cast<const void*>(&k_update<128, true>),
+                              reinterpret_cast<const void*>(&k_update<64, false>),
+                              reinterpret_cast<const void*>(&k_update<64, true>)};
+        bool ok = true;
+        for (const void* f : fns)
+            ok = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds) ==
+                     hipSuccess && ok;
         (void)hipGetLastError();
         return ok;
     }();
     (void)lds_ok;
-    if (s.d == 128)
-        hipExtLaunchKernelGGL(k_update<128>, dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, s.C,
-                              s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
-                              rs_num, rs_den, u, step, lds_cap, sqrt_d);
-    else
-        hipExtLaunchKernelGGL(k_update<64>, dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, s.C,
-                              s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,
-                              rs_num, rs_den, u, step, lds_cap, sqrt_d);
+    const bool attn = L.qring != nullptr;
+#define HEADKV_UPDATE(D_, A_)                                                                      \
+    hipExtLaunchKernelGGL((k_update<D_, A_>), dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, s.C, \
+                          s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,         \
+                          rs_num, rs_den, u, step, lds_cap, sqrt_d)
+    if (s.d == 128) {
+        if (attn) HEADKV_UPDATE(128, true);
+        else HEADKV_UPDATE(128, false);
+    } else {
+        if (attn) HEADKV_UPDATE(64, true);
+        else HEADKV_UPDATE(64, false);
+    }
+#undef HEADKV_UPDATE
     return last_error();
 }
 

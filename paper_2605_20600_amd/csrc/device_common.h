@@ -80,9 +80,11 @@ __device__ __forceinline__ SegPtrs seg_ptrs(char* seg, int C, int cap, int d) {
 // row C+n, pos[n] = step, the query sum of the update window.  Split in a
 // load half and a store half so that a caller can put other loads between
 // them; the length n is changed by append_commit once no thread reads it.
+// The load half only issues loads (no loaded value is used before the store
+// half), so that a caller's loads are not held behind their latency.
 struct AppendVals {
     uint16_t k = 0, v = 0, qbits = 0;
-    double qs_old = 0.0, q = 0.0;
+    double qs_old = 0.0;
 };
 
 __device__ __forceinline__ AppendVals append_load(const LayerDev& L, int d, int h,
@@ -91,11 +93,8 @@ __device__ __forceinline__ AppendVals append_load(const LayerDev& L, int d, int 
     if (tid < d) {
         r.k = a.k[(size_t)h * d + tid];
         r.v = a.v[(size_t)h * d + tid];
-        if (a.accumulate || L.qring) {
-            r.qbits = a.q[(size_t)h * d + tid];
-            r.q = bf_f64(r.qbits);
-            if (a.accumulate && !a.reset) r.qs_old = L.qsum[(size_t)h * d + tid];
-        }
+        if (a.accumulate || L.qring) r.qbits = a.q[(size_t)h * d + tid];
+        if (a.accumulate && !a.reset) r.qs_old = L.qsum[(size_t)h * d + tid];
     }
     return r;
 }
@@ -108,7 +107,7 @@ __device__ __forceinline__ void append_store(const LayerDev& L, int C, int d, in
     const size_t row = (size_t)(C + n) * d;
     s.K[row + tid] = r.k;
     s.V[row + tid] = r.v;
-    if (a.accumulate) L.qsum[(size_t)h * d + tid] = r.qs_old + r.q;  // 0 + q on a reset
+    if (a.accumulate) L.qsum[(size_t)h * d + tid] = r.qs_old + bf_f64(r.qbits);  // 0 + q on a reset
     if (L.qring) L.qring[((size_t)h * L.ring_len + a.step % L.ring_len) * d + tid] = r.qbits;
     if (tid == 0) s.pos[n] = a.step;
 }
