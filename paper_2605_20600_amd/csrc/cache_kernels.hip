@@ -150,19 +150,26 @@ struct UpdateLds {
     static __host__ __device__ int words(int N) { return (N + 31) >> 5; }
     static __host__ __device__ size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
     // bitmap | word prefix | order (u16) | evict (u8) | positions (i32) |
-    // scores (f64, also two int lists) | query sum (f64 [d]) | with
-    // attention-sum scores: weights of the cache (f64 [C + cap])
+    // scores (f64, also two int lists) | query sum (f64 [d]), or with
+    // attention-sum scores G queries (f64 [G][d]) | with attention-sum scores:
+    // weights of the cache for each query of a group (f64 [G][C + cap])
     static __host__ __device__ size_t off_wpre(int N) { return a16(4 * (size_t)words(N)); }
     static __host__ __device__ size_t off_order(int N) { return off_wpre(N) + a16(4 * (size_t)words(N)); }
     static __host__ __device__ size_t off_evict(int N, int cap) { return off_order(N) + a16(2 * (size_t)cap); }
     static __host__ __device__ size_t off_pos(int N, int cap) { return off_evict(N, cap) + a16((size_t)cap); }
     static __host__ __device__ size_t off_sig(int N, int cap) { return off_pos(N, cap) + a16(4 * (size_t)cap); }
     static __host__ __device__ size_t off_qs(int N, int cap) { return off_sig(N, cap) + a16(8 * (size_t)cap); }
-    static __host__ __device__ size_t off_w(int N, int cap, int d) { return off_qs(N, cap) + a16(8 * (size_t)d); }
-    static __host__ __device__ size_t bytes(int N, int cap, int d, int C, bool attn) {
-        return off_w(N, cap, d) + (attn ? a16(8 * ((size_t)C + cap)) : 0);
+    static __host__ __device__ size_t off_w(int N, int cap, int d, int g) {
+        return off_qs(N, cap) + a16(8 * (size_t)d * g);
+    }
+    static __host__ __device__ size_t bytes(int N, int cap, int d, int C, bool attn, int g) {
+        return off_w(N, cap, d, attn ? g : 1) + (attn ? a16(8 * (size_t)g * ((size_t)C + cap)) : 0);
     }
 };
+
+// Window queries scored together by the attention-sum variant: up to 8 when
+// the period and the LDS allow, else one at a time.
+constexpr int kQueryGroup = 8;
 
 // fp64 score -> unsigned key with the same order (-0 and +0 map to one key,
 // since they compare equal).
@@ -257,57 +264,125 @@ __device__ __forceinline__ double dot_row(const double* qd, const uint16_t* row)
 // ORC_SCORE_ATTN_SUM): for each window query p (steps max(0, step-P+1) ..
 // step, from the query ring), its softmax over the cache it attended -- the
 // prefix rows, then the retained tokens with position <= p in position order
-// -- with logits q.k / sqrt(d) in fp64, exp(l - max) summed in that order by
-// one thread; sig[r] for the history ranks [r_lo, r_hi) accumulates the
-// weights query by query.  w: LDS scratch of C + cap fp64.
-template <int D>
+// -- with logits q.k / sqrt(d) in fp64 and exp(l - max) summed in that order;
+// sig[r] for the history ranks [r_lo, r_hi) accumulates the weights query by
+// query, in step order.
+// The window is taken G queries at a time: each thread reads a cached row once
+// and runs the G dot products as G independent fp64 chains (dims in order, no
+// FMA); the G normalisers are summed by G threads at once, each over its
+// query's cache in order.  qd: LDS [G][D]; w: LDS [G][wst] with wst >= C + n.
+template <int D, int G>
 __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C, int h, int n,
                                      int r_lo, int r_hi, int step,
                                      const uint16_t* order, const int32_t* pos, double* qd,
-                                     double* sig, double* w, double sqrt_d, int tid) {
+                                     double* sig, double* w, int wst, double sqrt_d, int tid) {
 #pragma clang fp contract(off)
-    __shared__ double red[kBlock / 64];
-    __shared__ double zsh;
-    __shared__ int nv_sh;
+    constexpr int WAVES = kBlock / 64;
+    __shared__ double red[WAVES][G];
+    __shared__ double msh[G], zsh[G];
+    __shared__ int nvs[G];
     const int P = L.ring_len;
     const int p0 = step - P + 1 > 0 ? step - P + 1 : 0;
+    const int lane = tid & 63, wave = tid >> 6;
     for (int r = r_lo + tid; r < r_hi; r += kBlock) sig[r] = 0.0;
-    for (int p = p0; p <= step; ++p) {
-        const uint16_t* qp = L.qring + ((size_t)h * P + p % P) * D;
-        for (int i = tid; i < D; i += kBlock) qd[i] = bf_f64(qp[i]);
-        if (tid == 0) {  // visible visual tokens: ranks with position <= p
+    for (int pa = p0; pa <= step; pa += G) {
+        const int ng = step + 1 - pa < G ? step + 1 - pa : G;  // queries of this group
+        // the group's queries in fp64 (rows past ng are zero and unused)
+        for (int i = tid; i < G * D; i += kBlock) {
+            const int g = i / D, e = i - g * D;
+            qd[i] = g < ng ? bf_f64(L.qring[((size_t)h * P + (pa + g) % P) * D + e]) : 0.0;
+        }
+        if (tid < ng) {  // visible visual tokens of query pa + tid: ranks with position <= p
+            const int p = pa + tid;
             int lo = 0, hi = n;
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
                 if (pos[order[mid]] <= p) lo = mid + 1; else hi = mid;
             }
-            nv_sh = lo;
+            nvs[tid] = lo;
         }
         __syncthreads();
-        const int nv = nv_sh;
-        double m = -INFINITY;
-        for (int j = tid; j < C + nv; j += kBlock) {
-            const uint16_t* row = j < C ? S.K + (size_t)j * D : S.K + (size_t)(C + order[j - C]) * D;
-            w[j] = dot_row<D>(qd, row) / sqrt_d;
-            m = fmax(m, w[j]);
+        int vis[G];  // cache length seen by each query (non-decreasing in g)
+#pragma unroll
+        for (int g = 0; g < G; ++g) vis[g] = C + nvs[g < ng ? g : ng - 1];
+        const int rows = vis[G - 1];
+        // logits of every visible row for all queries of the group, and maxima
+        double m[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) m[g] = -INFINITY;
+        for (int j = tid; j < rows; j += kBlock) {
+            const uint16_t* row =
+                j < C ? S.K + (size_t)j * D : S.K + (size_t)(C + order[j - C]) * D;
+            const uint4* kr = reinterpret_cast<const uint4*>(row);
+            // the queries are read from LDS for every row: an offset of zero
+            // the compiler cannot see through keeps it from hoisting all G x D
+            // of them out of the loop
+            int zo;
+            asm volatile("s_mov_b32 %0, 0" : "=s"(zo));
+            const double* qz = qd + zo;
+            double acc[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g) acc[g] = 0.0;
+            constexpr int HR = D / 16;  // half a row in flight at a time
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                uint4 v[HR];
+#pragma unroll
+                for (int c = 0; c < HR; ++c) v[c] = kr[half * HR + c];
+#pragma unroll
+                for (int c = 0; c < HR; ++c) {
+                    const uint32_t wv[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+                    const int i0 = 8 * (half * HR + c);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const double klo = (double)bf_lo(wv[e]), khi = (double)bf_hi(wv[e]);
+#pragma unroll
+                        for (int g = 0; g < G; ++g) {
+                            acc[g] = acc[g] + qz[g * D + i0 + 2 * e] * klo;
+                            acc[g] = acc[g] + qz[g * D + i0 + 2 * e + 1] * khi;
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const double l = acc[g] / sqrt_d;
+                w[(size_t)g * wst + j] = l;
+                if (j < vis[g]) m[g] = fmax(m[g], l);
+            }
         }
-        for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
-        if ((tid & 63) == 0) red[tid >> 6] = m;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            for (int o = 32; o > 0; o >>= 1) m[g] = fmax(m[g], __shfl_xor(m[g], o));
+            if (lane == 0) red[wave][g] = m[g];
+        }
         __syncthreads();
-        m = red[0];
-        for (int i = 1; i < kBlock / 64; ++i) m = fmax(m, red[i]);
-        for (int j = tid; j < C + nv; j += kBlock) w[j] = exp(w[j] - m);
+        if (tid < G) {
+            double mx = red[0][tid];
+            for (int i = 1; i < WAVES; ++i) mx = fmax(mx, red[i][tid]);
+            msh[tid] = mx;
+        }
         __syncthreads();
-        if (tid == 0) {  // normaliser, summed over the cache in order
+        for (int j = tid; j < rows; j += kBlock)
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+                if (j < vis[g]) w[(size_t)g * wst + j] = exp(w[(size_t)g * wst + j] - msh[g]);
+        __syncthreads();
+        if (tid < ng) {  // normaliser of query pa + tid, summed over its cache in order
+            const double* wg = w + (size_t)tid * wst;
+            const int len = C + nvs[tid];
             double z = 0.0;
-            for (int j = 0; j < C + nv; ++j) z += w[j];
-            zsh = z;
+            for (int j = 0; j < len; ++j) z += wg[j];
+            zsh[tid] = z;
         }
         __syncthreads();
-        const double z = zsh;
-        for (int r = r_lo + tid; r < r_hi; r += kBlock)
-            if (r < nv) sig[r] = sig[r] + w[C + r] / z;
-        __syncthreads();  // w, qd, red and zsh are rewritten for the next query
+        for (int r = r_lo + tid; r < r_hi; r += kBlock) {
+            double a = sig[r];
+            for (int g = 0; g < ng; ++g)
+                if (r < nvs[g]) a = a + w[(size_t)g * wst + C + r] / zsh[g];
+            sig[r] = a;
+        }
+        __syncthreads();  // qd, w, nvs, msh and zsh are rewritten for the next group
     }
 }
 
@@ -316,7 +391,7 @@ __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C,
 // new segment).  ATTN_SUM: the attention-sum scores instead of Eq. 6; a
 // separate instantiation, since its fp64 exp needs about twice the registers
 // (the Eq. 6 kernel stays under 64 VGPRs: eight 256-thread blocks per CU).
-template <int D, bool ATTN_SUM>
+template <int D, bool ATTN_SUM, int G>
 __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, AppendArgs a,
                                                    const char* src_kv, int relayout,
                                                    int64_t dense_seg_bytes, int dense_cap,
@@ -407,10 +482,10 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
             const int r_lo = sel_long ? 0 : n_long;
             const int r_hi = sel_near ? T : n_long;
             if (ATTN_SUM) {
-                attention_sum_scores<D>(L, S, C, h, n, r_lo, r_hi, step, order, pos, qs, sig,
-                                        reinterpret_cast<double*>(
-                                            lds + UpdateLds::off_w(N, lds_cap, D)),
-                                        sqrt_d, tid);
+                attention_sum_scores<D, G>(
+                    L, S, C, h, n, r_lo, r_hi, step, order, pos, qs, sig,
+                    reinterpret_cast<double*>(lds + UpdateLds::off_w(N, lds_cap, D, G)),
+                    C + lds_cap, sqrt_d, tid);
             } else {
             // Eq. (6): mean raw logit of the past-P queries; the positive factor
             // 1/(P sqrt(d)) is dropped, the order is that of (sum q) . k, summed
@@ -563,20 +638,31 @@ int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
     return last_error();
 }
 
+// Queries per group of the attention-sum scores: kQueryGroup when the period
+// has that many and their weights fit in the LDS, else 1.
+int update_query_group(int N, int cap, int d, int C, bool attn_scores, int period) {
+    if (!attn_scores || period < kQueryGroup) return 1;
+    return UpdateLds::bytes(N, cap, d, C, true, kQueryGroup) <= kUpdateLdsBudget ? kQueryGroup : 1;
+}
+
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
                   int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
                   int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
                   void* stream, void* ev_start, void* ev_stop) {
     hipStream_t st = (hipStream_t)stream;
     hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
-    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, L.qring != nullptr);
+    const bool attn = L.qring != nullptr;
+    const int G = update_query_group(s.N, lds_cap, s.d, s.C, attn, L.ring_len);
+    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, attn, G);
     // allow the update block more than 64 KB of dynamic LDS (gfx950: 160 KB)
     static const bool lds_ok = [] {
         const int max_lds = 160 * 1024;
-        const void* fns[4] = {reinterpret_cast<const void*>(&k_update<128, false>),
-                              reinterpret_cast<const void*>(&k_update<128, true>),
-                              reinterpret_cast<const void*>(&k_update<64, false>),
-                              reinterpret_cast<const void*>(&k_update<64, true>)};
+        const void* fns[6] = {reinterpret_cast<const void*>(&k_update<128, false, 1>),
+                              reinterpret_cast<const void*>(&k_update<128, true, 1>),
+                              reinterpret_cast<const void*>(&k_update<128, true, kQueryGroup>),
+                              reinterpret_cast<const void*>(&k_update<64, false, 1>),
+                              reinterpret_cast<const void*>(&k_update<64, true, 1>),
+                              reinterpret_cast<const void*>(&k_update<64, true, kQueryGroup>)};
         bool ok = true;
         for (const void* f : fns)
             ok = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds) ==
@@ -585,24 +671,25 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
         return ok;
     }();
     (void)lds_ok;
-    const bool attn = L.qring != nullptr;
-#define HEADKV_UPDATE(D_, A_)                                                                      \
-    hipExtLaunchKernelGGL((k_update<D_, A_>), dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, s.C, \
-                          s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,         \
+#define HEADKV_UPDATE(D_, A_, G_)                                                                  \
+    hipExtLaunchKernelGGL((k_update<D_, A_, G_>), dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, \
+                          s.C, s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,    \
                           rs_num, rs_den, u, step, lds_cap, sqrt_d)
     if (s.d == 128) {
-        if (attn) HEADKV_UPDATE(128, true);
-        else HEADKV_UPDATE(128, false);
+        if (!attn) HEADKV_UPDATE(128, false, 1);
+        else if (G == kQueryGroup) HEADKV_UPDATE(128, true, kQueryGroup);
+        else HEADKV_UPDATE(128, true, 1);
     } else {
-        if (attn) HEADKV_UPDATE(64, true);
-        else HEADKV_UPDATE(64, false);
+        if (!attn) HEADKV_UPDATE(64, false, 1);
+        else if (G == kQueryGroup) HEADKV_UPDATE(64, true, kQueryGroup);
+        else HEADKV_UPDATE(64, true, 1);
     }
 #undef HEADKV_UPDATE
     return last_error();
 }
 
 size_t update_lds_bytes(int N, int cap, int d, int C, bool attn_scores) {
-    return UpdateLds::bytes(N, cap, d, C, attn_scores);
+    return UpdateLds::bytes(N, cap, d, C, attn_scores, 1);
 }
 
 int launch_export(const LayerDev& L, const Shape& s, uint8_t* mask, int32_t* count,

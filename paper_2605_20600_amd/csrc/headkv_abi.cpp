@@ -108,7 +108,7 @@ headkv_status validate_config(const headkv_config* c) {
         return fail(HEADKV_ERR_INVALID_ARG, "unknown score_mode");
     if (c->score_mode == HEADKV_SCORE_ATTN_SUM &&
         update_lds_bytes(c->num_visual, std::min(c->num_visual, HEADKV_MAX_CAPACITY), c->head_dim,
-                         c->prefix_len, true) > 160 * 1024)
+                         c->prefix_len, true) > kUpdateLdsBudget)
         return fail(HEADKV_ERR_UNSUPPORTED, "attention-sum scores: prefix + capacity too large for LDS");
     if (c->cfg_pairs && c->batch % 2 != 0)
         return fail(HEADKV_ERR_INVALID_ARG, "cfg_pairs needs an even batch");

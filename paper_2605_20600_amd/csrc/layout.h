@@ -150,6 +150,9 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
                   void* stream, void* ev_start, void* ev_stop);
 // Dynamic LDS of one update block (C: prefix rows, with attention-sum scores).
 size_t update_lds_bytes(int N, int cap, int d, int C, bool attn_scores);
+// Dynamic LDS an update block may take: the CU's 160 KB less a margin for the
+// kernel's static LDS (block scans, radix histogram, reductions).
+constexpr size_t kUpdateLdsBudget = 156 * 1024;
 // How one attention launch covers a layer (or a group of its heads).
 struct AttnPlan {
     int threads;     // 1024, 512 or 256
