@@ -26,6 +26,17 @@ HEADKV_BUDGET_TOTAL = 2
 HEADKV_SCORE_MEAN_LOGIT = 0
 HEADKV_SCORE_ATTN_SUM = 1
 
+HEADKV_MAX_VISUAL = 16384
+HEADKV_MAX_PREFIX = 2048
+HEADKV_MAX_CAPACITY = 4608
+
+HEADKV_TIMED_ATTN_APPEND = 0        # fused append + attention, compressed cache
+HEADKV_TIMED_ATTN = 1               # attention after an update
+HEADKV_TIMED_UPDATE = 2             # append + periodic update
+HEADKV_TIMED_PREFILL = 3            # prefix store + causal prefix attention
+HEADKV_TIMED_ATTN_APPEND_DENSE = 4  # fused append + attention before grouping
+HEADKV_TIMED_KINDS = 5
+
 HEADKV_ATTN_VARLEN = 0
 HEADKV_ATTN_PADDED = 1
 HEADKV_ATTN_GROUPED = 2
@@ -210,7 +221,7 @@ def headkv_timing_collect(h: int):
     after an update, append + update, prefill, fused append + attention before
     grouping) a list of (kernel ms, launches, algorithmic bytes), and the
     dropped count."""
-    K = 5
+    K = HEADKV_TIMED_KINDS
     ms = (ctypes.c_double * K)()
     n = (ctypes.c_int64 * K)()
     b = (ctypes.c_double * K)()

@@ -68,6 +68,15 @@ def test_config_struct_matches_header():
     assert [(n, ct[t]) for t, n in fields] == list(B.HeadKVConfig._fields_)
 
 
+def test_constants_match_header():
+    # every integer constant the header defines has the same value in the binding
+    src = open(HEADER).read()
+    found = re.findall(r"#define (HEADKV_[A-Z_0-9]+) \(?(-?\d+)\)?", src)
+    assert len(found) >= 20
+    for name, value in found:
+        assert getattr(B, name, None) == int(value), name
+
+
 def _handle(wl=W.TINY):
     cfg = make_config(wl)
     return B.headkv_create(cfg, [FAKE] * cfg.num_layers, [FAKE + 4096] * cfg.num_layers, FAKE), cfg

@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import oracle
-from paper_2605_20600_amd import workloads as W
+from paper_2605_20600_amd import binding as B, synth, workloads as W
 from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation
 
 pytestmark = pytest.mark.gpu
@@ -94,3 +94,75 @@ def test_few_long_heads_split_d64():
     wl = W.TINY.with_(heads=2, grid_rows=32, grid_cols=32, period=32, group_threshold=600,
                       budget_mode=W.BUDGET_OVERRIDE)
     _run(wl, budgets=[[1000, 900]], steps=[0, 300, 599, 600, 601, 800, 1023])
+
+
+def test_limits_prefix_capacity_and_length():
+    # the documented limits at once: a 2048-token prefix, 16384 visual tokens
+    # and heads holding HEADKV_MAX_CAPACITY = 4608 visual tokens (budget 4480 +
+    # period 128); heads 0-1 are planted local (sliding window), 2-3 global (STE)
+    wl = W.TINY.with_(heads=4, head_dim=128, prefix_len=2048, grid_rows=128, grid_cols=128,
+                      period=128, group_threshold=256, budget_mode=W.BUDGET_OVERRIDE)
+    N, P, t_g = wl.num_visual, wl.period, wl.group_threshold - 1
+    bud = [B.HEADKV_MAX_CAPACITY - P, 256, B.HEADKV_MAX_CAPACITY - P, 256]
+    # steps: grouping, the first updates, a global head at full capacity just
+    # before an update, the last steps
+    k_full = (B.HEADKV_MAX_CAPACITY - P - (t_g + 1)) // P + 2
+    steps = sorted({0, t_g - 1, t_g, t_g + 1, t_g + P - 1, t_g + P, t_g + k_full * P - 1,
+                    t_g + k_full * P, N // 2, N - 2, N - 1})
+    inp = DeviceInputs(wl, layers=[0])
+    inp.override[0] = torch.as_tensor(np.asarray(bud, dtype=np.int32), device="cuda")
+    sess = new_session(wl)
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps)
+    torch.cuda.synchronize()
+    ref = oracle.simulate(wl, 0, 0, snap_steps=steps, budget_override=bud, want_out=False)
+    assert list(ref["labels"]) == [1, 1, 0, 0]
+    assert np.array_equal(res["is_local"][0].cpu().numpy(), ref["labels"])
+    assert np.array_equal(res["n_star"][0].cpu().numpy(), ref["n_star"])
+    assert np.array_equal(res["budgets"][0].cpu().numpy(), ref["budgets"])
+    heads = [synth.head_inputs(wl, 0, 0, h) for h in range(wl.heads)]
+    worst, full = 0.0, 0
+    for i, t in enumerate(steps):
+        mask, count = res["snap"][(t, 0)]
+        mask, count = mask.cpu().numpy(), count.cpu().numpy()
+        out = res["out"][(t, 0)][0].cpu().double().numpy()
+        for h in range(wl.heads):
+            assert np.array_equal(mask[h], ref["snaps"][h][i]), (h, t)
+            full = max(full, int(count[h]))
+            q, k, v, kc, vc = heads[h]
+            keep = np.nonzero(mask[h])[0]
+            exp = oracle.attention(q[t], torch.cat([kc, k[keep]]), torch.cat([vc, v[keep]]))
+            err = float(np.abs(out[h] - exp).max())
+            worst = max(worst, err)
+            assert err <= ATOL, (h, t, err)
+    assert full == B.HEADKV_MAX_CAPACITY - 1  # a head one token short of its capacity
+    print(f"limits: bit-exact retained sets, max err {worst:.2e}, largest head {full}", flush=True)
+
+
+def test_side_streams_two_handles_concurrently():
+    # two handles driven from two host threads on two non-default streams at
+    # once; each must match the oracle on its own
+    from concurrent.futures import ThreadPoolExecutor
+    wl = W.TINY
+    steps = [0, wl.group_threshold - 1, wl.group_threshold, 100, 200, wl.num_visual - 1]
+    inp = DeviceInputs(wl, layers=[0])
+
+    def one(_):
+        s = torch.cuda.Stream()
+        with torch.cuda.stream(s):
+            sess = new_session(wl)
+            r = run_generation(sess, inp, out_steps=steps, snap_steps=steps)
+            s.synchronize()
+        return r
+
+    with ThreadPoolExecutor(max_workers=2) as ex:
+        runs = list(ex.map(one, range(2)))
+    ref = oracle.simulate(wl, 0, 0, snap_steps=steps)
+    for r in runs:
+        assert np.array_equal(r["is_local"][0].cpu().numpy(), ref["labels"])
+        assert np.array_equal(r["budgets"][0].cpu().numpy(), ref["budgets"])
+        for i, t in enumerate(steps):
+            mask = r["snap"][(t, 0)][0].cpu().numpy()
+            out = r["out"][(t, 0)][0].cpu().double().numpy()
+            for h in range(wl.heads):
+                assert np.array_equal(mask[h], ref["snaps"][h][i]), (h, t)
+                assert float(np.abs(out[h] - ref["out"][h][t]).max()) <= ATOL, (h, t)
