@@ -157,12 +157,14 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     // and their first use
     if (t_begin < t_stop) {  // a chunk past the head's length reads nothing
         Vec kk[TPR], vv[TPR];
+        // all K rows of the pass, then all V rows: the logits and their max
+        // are computed while the V rows are still arriving
 #pragma unroll
-        for (int j = 0; j < TPR; ++j) {
-            const int tok = min(t_begin + j * ROWS + row, t_stop - 1);
-            kk[j] = nt_load<NW>(krow(tok) + col * VPL);
-            vv[j] = nt_load<NW>(vrow(tok) + col * VPL);
-        }
+        for (int j = 0; j < TPR; ++j)
+            kk[j] = nt_load<NW>(krow(min(t_begin + j * ROWS + row, t_stop - 1)) + col * VPL);
+#pragma unroll
+        for (int j = 0; j < TPR; ++j)
+            vv[j] = nt_load<NW>(vrow(min(t_begin + j * ROWS + row, t_stop - 1)) + col * VPL);
         // keep every load of the pass ahead of its first use
         __builtin_amdgcn_sched_barrier(0);
         if (owner) append_store(L, C, D, h, n, a, av, tid);
@@ -177,11 +179,11 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     for (int t0 = t_begin + TP; t0 < t_stop; t0 += TP) {
         Vec kk[TPR], vv[TPR];
 #pragma unroll
-        for (int j = 0; j < TPR; ++j) {
-            const int tok = min(t0 + j * ROWS + row, t_stop - 1);
-            kk[j] = nt_load<NW>(krow(tok) + col * VPL);
-            vv[j] = nt_load<NW>(vrow(tok) + col * VPL);
-        }
+        for (int j = 0; j < TPR; ++j)
+            kk[j] = nt_load<NW>(krow(min(t0 + j * ROWS + row, t_stop - 1)) + col * VPL);
+#pragma unroll
+        for (int j = 0; j < TPR; ++j)
+            vv[j] = nt_load<NW>(vrow(min(t0 + j * ROWS + row, t_stop - 1)) + col * VPL);
         __builtin_amdgcn_sched_barrier(0);
         attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, t_end, qf, m, l, acc);
     }
