@@ -408,22 +408,29 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
     double* qs = reinterpret_cast<double*>(lds + UpdateLds::off_qs(N, lds_cap));
     int32_t* pos = reinterpret_cast<int32_t*>(lds + UpdateLds::off_pos(N, lds_cap));
     const int h = blockIdx.x, tid = threadIdx.x;
-    if (a.k != nullptr) {  // the step's append, then the update that follows it
-        const int n0 = L.n[h];
-        append_token(L, C, D, h, n0, a, tid);
-        __syncthreads();
-        append_commit(L, h, n0, tid);
-        __syncthreads();
-    }
-    const int n = L.n[h];
+    const int n0 = L.n[h];
     const int B = L.budget[h];
     const int local = L.label[h];
+    // the step's append, then the update that follows it; the update takes the
+    // new token's position and the new query sum from the append's own values
+    // rather than reading them back from memory
+    const bool app = a.k != nullptr;
+    double qs_new = 0.0;
+    if (app) {
+        const AppendVals av = append_load(L, D, h, a, tid);
+        append_store(L, C, D, h, n0, a, av, tid);
+        qs_new = av.qs_old + bf_f64(av.qbits);  // the query sum append_store wrote
+    }
+    const int n = n0 + (app ? 1 : 0);
     // Eq. (2): history = retained tokens older than the recent window
     const int w_eff = recent_len < B ? recent_len : B;
     const int T = n > w_eff ? n - w_eff : 0;
     const int keep = B - w_eff;
     const int M = T > keep ? T - keep : 0;
-    if (!relayout && M == 0) return;
+    if (!relayout && M == 0) {
+        if (app && tid == 0) L.n[h] = n;
+        return;
+    }
 
     const int src_cap = relayout ? dense_cap : L.cap[h];
     char* src_seg = relayout ? const_cast<char*>(src_kv) + (int64_t)h * dense_seg_bytes
@@ -436,7 +443,7 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
     for (int i = tid; i < n; i += kBlock) evict[i] = 0;
     __syncthreads();
     for (int s = tid; s < n; s += kBlock) {
-        const int p = S.pos[s];
+        const int p = (app && s == n0) ? a.step : S.pos[s];
         pos[s] = p;
         atomicOr(&bm[p >> 5], 1u << (p & 31));
     }
@@ -491,7 +498,8 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
             // 1/(P sqrt(d)) is dropped, the order is that of (sum q) . k, summed
             // over the dims in order in fp64.  Each thread reads half of its row's
             // 16-byte chunks together and then walks them in order.
-            for (int i = tid; i < D; i += kBlock) qs[i] = L.qsum[(size_t)h * D + i];
+            for (int i = tid; i < D; i += kBlock)
+                qs[i] = (app && a.accumulate) ? qs_new : L.qsum[(size_t)h * D + i];
             __syncthreads();
             for (int r = r_lo + tid; r < r_hi; r += kBlock) {
                 const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + order[r]) * D);
