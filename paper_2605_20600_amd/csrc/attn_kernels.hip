@@ -99,7 +99,7 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
 
 // The work of one attention block; `item` is its index among the blocks of
 // the layer.  TPR tokens per row and pass: 8, or 4 when every head fits in
-// half a pass.
+// half a pass, or 9 when that gives one pass where 8 would need two.
 template <int D, bool APPEND, int T, bool CHUNKED, int TPR>
 __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const AppendArgs& a,
                                            const uint16_t* __restrict__ q,
@@ -313,6 +313,8 @@ void attn_dispatch_t(const LayerDev& L, const Shape& s, const AppendArgs& a, con
         attn_launch<D, T, true, kAttnTpr>(L, s, a, q, out, partials, p, st, ev0, ev1);
     else if (p.tpr == kAttnTpr)
         attn_launch<D, T, false, kAttnTpr>(L, s, a, q, out, partials, p, st, ev0, ev1);
+    else if (p.tpr == kAttnTprWide)
+        attn_launch<D, T, false, kAttnTprWide>(L, s, a, q, out, partials, p, st, ev0, ev1);
     else
         attn_launch<D, T, false, kAttnTpr / 2>(L, s, a, q, out, partials, p, st, ev0, ev1);
 }
@@ -339,6 +341,9 @@ void layers_launch(const LayersArg& a, int layers, const MetaLayout& ml, const S
     if (tpr == kAttnTpr)
         hipLaunchKernelGGL((k_attn_layers<D, T, kAttnTpr>), grid, block, 0, st, a, ml, s.BH, s.C,
                            qscale);
+    else if (tpr == kAttnTprWide)
+        hipLaunchKernelGGL((k_attn_layers<D, T, kAttnTprWide>), grid, block, 0, st, a, ml, s.BH,
+                           s.C, qscale);
     else
         hipLaunchKernelGGL((k_attn_layers<D, T, kAttnTpr / 2>), grid, block, 0, st, a, ml, s.BH,
                            s.C, qscale);

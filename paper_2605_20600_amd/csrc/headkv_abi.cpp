@@ -366,6 +366,17 @@ int max_cap(const Layer& L) { return *std::max_element(L.cap.begin(), L.cap.end(
 
 // Largest block size at which `heads` one-block-per-head blocks are all
 // resident at once (256 beyond that; 1024 when they do not fill the CUs).
+// Tokens per row of a pass for a launch whose longest head reads `len`
+// tokens: half a pass when that suffices, the wide pass when it makes one pass
+// of what would otherwise take two, else the normal pass.
+int pass_tpr(int len, int threads, int d) {
+    if (len <= attn_tokens_per_pass(threads, d, kAttnTpr / 2)) return kAttnTpr / 2;
+    if (len > attn_tokens_per_pass(threads, d, kAttnTpr) &&
+        len <= attn_tokens_per_pass(threads, d, kAttnTprWide))
+        return kAttnTprWide;
+    return kAttnTpr;
+}
+
 int resident_threads(int heads) {
     for (int t = kAttnMaxThreads; t >= kAttnMinThreads; t /= 2)
         if (heads <= attn_resident_blocks(t)) return t;
@@ -389,9 +400,8 @@ int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
                         (appended ? 1 : 0);
     const int d = h->cfg.head_dim;
     auto whole = [&](int t, int heads, int use_order, int base, int pad) {
-        const int read = std::max(len_max, pad);
-        const int tpr = read <= attn_tokens_per_pass(t, d, kAttnTpr / 2) ? kAttnTpr / 2 : kAttnTpr;
-        return AttnPlan{t, 0, 0, heads, use_order, base, pad, tpr};
+        return AttnPlan{t, 0, 0, heads, use_order, base, pad,
+                        pass_tpr(std::max(len_max, pad), t, d)};
     };
     if (strategy == HEADKV_ATTN_PADDED) {
         out[0] = whole(resident_threads(BH), BH, 0, 0, len_max);
@@ -789,8 +799,7 @@ headkv_status headkv_decode_attn_layers(headkv_t h, int32_t layer_begin, int32_t
     const int t = resident_threads(BH);
     if (BH > attn_resident_blocks(t))
         return fail(HEADKV_ERR_UNSUPPORTED, "multi-layer attention needs every head resident");
-    const int tpr = len_max <= attn_tokens_per_pass(t, h->cfg.head_dim, kAttnTpr / 2) ? kAttnTpr / 2
-                                                                                      : kAttnTpr;
+    const int tpr = pass_tpr(len_max, t, h->cfg.head_dim);
     return hip_status(launch_attn_layers(args, n, h->ml, h->shape, t, tpr, stream),
                       "multi-layer attention launch");
 }

@@ -18,6 +18,9 @@ namespace headkv {
 
 constexpr int kBlock = 256;  // threads per block of the cache kernels
 constexpr int kAttnTpr = 8;  // tokens per 16-lane row per attention pass
+// A wider pass (9 tokens per row, still under 128 VGPRs) for launches whose
+// longest head just misses one pass of 8: one pass instead of two.
+constexpr int kAttnTprWide = 9;
 constexpr int kCus = 256;    // MI355X compute units
 // Attention blocks have 1024, 512 or 256 threads; 1024 threads of at most 128
 // VGPRs fill a CU, so a CU holds 1024 / threads blocks at once.  A token row

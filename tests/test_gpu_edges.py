@@ -166,3 +166,16 @@ def test_side_streams_two_handles_concurrently():
             for h in range(wl.heads):
                 assert np.array_equal(mask[h], ref["snaps"][h][i]), (h, t)
                 assert float(np.abs(out[h] - ref["out"][h][t]).max()) <= ATOL, (h, t)
+
+
+def test_wide_pass_d64():
+    # 8 x 32 heads of d = 64 in 1024-thread blocks (128 rows): near the end the
+    # longest head reads up to 32 + 1031 + 1 tokens, more than one pass of 8
+    # tokens per row (1024) and within one of 9 (1152)
+    wl = W.TINY.with_(batch=8, heads=32, grid_rows=32, grid_cols=32, period=32,
+                      group_threshold=100, budget_mode=W.BUDGET_OVERRIDE)
+    rng = np.random.default_rng(11)
+    bud = rng.integers(64, 1001, size=(8, 32))
+    bud[0, 3] = bud[7, 30] = 1000
+    _run(wl, budgets=bud, slices=((0, 0), (0, 7)),
+         steps=[99, 100, 500, 990, 1000, 1010, 1022, 1023])
