@@ -364,8 +364,6 @@ void commit_append(headkv_t h, Layer& L, int32_t step, bool update) {
 
 int max_cap(const Layer& L) { return *std::max_element(L.cap.begin(), L.cap.end()); }
 
-// Largest block size at which `heads` one-block-per-head blocks are all
-// resident at once (256 beyond that; 1024 when they do not fill the CUs).
 // Tokens per row of a pass for a launch whose longest head reads `len`
 // tokens: half a pass when that suffices, the wide pass when it makes one pass
 // of what would otherwise take two, else the normal pass.
@@ -377,6 +375,8 @@ int pass_tpr(int len, int threads, int d) {
     return kAttnTpr;
 }
 
+// Largest block size at which `heads` one-block-per-head blocks are all
+// resident at once (256 beyond that; 1024 when they do not fill the CUs).
 int resident_threads(int heads) {
     for (int t = kAttnMaxThreads; t >= kAttnMinThreads; t /= 2)
         if (heads <= attn_resident_blocks(t)) return t;
