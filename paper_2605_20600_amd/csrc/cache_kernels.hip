@@ -268,9 +268,9 @@ __device__ __forceinline__ double dot_row(const double* qd, const uint16_t* row)
 // sig[r] for the history ranks [r_lo, r_hi) accumulates the weights query by
 // query, in step order.
 // The window is taken G queries at a time: each thread reads a cached row once
-// and runs the G dot products as G independent fp64 chains (dims in order, no
-// FMA); the G normalisers are summed by G threads at once, each over its
-// query's cache in order.  qd: LDS [G][D]; w: LDS [G][wst] with wst >= C + n.
+// and runs the G dot products as G independent fp64 chains (dims in order);
+// the G normalisers are summed by G threads at once, each over its query's
+// cache in order.  qd: LDS [D][G]; w: LDS [G][wst] with wst >= C + n.
 template <int D, int G>
 __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C, int h, int n,
                                      int r_lo, int r_hi, int step,
@@ -290,7 +290,7 @@ __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C,
         // the group's queries in fp64 (rows past ng are zero and unused)
         for (int i = tid; i < G * D; i += kBlock) {
             const int g = i / D, e = i - g * D;
-            qd[i] = g < ng ? bf_f64(L.qring[((size_t)h * P + (pa + g) % P) * D + e]) : 0.0;
+            qd[e * G + g] = g < ng ? bf_f64(L.qring[((size_t)h * P + (pa + g) % P) * D + e]) : 0.0;
         }
         if (tid < ng) {  // visible visual tokens of query pa + tid: ranks with position <= p
             const int p = pa + tid;
@@ -320,9 +320,19 @@ __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C,
             int zo;
             asm volatile("s_mov_b32 %0, 0" : "=s"(zo));
             const double* qz = qd + zo;
-            double acc[G];
+            // qz is dim-major ([D][G]): the query values of the next S dims are
+            // read while this S dims' products are added (a scheduling barrier
+            // keeps the reads a stage ahead).  The product of two bf16 values
+            // is exact in fp64, so an fma rounds exactly like the oracle's
+            // multiply and add.
+            constexpr int S = 4;
+            double acc[G], qa[S][G], qb[S][G];
 #pragma unroll
             for (int g = 0; g < G; ++g) acc[g] = 0.0;
+#pragma unroll
+            for (int e = 0; e < S; ++e)
+#pragma unroll
+                for (int g = 0; g < G; ++g) qa[e][g] = qz[e * G + g];
             constexpr int HR = D / 16;  // half a row in flight at a time
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
@@ -332,15 +342,28 @@ __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C,
 #pragma unroll
                 for (int c = 0; c < HR; ++c) {
                     const uint32_t wv[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
-                    const int i0 = 8 * (half * HR + c);
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const double klo = (double)bf_lo(wv[e]), khi = (double)bf_hi(wv[e]);
+                    for (int st = 0; st < 8 / S; ++st) {
+                        const int i0 = 8 * (half * HR + c) + st * S;  // first dim of the stage
+                        if (i0 + S < D) {
 #pragma unroll
-                        for (int g = 0; g < G; ++g) {
-                            acc[g] = acc[g] + qz[g * D + i0 + 2 * e] * klo;
-                            acc[g] = acc[g] + qz[g * D + i0 + 2 * e + 1] * khi;
+                            for (int e = 0; e < S; ++e)
+#pragma unroll
+                                for (int g = 0; g < G; ++g) qb[e][g] = qz[(i0 + S + e) * G + g];
                         }
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int e = 0; e < S; ++e) {
+                            const int k = st * S + e;  // dim within the 16-byte chunk
+                            const double kv =
+                                (double)((k & 1) ? bf_hi(wv[k / 2]) : bf_lo(wv[k / 2]));
+#pragma unroll
+                            for (int g = 0; g < G; ++g) acc[g] = fma(qa[e][g], kv, acc[g]);
+                        }
+#pragma unroll
+                        for (int e = 0; e < S; ++e)
+#pragma unroll
+                            for (int g = 0; g < G; ++g) qa[e][g] = qb[e][g];
                     }
                 }
             }
@@ -372,7 +395,16 @@ __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C,
             const double* wg = w + (size_t)tid * wst;
             const int len = C + nvs[tid];
             double z = 0.0;
-            for (int j = 0; j < len; ++j) z += wg[j];
+            int j = 0;
+            // the reads go out eight at a time, the additions stay in order
+            for (; j + 8 <= len; j += 8) {
+                double t[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) t[u] = wg[j + u];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) z += t[u];
+            }
+            for (; j < len; ++j) z += wg[j];
             zsh[tid] = z;
         }
         __syncthreads();
