@@ -15,8 +15,10 @@
 //   k_export   retained-position masks for parity checks.
 //
 // Everything that decides an index (grouping mass, eviction scores) is
-// computed in fp64 with one fixed summation order and no fused multiply-add,
-// so the decisions do not depend on thread scheduling.
+// computed in fp64 with one fixed summation order, so the decisions do not
+// depend on thread scheduling; multiplies and adds stay separate wherever a
+// product can round (the attention-sum logits multiply two bf16 values, exact
+// in fp64, and use fma).
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
