@@ -78,6 +78,7 @@ def parse():
 # sources of the attention kernel: the profiler's byte counters stay valid
 # while these are unchanged
 ATTN_SOURCES = ("paper_2605_20600_amd/csrc/attn_kernels.hip",
+                "paper_2605_20600_amd/csrc/attn_block.h",
                 "paper_2605_20600_amd/csrc/device_common.h",
                 "paper_2605_20600_amd/csrc/layout.h")
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_attn_lumina768_b8_rho1-8_traffic.json")
@@ -367,7 +368,8 @@ def main():
              "k_attn<d> (after an update)",
              "k_update<d> (append + periodic update)",
              "k_prefill_attn<d> (prefix store + causal attention, headkv_prefill_attn)",
-             "k_attn<d, append> (headkv_decode_step, full cache before grouping)"]
+             "k_attn<d, append> (headkv_decode_step, full cache before grouping)",
+             "k_update_attn<d> (append + periodic update + attention, one launch)"]
     kinds = {}
     for name, (kms, kn, kb) in zip(names, per_kind):
         if kn:

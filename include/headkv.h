@@ -253,7 +253,10 @@ headkv_status headkv_timing_reserve(headkv_t h, int64_t launches);
 #define HEADKV_TIMED_PREFILL 3     /* prefix store + causal prefix attention */
 #define HEADKV_TIMED_ATTN_APPEND_DENSE 4 /* fused append + attention before
                                             grouping (full cache) */
-#define HEADKV_TIMED_KINDS 5
+#define HEADKV_TIMED_UPDATE_ATTN 5 /* append + periodic update + attention in
+                                      one launch (one block per head of
+                                      256 threads) */
+#define HEADKV_TIMED_KINDS 6
 
 /* Waits for the timed launches since the last collect and returns, per kind
  * (arrays of HEADKV_TIMED_KINDS), the sum of their kernel durations (ms), their

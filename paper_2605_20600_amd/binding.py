@@ -35,7 +35,8 @@ HEADKV_TIMED_ATTN = 1               # attention after an update
 HEADKV_TIMED_UPDATE = 2             # append + periodic update
 HEADKV_TIMED_PREFILL = 3            # prefix store + causal prefix attention
 HEADKV_TIMED_ATTN_APPEND_DENSE = 4  # fused append + attention before grouping
-HEADKV_TIMED_KINDS = 5
+HEADKV_TIMED_UPDATE_ATTN = 5        # append + periodic update + attention, one launch
+HEADKV_TIMED_KINDS = 6
 
 HEADKV_ATTN_VARLEN = 0
 HEADKV_ATTN_PADDED = 1
@@ -219,8 +220,8 @@ def headkv_timing_reserve(h: int, launches: int) -> None:
 def headkv_timing_collect(h: int):
     """Returns per kind (fused append + attention after grouping, attention
     after an update, append + update, prefill, fused append + attention before
-    grouping) a list of (kernel ms, launches, algorithmic bytes), and the
-    dropped count."""
+    grouping, append + update + attention in one launch) a list of (kernel ms,
+    launches, algorithmic bytes), and the dropped count."""
     K = HEADKV_TIMED_KINDS
     ms = (ctypes.c_double * K)()
     n = (ctypes.c_int64 * K)()

@@ -1,0 +1,233 @@
+// The decode-attention block of Eq. (1) over one head of the compressed cache,
+// shared by the attention kernels and the fused update + attention kernel.
+//
+// A block of T threads is rows of d/8 lanes (16 at d = 128, 8 at d = 64); each
+// row holds one token at a time, 8 elements per lane (one 16-byte load), so the
+// rows of a wavefront read consecutive K or V rows of the segment (1 KB).  A
+// pass covers T/(d/8) x TPR tokens: every load of the pass is issued before
+// the first one is used (row indices past the end are clamped to the last
+// token and their logits masked, so no load sits behind a branch), the K rows
+// before the V rows.  K/V are read once per step, so the loads are
+// non-temporal.  The softmax is online per row; rows are merged with
+// cross-lane swaps and the wavefronts through LDS.  With an append, the step's
+// token is attended from the input and written into the cache by the block
+// whose range holds it.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "device_common.h"
+#include "layout.h"
+
+namespace headkv {
+namespace dev {
+
+template <int D>
+struct AttnRegs {
+    static constexpr int LPR = D / 8;   // lanes per token row
+    static constexpr int VPL = 8;       // bf16 elements per lane
+    static constexpr int NW = VPL / 2;  // 32-bit words per lane
+    using Vec = Words<NW>;
+};
+
+template <int NW>
+__device__ __forceinline__ Words<NW> nt_load(const uint16_t* p) {
+    typedef unsigned int vec_t __attribute__((ext_vector_type(NW)));
+    const vec_t t = __builtin_nontemporal_load(reinterpret_cast<const vec_t*>(p));
+    Words<NW> w;
+#pragma unroll
+    for (int e = 0; e < NW; ++e) w.w[e] = t[e];
+    return w;
+}
+
+// Online-softmax update of one row's state with NT tokens t0 + j * ROWS + row
+// (those at or past t_end masked); k/v hold their d/16 elements of the lane.
+template <int D, int NT, int ROWS>
+__device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec (&kk)[NT],
+                                                const typename AttnRegs<D>::Vec (&vv)[NT],
+                                                int t0, int row, int t_end, const float* qf,
+                                                float& m, float& l, float* acc) {
+    constexpr int NW = AttnRegs<D>::NW;
+    constexpr int VPL = AttnRegs<D>::VPL;
+    float s[NT];
+    float mx = m;
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        float dp = 0.f;
+#pragma unroll
+        for (int e = 0; e < NW; ++e) {
+            dp += qf[2 * e] * bf_lo(kk[j].w[e]);
+            dp += qf[2 * e + 1] * bf_hi(kk[j].w[e]);
+        }
+        dp = lanes_sum<AttnRegs<D>::LPR>(dp);
+        s[j] = (t0 + j * ROWS + row < t_end) ? dp : -INFINITY;
+        mx = fmaxf(mx, s[j]);
+    }
+    if (mx != -INFINITY) {
+        const float f = __builtin_amdgcn_exp2f(m - mx);  // m = -inf gives 0
+        l *= f;
+#pragma unroll
+        for (int e = 0; e < VPL; ++e) acc[e] *= f;
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const float p = __builtin_amdgcn_exp2f(s[j] - mx);
+            l += p;
+#pragma unroll
+            for (int e = 0; e < NW; ++e) {
+                acc[2 * e] += p * bf_lo(vv[j].w[e]);
+                acc[2 * e + 1] += p * bf_hi(vv[j].w[e]);
+            }
+        }
+        m = mx;
+    }
+}
+
+// The work of one attention block; `item` is its index among the blocks of
+// the layer.  TPR tokens per row and pass: 8, or 4 when every head fits in
+// half a pass, or 9 when that gives one pass where 8 would need two.
+template <int D, bool APPEND, int T, bool CHUNKED, int TPR>
+__device__ __forceinline__ void attn_block(const LayerDev& L, int C, const AppendArgs& a,
+                                           const uint16_t* __restrict__ q,
+                                           float* __restrict__ out, float* __restrict__ part,
+                                           int use_order, int order_base, int pad_len,
+                                           float qscale, int item, int n_given = -1) {
+    using Vec = typename AttnRegs<D>::Vec;
+    constexpr int VPL = AttnRegs<D>::VPL;
+    constexpr int NW = AttnRegs<D>::NW;
+    constexpr int LPR = AttnRegs<D>::LPR;
+    constexpr int ROWS = T / LPR;
+    constexpr int TP = ROWS * TPR;  // tokens per pass
+    constexpr int WAVES = T / 64;
+    int h, t_begin;
+    if (CHUNKED) {
+        const uint32_t it = L.items[item];
+        h = (int)(it >> 8);
+        t_begin = (int)(it & 255u) * TP;
+    } else {
+        h = use_order ? L.order[order_base + item] : item;
+        t_begin = 0;
+    }
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int row = tid / LPR, col = tid % LPR;
+    const Vec qraw = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
+    // n_given: the length as the caller already knows it (a kernel that has
+    // just changed it), else the one in memory
+    const int n = n_given >= 0 ? n_given : L.n[h];
+    const int len = C + n + (APPEND ? 1 : 0);
+    const int t_end = CHUNKED ? min(len, t_begin + TP) : len;
+    // padding strategy: rows up to pad_len are read, those past len masked
+    const int t_stop = CHUNKED ? t_end : max(len, pad_len);
+    // the block whose range holds the new token (always the one block of a head
+    // that is not chunked) performs the append
+    const bool owner = APPEND && (!CHUNKED || (t_begin <= len - 1 && len - 1 < t_end));
+    const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + L.seg_off[h]);
+    const uint16_t* V = K + (size_t)(C + L.cap[h]) * D;
+    // K (or V) row of token `tok`: the step's new token comes from the input
+    auto krow = [&](int tok) {
+        return (APPEND && tok == len - 1) ? a.k + (size_t)h * D : K + (size_t)tok * D;
+    };
+    auto vrow = [&](int tok) {
+        return (APPEND && tok == len - 1) ? a.v + (size_t)h * D : V + (size_t)tok * D;
+    };
+
+    // the append's loads go out before the K/V stream and its stores right
+    // after (the attention reads the new token from the input, never from row
+    // C+n); n itself changes once no block reads it
+    AppendVals av;
+    if (owner) av = append_load(L, D, h, a, tid);
+    float m = -INFINITY, l = 0.f;
+    float acc[VPL];
+#pragma unroll
+    for (int e = 0; e < VPL; ++e) acc[e] = 0.f;
+    float qf[VPL];
+    // first pass: the append's store and q's conversion go between its loads
+    // and their first use
+    if (t_begin < t_stop) {  // a chunk past the head's length reads nothing
+        Vec kk[TPR], vv[TPR];
+        // all K rows of the pass, then all V rows: the logits and their max
+        // are computed while the V rows are still arriving
+#pragma unroll
+        for (int j = 0; j < TPR; ++j)
+            kk[j] = nt_load<NW>(krow(min(t_begin + j * ROWS + row, t_stop - 1)) + col * VPL);
+#pragma unroll
+        for (int j = 0; j < TPR; ++j)
+            vv[j] = nt_load<NW>(vrow(min(t_begin + j * ROWS + row, t_stop - 1)) + col * VPL);
+        // keep every load of the pass ahead of its first use
+        __builtin_amdgcn_sched_barrier(0);
+        if (owner) append_store(L, C, D, h, n, a, av, tid);
+#pragma unroll
+        for (int e = 0; e < NW; ++e) {
+            qf[2 * e] = bf_lo(qraw.w[e]) * qscale;
+            qf[2 * e + 1] = bf_hi(qraw.w[e]) * qscale;
+        }
+        attn_accumulate<D, TPR, ROWS>(kk, vv, t_begin, row, t_end, qf, m, l, acc);
+    }
+    // further passes of a head longer than one pass
+    for (int t0 = t_begin + TP; t0 < t_stop; t0 += TP) {
+        Vec kk[TPR], vv[TPR];
+#pragma unroll
+        for (int j = 0; j < TPR; ++j)
+            kk[j] = nt_load<NW>(krow(min(t0 + j * ROWS + row, t_stop - 1)) + col * VPL);
+#pragma unroll
+        for (int j = 0; j < TPR; ++j)
+            vv[j] = nt_load<NW>(vrow(min(t0 + j * ROWS + row, t_stop - 1)) + col * VPL);
+        __builtin_amdgcn_sched_barrier(0);
+        attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, t_end, qf, m, l, acc);
+    }
+    // merge the rows of each wavefront
+#pragma unroll
+    for (int off = LPR; off <= 32; off <<= 1) {
+        const float mo = __shfl_xor(m, off);
+        const float lo = __shfl_xor(l, off);
+        const float mn = fmaxf(m, mo);
+        const float fa = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mn);
+        const float fb = (mo == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mo - mn);
+        l = l * fa + lo * fb;
+#pragma unroll
+        for (int e = 0; e < VPL; ++e) {
+            const float ao = __shfl_xor(acc[e], off);
+            acc[e] = acc[e] * fa + ao * fb;
+        }
+        m = mn;
+    }
+    __shared__ float sm[WAVES], sl[WAVES];
+    __shared__ float sacc[WAVES][D];
+    if (lane < LPR) {
+#pragma unroll
+        for (int e = 0; e < VPL; ++e) sacc[wave][col * VPL + e] = acc[e];
+        if (lane == 0) {
+            sm[wave] = m;
+            sl[wave] = l;
+        }
+    }
+    __syncthreads();  // every wavefront has read n before the append changes it
+    if (owner && !CHUNKED) append_commit(L, h, n, tid);
+    if (tid < D) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) mx = fmaxf(mx, sm[w]);
+        float o = 0.f, z = 0.f;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) {
+            const float f = (sm[w] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sm[w] - mx);
+            o += f * sacc[w][tid];
+            z += f * sl[w];
+        }
+        if (!CHUNKED) {
+            out[(size_t)h * D + tid] = o / z;
+        } else {
+            float* pp = part + (size_t)item * (D + 2);
+            pp[tid] = o;
+            if (tid == 0) {
+                pp[D] = mx;
+                pp[D + 1] = z;
+            }
+        }
+    }
+}
+
+}  // namespace dev
+}  // namespace headkv

@@ -26,6 +26,7 @@
 #include <cstdint>
 
 #include "../../include/headkv.h"
+#include "attn_block.h"
 #include "device_common.h"
 #include "layout.h"
 
@@ -425,12 +426,14 @@ __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C,
 // new segment).  ATTN_SUM: the attention-sum scores instead of Eq. 6; a
 // separate instantiation, since its fp64 exp needs about twice the registers
 // (the Eq. 6 kernel stays under 64 VGPRs: eight 256-thread blocks per CU).
+// The update of head h by the block's kBlock threads (body of k_update and of
+// the fused update + attention kernel); returns the head's length afterwards.
 template <int D, bool ATTN_SUM, int G>
-__global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, AppendArgs a,
-                                                   const char* src_kv, int relayout,
-                                                   int64_t dense_seg_bytes, int dense_cap,
-                                                   int recent_len, int rs_num, int rs_den, int u,
-                                                   int step, int lds_cap, double sqrt_d) {
+__device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, const AppendArgs& a,
+                                            const char* src_kv, int relayout,
+                                            int64_t dense_seg_bytes, int dense_cap,
+                                            int recent_len, int rs_num, int rs_den, int u,
+                                            int step, int lds_cap, double sqrt_d, int h) {
 #pragma clang fp contract(off)
     constexpr int kRow16 = D / 8;  // 16-byte chunks per row
     extern __shared__ __align__(16) unsigned char lds[];
@@ -441,7 +444,7 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
     double* sig = reinterpret_cast<double*>(lds + UpdateLds::off_sig(N, lds_cap));
     double* qs = reinterpret_cast<double*>(lds + UpdateLds::off_qs(N, lds_cap));
     int32_t* pos = reinterpret_cast<int32_t*>(lds + UpdateLds::off_pos(N, lds_cap));
-    const int h = blockIdx.x, tid = threadIdx.x;
+    const int tid = threadIdx.x;
     const int n0 = L.n[h];
     const int B = L.budget[h];
     const int local = L.label[h];
@@ -463,7 +466,7 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
     const int M = T > keep ? T - keep : 0;
     if (!relayout && M == 0) {
         if (app && tid == 0) L.n[h] = n;
-        return;
+        return n;
     }
 
     const int src_cap = relayout ? dense_cap : L.cap[h];
@@ -632,6 +635,37 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
         for (int j = tid; j < nh; j += kBlock) S.pos[list_a[j]] = pos[list_b[j]];
     }
     if (tid == 0) L.n[h] = n_new;
+    return n_new;
+}
+
+template <int D, bool ATTN_SUM, int G>
+__global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, AppendArgs a,
+                                                   const char* src_kv, int relayout,
+                                                   int64_t dense_seg_bytes, int dense_cap,
+                                                   int recent_len, int rs_num, int rs_den, int u,
+                                                   int step, int lds_cap, double sqrt_d) {
+    update_block<D, ATTN_SUM, G>(L, C, N, a, src_kv, relayout, dense_seg_bytes, dense_cap,
+                                 recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d,
+                                 (int)blockIdx.x);
+}
+
+// A step's append, periodic update and attention in one launch, for layers
+// whose attention runs one kBlock-thread block per head: the block updates its
+// head (Eq. 6 scores), then attends over the updated cache with the length it
+// has just computed.  The head comes from the dispatch order when use_order.
+// At most 128 VGPRs, as the attention kernels: four blocks per CU.
+template <int D, int TPR>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_update_attn(
+    LayerDev L, int C, int N, AppendArgs a, int recent_len, int rs_num, int rs_den, int u,
+    int step, int lds_cap, double sqrt_d, const uint16_t* __restrict__ q,
+    float* __restrict__ out, int use_order, int pad_len, float qscale) {
+    const int h = use_order ? L.order[blockIdx.x] : (int)blockIdx.x;
+    const int n = update_block<D, false, 1>(L, C, N, a, nullptr, 0, 0, 0, recent_len, rs_num,
+                                            rs_den, u, step, lds_cap, sqrt_d, h);
+    __syncthreads();  // the rows the update moved are read by other threads
+    const AppendArgs none{};
+    attn_block<D, false, kBlock, false, TPR>(L, C, none, q, out, nullptr, 0, 0, pad_len, qscale,
+                                             h, n);
 }
 
 // ------------------------------------------------------------------- export
@@ -727,6 +761,47 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
         else HEADKV_UPDATE(64, true, 1);
     }
 #undef HEADKV_UPDATE
+    return last_error();
+}
+
+int launch_update_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, int recent_len,
+                       int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
+                       const uint16_t* q, float* out, int use_order, int pad_len, int tpr,
+                       void* stream, void* ev_start, void* ev_stop) {
+    hipStream_t st = (hipStream_t)stream;
+    hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
+    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, false, 1);
+    static const bool lds_ok = [] {
+        const int max_lds = 160 * 1024;
+        const void* fns[6] = {reinterpret_cast<const void*>(&k_update_attn<128, kAttnTpr / 2>),
+                              reinterpret_cast<const void*>(&k_update_attn<128, kAttnTpr>),
+                              reinterpret_cast<const void*>(&k_update_attn<128, kAttnTprWide>),
+                              reinterpret_cast<const void*>(&k_update_attn<64, kAttnTpr / 2>),
+                              reinterpret_cast<const void*>(&k_update_attn<64, kAttnTpr>),
+                              reinterpret_cast<const void*>(&k_update_attn<64, kAttnTprWide>)};
+        bool ok = true;
+        for (const void* f : fns)
+            ok = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds) ==
+                     hipSuccess && ok;
+        (void)hipGetLastError();
+        return ok;
+    }();
+    (void)lds_ok;
+    const float qscale = (float)(1.4426950408889634 / sqrt_d);
+#define HEADKV_UPDATE_ATTN(D_, T_)                                                                \
+    hipExtLaunchKernelGGL((k_update_attn<D_, T_>), dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0,   \
+                          L, s.C, s.N, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q, \
+                          out, use_order, pad_len, qscale)
+    if (s.d == 128) {
+        if (tpr == kAttnTpr) HEADKV_UPDATE_ATTN(128, kAttnTpr);
+        else if (tpr == kAttnTprWide) HEADKV_UPDATE_ATTN(128, kAttnTprWide);
+        else HEADKV_UPDATE_ATTN(128, kAttnTpr / 2);
+    } else {
+        if (tpr == kAttnTpr) HEADKV_UPDATE_ATTN(64, kAttnTpr);
+        else if (tpr == kAttnTprWide) HEADKV_UPDATE_ATTN(64, kAttnTprWide);
+        else HEADKV_UPDATE_ATTN(64, kAttnTpr / 2);
+    }
+#undef HEADKV_UPDATE_ATTN
     return last_error();
 }
 

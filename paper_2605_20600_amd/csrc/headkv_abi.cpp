@@ -537,12 +537,27 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
     none.k = none.v = none.q = nullptr;
     void *e0, *e1;
     if (update) {
-        take_events(h, time_it, HEADKV_TIMED_UPDATE, update_bytes(h, L), &e0, &e1);
+        const double ub = update_bytes(h, L);  // over the lengths before the step
+        const int lds_cap = max_cap(L);
+        commit_append(h, L, step, update);
+        // the attention that follows, over the lengths after the update: with
+        // one kBlock-thread block per head, the update's block attends too
+        AttnPlan plans[2];
+        const int np = attn_plans(h, L, false, plans);
+        if (c.score_mode == HEADKV_SCORE_MEAN_LOGIT && np == 1 && !plans[0].chunked &&
+            plans[0].threads == kBlock) {
+            take_events(h, time_it, HEADKV_TIMED_UPDATE_ATTN, ub + attn_bytes(h, L), &e0, &e1);
+            return hip_status(launch_update_attn(D, h->shape, a, c.recent_len, c.rs_num, c.rs_den,
+                                                 u, step, lds_cap, sqrt_d(h), q, out,
+                                                 plans[0].use_order, plans[0].pad_len,
+                                                 plans[0].tpr, stream, e0, e1),
+                              "append + update + attention launch");
+        }
+        take_events(h, time_it, HEADKV_TIMED_UPDATE, ub, &e0, &e1);
         st = hip_status(launch_update(D, h->shape, a, nullptr, 0, 0, 0, c.recent_len, c.rs_num,
-                                      c.rs_den, u, step, max_cap(L), sqrt_d(h), stream, e0, e1),
+                                      c.rs_den, u, step, lds_cap, sqrt_d(h), stream, e0, e1),
                         "append + update launch");
         if (st) return st;
-        commit_append(h, L, step, update);
         take_events(h, time_it, HEADKV_TIMED_ATTN, attn_bytes(h, L), &e0, &e1);
         return hip_status(launch_attention(h, L, D, none, q, out, stream, e0, e1),
                           "attention launch");
