@@ -181,10 +181,12 @@ def test_wide_pass_d64():
          steps=[99, 100, 500, 990, 1000, 1010, 1022, 1023])
 
 
-@pytest.mark.parametrize("fused", [True, False])
-def test_update_and_attention_in_one_launch(fused):
+@pytest.mark.parametrize("fused,strategy", [(True, 0), (False, 0), (True, 1)],
+                         ids=["fused", "separate", "fused-padded"])
+def test_update_and_attention_in_one_launch(fused, strategy):
     # 24 x 24 = 576 heads: the attention runs one 256-thread block per head, so
     # each update step's append, update and attention go out as one launch
-    # (fused) or as the separate calls; every step checked
+    # (fused) or as the separate calls; every step checked, with per-head
+    # lengths and with padding + mask
     wl = W.TINY.with_(batch=24, heads=24, period=4)
-    _run(wl, slices=((0, 0), (0, 23)), fused=fused)
+    _run(wl, slices=((0, 0), (0, 23)), fused=fused, attn_strategy=strategy)
