@@ -186,29 +186,30 @@ __device__ __forceinline__ uint64_t score_key(double x) {
 // a radix select over the keys, 8 bits per pass from the top, that stops as
 // soon as the chosen digit's bucket leaves entirely; if the exact threshold key
 // is reached, the entries equal to it leave in rank order.
+template <int NT>
 __device__ void select_lowest(const double* sig, const uint16_t* order, uint8_t* evict, int lo,
                               int hi, int mq, int tid) {
     __shared__ uint32_t hist[256];
     __shared__ int pick[3];  // digit, entries below its bucket, bucket size
     if (mq <= 0) return;
     if (mq >= hi - lo) {
-        for (int r = lo + tid; r < hi; r += kBlock) evict[order[r]] = 1;
+        for (int r = lo + tid; r < hi; r += NT) evict[order[r]] = 1;
         return;
     }
     uint64_t prefix = 0;  // chosen digits so far
     int want = mq;        // entries still to take at or above the prefix
     for (int shift = 56;; shift -= 8) {
         const uint64_t above = shift == 56 ? 0ull : ~0ull << (shift + 8);
-        hist[tid] = 0u;
+        if (tid < 256) hist[tid] = 0u;
         __syncthreads();
-        for (int r = lo + tid; r < hi; r += kBlock) {
+        for (int r = lo + tid; r < hi; r += NT) {
             const uint64_t k = score_key(sig[r]);
             if ((k & above) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
         }
         __syncthreads();
-        const int c = (int)hist[tid];
+        const int c = tid < 256 ? (int)hist[tid] : 0;
         int tot;
-        const int ex = block_exclusive_scan(c, &tot);
+        const int ex = block_exclusive_scan<NT>(c, &tot);
         if (ex < want && want <= ex + c) {
             pick[0] = tid;
             pick[1] = ex;
@@ -219,22 +220,22 @@ __device__ void select_lowest(const double* sig, const uint16_t* order, uint8_t*
         want -= pick[1];
         const uint64_t upto = ~0ull << shift;
         if (want == pick[2]) {  // the whole bucket leaves with everything below it
-            for (int r = lo + tid; r < hi; r += kBlock)
+            for (int r = lo + tid; r < hi; r += NT)
                 if ((score_key(sig[r]) & upto) <= prefix) evict[order[r]] = 1;
             return;
         }
         if (shift == 0) {  // prefix is the exact threshold key
             int taken = 0;
-            for (int r0 = lo; r0 < hi && taken < want; r0 += kBlock) {
+            for (int r0 = lo; r0 < hi && taken < want; r0 += NT) {
                 const int r = r0 + tid;
                 const uint64_t k = r < hi ? score_key(sig[r]) : ~0ull;
                 const int eq = (r < hi && k == prefix) ? 1 : 0;
                 int t;
-                const int e = block_exclusive_scan(eq, &t);
+                const int e = block_exclusive_scan<NT>(eq, &t);
                 if (eq && taken + e < want) evict[order[r]] = 1;
                 taken += t;
             }
-            for (int r = lo + tid; r < hi; r += kBlock)
+            for (int r = lo + tid; r < hi; r += NT)
                 if (score_key(sig[r]) < prefix) evict[order[r]] = 1;
             return;
         }
@@ -426,15 +427,17 @@ __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C,
 // new segment).  ATTN_SUM: the attention-sum scores instead of Eq. 6; a
 // separate instantiation, since its fp64 exp needs about twice the registers
 // (the Eq. 6 kernel stays under 64 VGPRs: eight 256-thread blocks per CU).
-// The update of head h by the block's kBlock threads (body of k_update and of
-// the fused update + attention kernel); returns the head's length afterwards.
-template <int D, bool ATTN_SUM, int G>
+// The update of head h by the block's NT threads (body of k_update and of the
+// fused update + attention kernel); returns the head's length afterwards.
+template <int D, bool ATTN_SUM, int G, int NT = kBlock>
 __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, const AppendArgs& a,
                                             const char* src_kv, int relayout,
                                             int64_t dense_seg_bytes, int dense_cap,
                                             int recent_len, int rs_num, int rs_den, int u,
                                             int step, int lds_cap, double sqrt_d, int h) {
 #pragma clang fp contract(off)
+    static_assert(!ATTN_SUM || NT == kBlock, "attention-sum scores run in 256-thread blocks");
+    static_assert(NT >= 256 && NT % 64 == 0, "the radix select needs at least 256 threads");
     constexpr int kRow16 = D / 8;  // 16-byte chunks per row
     extern __shared__ __align__(16) unsigned char lds[];
     uint32_t* bm = reinterpret_cast<uint32_t*>(lds);
@@ -476,10 +479,10 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
 
     // rank every occupied slot by its position: bitmap + prefix popcount
     const int nw = UpdateLds::words(N);
-    for (int i = tid; i < nw; i += kBlock) bm[i] = 0u;
-    for (int i = tid; i < n; i += kBlock) evict[i] = 0;
+    for (int i = tid; i < nw; i += NT) bm[i] = 0u;
+    for (int i = tid; i < n; i += NT) evict[i] = 0;
     __syncthreads();
-    for (int s = tid; s < n; s += kBlock) {
+    for (int s = tid; s < n; s += NT) {
         const int p = (app && s == n0) ? a.step : S.pos[s];
         pos[s] = p;
         atomicOr(&bm[p >> 5], 1u << (p & 31));
@@ -490,12 +493,12 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
         const int c0 = w0 < nw ? __popc(bm[w0]) : 0;
         const int c1 = w0 + 1 < nw ? __popc(bm[w0 + 1]) : 0;
         int tot;
-        const int ex = block_exclusive_scan(c0 + c1, &tot);
+        const int ex = block_exclusive_scan<NT>(c0 + c1, &tot);
         if (w0 < nw) wpre[w0] = ex;
         if (w0 + 1 < nw) wpre[w0 + 1] = ex + c0;
     }
     __syncthreads();
-    for (int s = tid; s < n; s += kBlock) {
+    for (int s = tid; s < n; s += NT) {
         const int p = pos[s];
         const int r = wpre[p >> 5] + __popc(bm[p >> 5] & ((1u << (p & 31)) - 1u));
         order[r] = (uint16_t)s;
@@ -505,7 +508,7 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
     if (M > 0) {
         if (local) {
             // Eq. (3): sliding window, the M oldest leave
-            for (int r = tid; r < M; r += kBlock) evict[order[r]] = 1;
+            for (int r = tid; r < M; r += NT) evict[order[r]] = 1;
         } else {
             // Eq. (5): long-range part = the oldest floor(T r_s) history tokens
             const int n_long = (int)((long long)T * rs_num / rs_den);
@@ -535,10 +538,10 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
             // 1/(P sqrt(d)) is dropped, the order is that of (sum q) . k, summed
             // over the dims in order in fp64.  Each thread reads half of its row's
             // 16-byte chunks together and then walks them in order.
-            for (int i = tid; i < D; i += kBlock)
+            for (int i = tid; i < D; i += NT)
                 qs[i] = (app && a.accumulate) ? qs_new : L.qsum[(size_t)h * D + i];
             __syncthreads();
-            for (int r = r_lo + tid; r < r_hi; r += kBlock) {
+            for (int r = r_lo + tid; r < r_hi; r += NT) {
                 const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + order[r]) * D);
                 double acc = 0.0;
                 // half a row in flight at a time keeps the kernel under 64
@@ -566,8 +569,8 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
             }
             __syncthreads();
             // per part, evict the m lowest by (score, position)
-            select_lowest(sig, order, evict, 0, n_long, m_long, tid);
-            select_lowest(sig, order, evict, n_long, T, m_near, tid);
+            select_lowest<NT>(sig, order, evict, 0, n_long, m_long, tid);
+            select_lowest<NT>(sig, order, evict, n_long, T, m_near, tid);
         }
     }
     __syncthreads();
@@ -582,16 +585,16 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
         const uint4* sv = reinterpret_cast<const uint4*>(S.V);
         uint4* dk = reinterpret_cast<uint4*>(Dd.K);
         uint4* dv = reinterpret_cast<uint4*>(Dd.V);
-        for (int i = tid; i < C * kRow16; i += kBlock) {
+        for (int i = tid; i < C * kRow16; i += NT) {
             dk[i] = sk[i];
             dv[i] = sv[i];
         }
         int base = 0;
-        for (int r0 = 0; r0 < n; r0 += kBlock) {
+        for (int r0 = 0; r0 < n; r0 += NT) {
             const int r = r0 + tid;
             const int kf = (r < n && !evict[order[r]]) ? 1 : 0;
             int tot;
-            const int ex = block_exclusive_scan(kf, &tot);
+            const int ex = block_exclusive_scan<NT>(kf, &tot);
             if (kf) {
                 list_a[base + ex] = order[r];
                 Dd.pos[base + ex] = pos[order[r]];
@@ -599,7 +602,7 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
             base += tot;
         }
         __syncthreads();
-        for (int i = tid; i < n_new * kRow16; i += kBlock) {
+        for (int i = tid; i < n_new * kRow16; i += NT) {
             const int j = i / kRow16, c = i - j * kRow16;
             const size_t src = (size_t)(C + list_a[j]) * kRow16 + c;
             const size_t dst = (size_t)(C + j) * kRow16 + c;
@@ -610,13 +613,13 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
         // in place: evicted slots below n_new are refilled from kept slots at or
         // above n_new; the two sets are disjoint, so no copy reads a written row
         int nh = 0, nf = 0;
-        for (int s0 = 0; s0 < n; s0 += kBlock) {
+        for (int s0 = 0; s0 < n; s0 += NT) {
             const int s = s0 + tid;
             const int hf = (s < n_new && evict[s]) ? 1 : 0;
             const int ff = (s >= n_new && s < n && !evict[s]) ? 1 : 0;
             int th, tf;
-            const int eh = block_exclusive_scan(hf, &th);
-            const int ef = block_exclusive_scan(ff, &tf);
+            const int eh = block_exclusive_scan<NT>(hf, &th);
+            const int ef = block_exclusive_scan<NT>(ff, &tf);
             if (hf) list_a[nh + eh] = s;
             if (ff) list_b[nf + ef] = s;
             nh += th;
@@ -625,14 +628,14 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
         __syncthreads();
         uint4* k4 = reinterpret_cast<uint4*>(S.K);
         uint4* v4 = reinterpret_cast<uint4*>(S.V);
-        for (int i = tid; i < nh * kRow16; i += kBlock) {
+        for (int i = tid; i < nh * kRow16; i += NT) {
             const int j = i / kRow16, c = i - j * kRow16;
             const size_t dst = (size_t)(C + list_a[j]) * kRow16 + c;
             const size_t src = (size_t)(C + list_b[j]) * kRow16 + c;
             k4[dst] = k4[src];
             v4[dst] = v4[src];
         }
-        for (int j = tid; j < nh; j += kBlock) S.pos[list_a[j]] = pos[list_b[j]];
+        for (int j = tid; j < nh; j += NT) S.pos[list_a[j]] = pos[list_b[j]];
     }
     if (tid == 0) L.n[h] = n_new;
     return n_new;
@@ -650,22 +653,23 @@ __global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, App
 }
 
 // A step's append, periodic update and attention in one launch, for layers
-// whose attention runs one kBlock-thread block per head: the block updates its
-// head (Eq. 6 scores), then attends over the updated cache with the length it
-// has just computed.  The head comes from the dispatch order when use_order.
-// At most 128 VGPRs, as the attention kernels: four blocks per CU.
-template <int D, int TPR>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(4))) void k_update_attn(
+// whose attention runs one T-thread block per head: the block updates its
+// head (Eq. 6 scores) with all its threads, then attends over the updated
+// cache with the length it has just computed.  The head comes from the
+// dispatch order when use_order.  At most 128 VGPRs, as the attention
+// kernels: 1024 / T blocks per CU.
+template <int D, int T, int TPR>
+__global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_update_attn(
     LayerDev L, int C, int N, AppendArgs a, int recent_len, int rs_num, int rs_den, int u,
     int step, int lds_cap, double sqrt_d, const uint16_t* __restrict__ q,
     float* __restrict__ out, int use_order, int pad_len, float qscale) {
     const int h = use_order ? L.order[blockIdx.x] : (int)blockIdx.x;
-    const int n = update_block<D, false, 1>(L, C, N, a, nullptr, 0, 0, 0, recent_len, rs_num,
-                                            rs_den, u, step, lds_cap, sqrt_d, h);
+    const int n = update_block<D, false, 1, T>(L, C, N, a, nullptr, 0, 0, 0, recent_len,
+                                               rs_num, rs_den, u, step, lds_cap, sqrt_d, h);
     __syncthreads();  // the rows the update moved are read by other threads
     const AppendArgs none{};
-    attn_block<D, false, kBlock, false, TPR>(L, C, none, q, out, nullptr, 0, 0, pad_len, qscale,
-                                             h, n);
+    attn_block<D, false, T, false, TPR>(L, C, none, q, out, nullptr, 0, 0, pad_len, qscale, h,
+                                        n);
 }
 
 // ------------------------------------------------------------------- export
@@ -764,44 +768,77 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
     return last_error();
 }
 
-int launch_update_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, int recent_len,
-                       int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
-                       const uint16_t* q, float* out, int use_order, int pad_len, int tpr,
-                       void* stream, void* ev_start, void* ev_stop) {
-    hipStream_t st = (hipStream_t)stream;
-    hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
-    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, false, 1);
+namespace {
+
+template <int D, int T, int TPR>
+void update_attn_launch(const LayerDev& L, const Shape& s, const AppendArgs& a, int recent_len,
+                        int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
+                        const uint16_t* q, float* out, int use_order, int pad_len, size_t lds,
+                        hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    // allow more than 64 KB of dynamic LDS (gfx950: 160 KB), once per kernel
     static const bool lds_ok = [] {
-        const int max_lds = 160 * 1024;
-        const void* fns[6] = {reinterpret_cast<const void*>(&k_update_attn<128, kAttnTpr / 2>),
-                              reinterpret_cast<const void*>(&k_update_attn<128, kAttnTpr>),
-                              reinterpret_cast<const void*>(&k_update_attn<128, kAttnTprWide>),
-                              reinterpret_cast<const void*>(&k_update_attn<64, kAttnTpr / 2>),
-                              reinterpret_cast<const void*>(&k_update_attn<64, kAttnTpr>),
-                              reinterpret_cast<const void*>(&k_update_attn<64, kAttnTprWide>)};
-        bool ok = true;
-        for (const void* f : fns)
-            ok = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds) ==
-                     hipSuccess && ok;
+        const bool ok = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_update_attn<D, T, TPR>),
+                                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                                            160 * 1024) == hipSuccess;
         (void)hipGetLastError();
         return ok;
     }();
     (void)lds_ok;
     const float qscale = (float)(1.4426950408889634 / sqrt_d);
-#define HEADKV_UPDATE_ATTN(D_, T_)                                                                \
-    hipExtLaunchKernelGGL((k_update_attn<D_, T_>), dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0,   \
-                          L, s.C, s.N, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q, \
-                          out, use_order, pad_len, qscale)
-    if (s.d == 128) {
-        if (tpr == kAttnTpr) HEADKV_UPDATE_ATTN(128, kAttnTpr);
-        else if (tpr == kAttnTprWide) HEADKV_UPDATE_ATTN(128, kAttnTprWide);
-        else HEADKV_UPDATE_ATTN(128, kAttnTpr / 2);
-    } else {
-        if (tpr == kAttnTpr) HEADKV_UPDATE_ATTN(64, kAttnTpr);
-        else if (tpr == kAttnTprWide) HEADKV_UPDATE_ATTN(64, kAttnTprWide);
-        else HEADKV_UPDATE_ATTN(64, kAttnTpr / 2);
-    }
-#undef HEADKV_UPDATE_ATTN
+    hipExtLaunchKernelGGL((k_update_attn<D, T, TPR>), dim3(s.BH), dim3(T), lds, st, e0, e1, 0, L,
+                          s.C, s.N, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q,
+                          out, use_order, pad_len, qscale);
+}
+
+template <int D, int T>
+void update_attn_tpr(const LayerDev& L, const Shape& s, const AppendArgs& a, int recent_len,
+                     int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
+                     const uint16_t* q, float* out, int use_order, int pad_len, int tpr,
+                     size_t lds, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    if (tpr == kAttnTpr)
+        update_attn_launch<D, T, kAttnTpr>(L, s, a, recent_len, rs_num, rs_den, u, step, lds_cap,
+                                           sqrt_d, q, out, use_order, pad_len, lds, st, e0, e1);
+    else if (tpr == kAttnTprWide)
+        update_attn_launch<D, T, kAttnTprWide>(L, s, a, recent_len, rs_num, rs_den, u, step,
+                                               lds_cap, sqrt_d, q, out, use_order, pad_len, lds,
+                                               st, e0, e1);
+    else
+        update_attn_launch<D, T, kAttnTpr / 2>(L, s, a, recent_len, rs_num, rs_den, u, step,
+                                               lds_cap, sqrt_d, q, out, use_order, pad_len, lds,
+                                               st, e0, e1);
+}
+
+template <int D>
+void update_attn_threads(const LayerDev& L, const Shape& s, const AppendArgs& a, int recent_len,
+                         int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
+                         const uint16_t* q, float* out, int use_order, int pad_len, int threads,
+                         int tpr, size_t lds, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+    if (threads == 1024)
+        update_attn_tpr<D, 1024>(L, s, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q,
+                                 out, use_order, pad_len, tpr, lds, st, e0, e1);
+    else if (threads == 512)
+        update_attn_tpr<D, 512>(L, s, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q,
+                                out, use_order, pad_len, tpr, lds, st, e0, e1);
+    else
+        update_attn_tpr<D, 256>(L, s, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q,
+                                out, use_order, pad_len, tpr, lds, st, e0, e1);
+}
+
+}  // namespace
+
+int launch_update_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, int recent_len,
+                       int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
+                       const uint16_t* q, float* out, int use_order, int pad_len, int threads,
+                       int tpr, void* stream, void* ev_start, void* ev_stop) {
+    hipStream_t st = (hipStream_t)stream;
+    hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
+    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, false, 1);
+    if (s.d == 128)
+        update_attn_threads<128>(L, s, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q,
+                                 out, use_order, pad_len, threads, tpr, lds, st, e0, e1);
+    else
+        update_attn_threads<64>(L, s, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q,
+                                out, use_order, pad_len, threads, tpr, lds, st, e0, e1);
     return last_error();
 }
 

@@ -37,10 +37,11 @@ __device__ __forceinline__ float lanes_sum(float v) {
     return v;
 }
 
-// Exclusive prefix sum over a 256-thread block; *total receives the sum.
-// Every thread of the block must call it.
+// Exclusive prefix sum over a block of NT threads (256 by default);
+// *total receives the sum.  Every thread of the block must call it.
+template <int NT = kBlock>
 __device__ inline int block_exclusive_scan(int x, int* total) {
-    __shared__ int wsum[kBlock / 64];
+    __shared__ int wsum[NT / 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int inc = x;
 #pragma unroll
@@ -52,7 +53,7 @@ __device__ inline int block_exclusive_scan(int x, int* total) {
     __syncthreads();
     int off = 0, tot = 0;
 #pragma unroll
-    for (int w = 0; w < kBlock / 64; ++w) {
+    for (int w = 0; w < NT / 64; ++w) {
         off += w < wave ? wsum[w] : 0;
         tot += wsum[w];
     }

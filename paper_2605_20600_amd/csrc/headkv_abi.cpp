@@ -541,16 +541,15 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
         const int lds_cap = max_cap(L);
         commit_append(h, L, step, update);
         // the attention that follows, over the lengths after the update: with
-        // one kBlock-thread block per head, the update's block attends too
+        // one block per head, the update's block attends too
         AttnPlan plans[2];
         const int np = attn_plans(h, L, false, plans);
-        if (c.score_mode == HEADKV_SCORE_MEAN_LOGIT && np == 1 && !plans[0].chunked &&
-            plans[0].threads == kBlock) {
+        if (c.score_mode == HEADKV_SCORE_MEAN_LOGIT && np == 1 && !plans[0].chunked) {
             take_events(h, time_it, HEADKV_TIMED_UPDATE_ATTN, ub + attn_bytes(h, L), &e0, &e1);
             return hip_status(launch_update_attn(D, h->shape, a, c.recent_len, c.rs_num, c.rs_den,
                                                  u, step, lds_cap, sqrt_d(h), q, out,
                                                  plans[0].use_order, plans[0].pad_len,
-                                                 plans[0].tpr, stream, e0, e1),
+                                                 plans[0].threads, plans[0].tpr, stream, e0, e1),
                               "append + update + attention launch");
         }
         take_events(h, time_it, HEADKV_TIMED_UPDATE, ub, &e0, &e1);

@@ -152,12 +152,12 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
                   int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
                   void* stream, void* ev_start, void* ev_stop);
 // Append + update (Eq. 6 scores) + attention of one layer step in one launch,
-// for attention plans of one kBlock-thread block per head; use_order, pad_len
-// and tpr as in that plan; q, out as in launch_attn.
+// for attention plans of one block per head; use_order, pad_len, threads and
+// tpr as in that plan; q, out as in launch_attn.
 int launch_update_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, int recent_len,
                        int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
-                       const uint16_t* q, float* out, int use_order, int pad_len, int tpr,
-                       void* stream, void* ev_start, void* ev_stop);
+                       const uint16_t* q, float* out, int use_order, int pad_len, int threads,
+                       int tpr, void* stream, void* ev_start, void* ev_stop);
 // Dynamic LDS of one update block (C: prefix rows, with attention-sum scores).
 size_t update_lds_bytes(int N, int cap, int d, int C, bool attn_scores);
 // Dynamic LDS an update block may take: the CU's 160 KB less a margin for the
