@@ -641,15 +641,17 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
     return n_new;
 }
 
-template <int D, bool ATTN_SUM, int G>
-__global__ __launch_bounds__(kBlock) void k_update(LayerDev L, int C, int N, AppendArgs a,
-                                                   const char* src_kv, int relayout,
-                                                   int64_t dense_seg_bytes, int dense_cap,
-                                                   int recent_len, int rs_num, int rs_den, int u,
-                                                   int step, int lds_cap, double sqrt_d) {
-    update_block<D, ATTN_SUM, G>(L, C, N, a, src_kv, relayout, dense_seg_bytes, dense_cap,
-                                 recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d,
-                                 (int)blockIdx.x);
+// NT threads per block: 256 with more heads than CUs (eight blocks per CU),
+// 1024 when each head has a CU to itself.
+template <int D, bool ATTN_SUM, int G, int NT>
+__global__ __launch_bounds__(NT) void k_update(LayerDev L, int C, int N, AppendArgs a,
+                                               const char* src_kv, int relayout,
+                                               int64_t dense_seg_bytes, int dense_cap,
+                                               int recent_len, int rs_num, int rs_den, int u,
+                                               int step, int lds_cap, double sqrt_d) {
+    update_block<D, ATTN_SUM, G, NT>(L, C, N, a, src_kv, relayout, dense_seg_bytes, dense_cap,
+                                     recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d,
+                                     (int)blockIdx.x);
 }
 
 // A step's append, periodic update and attention in one launch, for layers
@@ -737,12 +739,14 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
     // allow the update block more than 64 KB of dynamic LDS (gfx950: 160 KB)
     static const bool lds_ok = [] {
         const int max_lds = 160 * 1024;
-        const void* fns[6] = {reinterpret_cast<const void*>(&k_update<128, false, 1>),
-                              reinterpret_cast<const void*>(&k_update<128, true, 1>),
-                              reinterpret_cast<const void*>(&k_update<128, true, kQueryGroup>),
-                              reinterpret_cast<const void*>(&k_update<64, false, 1>),
-                              reinterpret_cast<const void*>(&k_update<64, true, 1>),
-                              reinterpret_cast<const void*>(&k_update<64, true, kQueryGroup>)};
+        const void* fns[8] = {reinterpret_cast<const void*>(&k_update<128, false, 1, kBlock>),
+                              reinterpret_cast<const void*>(&k_update<128, false, 1, 1024>),
+                              reinterpret_cast<const void*>(&k_update<128, true, 1, kBlock>),
+                              reinterpret_cast<const void*>(&k_update<128, true, kQueryGroup, kBlock>),
+                              reinterpret_cast<const void*>(&k_update<64, false, 1, kBlock>),
+                              reinterpret_cast<const void*>(&k_update<64, false, 1, 1024>),
+                              reinterpret_cast<const void*>(&k_update<64, true, 1, kBlock>),
+                              reinterpret_cast<const void*>(&k_update<64, true, kQueryGroup, kBlock>)};
         bool ok = true;
         for (const void* f : fns)
             ok = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds) ==
@@ -751,18 +755,23 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
         return ok;
     }();
     (void)lds_ok;
-#define HEADKV_UPDATE(D_, A_, G_)                                                                  \
-    hipExtLaunchKernelGGL((k_update<D_, A_, G_>), dim3(s.BH), dim3(kBlock), lds, st, e0, e1, 0, L, \
-                          s.C, s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap, recent_len,    \
-                          rs_num, rs_den, u, step, lds_cap, sqrt_d)
+    // a CU per head: the whole CU's threads on it (the attention-sum variant
+    // keeps 256)
+    const bool wide = !attn && s.BH <= kCus;
+#define HEADKV_UPDATE(D_, A_, G_, NT_)                                                             \
+    hipExtLaunchKernelGGL((k_update<D_, A_, G_, NT_>), dim3(s.BH), dim3(NT_), lds, st, e0, e1, 0,  \
+                          L, s.C, s.N, a, src_kv, relayout, dense_seg_bytes, dense_cap,           \
+                          recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d)
     if (s.d == 128) {
-        if (!attn) HEADKV_UPDATE(128, false, 1);
-        else if (G == kQueryGroup) HEADKV_UPDATE(128, true, kQueryGroup);
-        else HEADKV_UPDATE(128, true, 1);
+        if (wide) HEADKV_UPDATE(128, false, 1, 1024);
+        else if (!attn) HEADKV_UPDATE(128, false, 1, kBlock);
+        else if (G == kQueryGroup) HEADKV_UPDATE(128, true, kQueryGroup, kBlock);
+        else HEADKV_UPDATE(128, true, 1, kBlock);
     } else {
-        if (!attn) HEADKV_UPDATE(64, false, 1);
-        else if (G == kQueryGroup) HEADKV_UPDATE(64, true, kQueryGroup);
-        else HEADKV_UPDATE(64, true, 1);
+        if (wide) HEADKV_UPDATE(64, false, 1, 1024);
+        else if (!attn) HEADKV_UPDATE(64, false, 1, kBlock);
+        else if (G == kQueryGroup) HEADKV_UPDATE(64, true, kQueryGroup, kBlock);
+        else HEADKV_UPDATE(64, true, 1, kBlock);
     }
 #undef HEADKV_UPDATE
     return last_error();
