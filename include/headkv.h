@@ -218,8 +218,11 @@ headkv_status headkv_decode_attn_layers(headkv_t h, int32_t layer_begin, int32_t
 /* One whole decode step of `layer` in the fewest launches: the append of
  * headkv_append_and_evict (with its periodic update when due) followed by the
  * attention of headkv_decode_attn, with identical results.  Without an update
- * the append is fused into the attention kernel.  Arguments as for those two
- * calls.  The grouping step t_g needs the separate calls (HEADKV_ERR_STATE). */
+ * the append is fused into the attention kernel; with one, the append, the
+ * update and the attention run in one launch when the layer's attention takes
+ * one block per head with Eq. (6) scores, else in two.  Arguments as for those
+ * two calls.  The grouping step t_g needs the separate calls
+ * (HEADKV_ERR_STATE). */
 headkv_status headkv_decode_step(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
                                  const uint16_t* k, const uint16_t* v, float* out,
                                  void* stream);
