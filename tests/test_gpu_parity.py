@@ -151,6 +151,23 @@ def test_lumina768_sampled(rho):
     _run_and_check(wl, [0, 31], [(0, 0), (31, 7)], _steps(wl, extra=(127, 1000)))
 
 
+@pytest.mark.parametrize("seed", [7, 2024])
+def test_lumina768_other_data_seeds(seed):
+    # the full Lumina-768 shape on other synthetic draws: one layer, two batch
+    # rows, every head, at the sampled steps (grouping, updates, the end)
+    wl = W.LUMINA768
+    layer = 11
+    steps = _steps(wl, extra=(800, 1600))
+    inp = DeviceInputs(wl, layers=[layer], seed=seed)
+    sess = new_session(wl)
+    res = run_generation(sess, inp, out_steps=steps, snap_steps=steps)
+    torch.cuda.synchronize()
+    for b in (2, 6):
+        ref = oracle.simulate(wl, layer, b, snap_steps=steps, seed=seed)
+        worst, _ = _check_slice(wl, res, layer, b, steps, ref=ref)
+        _say(f"lumina768 seed {seed} layer {layer} b {b}: bit-exact; max err {worst:.2e}")
+
+
 def test_lumina768_separate_calls():
     wl = W.LUMINA768
     _run_and_check(wl, [5], [(5, 3)], _steps(wl), fused=False, all_heads=False)
