@@ -43,6 +43,79 @@ __device__ __forceinline__ Words<NW> nt_load(const uint16_t* p) {
     return w;
 }
 
+// Plain stores can stay in the writing XCD's L2, which another XCD does not
+// see before the kernel ends; agent-scope atomic stores and loads reach the
+// memory every XCD shares, without flushing or invalidating a whole L2.
+__device__ __forceinline__ void agent_store(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float agent_load(const float* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// s_waitcnt with vmcnt(0) only: this wavefront's global loads and stores
+// have completed
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8)); }
+
+// End of a chunk of a chunked launch: the chunks of a head count themselves
+// in L.done[h] once their partials (o, m, l) are out, and the chunk that
+// arrives last merges them -- m = max m_i, o = sum_i o_i 2^(m_i - m) /
+// sum_i l_i 2^(m_i - m) -- writes the head's output, commits the fused
+// append's length (every chunk read n before it counted itself) and clears the
+// counter for the next launch.
+template <int D, bool APPEND>
+__device__ __forceinline__ void chunk_merge(const LayerDev& L, int h, int n,
+                                            float* __restrict__ out,
+                                            const float* __restrict__ part, int tid) {
+    constexpr int PS = D + 2;
+    __shared__ int last;
+    // this wavefront's partial stores are complete before the barrier, so
+    // before the count
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    wait_vmem();
+    __syncthreads();
+    const int i0 = L.item_start[h], i1 = L.item_start[h + 1];
+    if (tid == 0)
+        last = __hip_atomic_fetch_add(L.done + h, 1, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT) == i1 - i0 - 1;
+    __syncthreads();
+    if (!last) return;
+    wait_vmem();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    if (tid < D) {
+        // the partials of up to CB chunks are loaded together (indices past
+        // the head's last chunk re-read it and are skipped), then merged
+        // online
+        constexpr int CB = 4;
+        float m = -INFINITY, num = 0.f, den = 0.f;
+        for (int i = i0; i < i1; i += CB) {
+            float mi[CB], oi[CB], li[CB];
+#pragma unroll
+            for (int k = 0; k < CB; ++k) {
+                const float* pp = part + (size_t)min(i + k, i1 - 1) * PS;
+                mi[k] = agent_load(pp + D);
+                oi[k] = agent_load(pp + tid);
+                li[k] = agent_load(pp + D + 1);
+            }
+#pragma unroll
+            for (int k = 0; k < CB; ++k) {
+                if (i + k < i1 && mi[k] != -INFINITY) {
+                    const float mn = fmaxf(m, mi[k]);
+                    const float fa = __builtin_amdgcn_exp2f(m - mn);  // m = -inf gives 0
+                    const float fb = __builtin_amdgcn_exp2f(mi[k] - mn);
+                    num = num * fa + oi[k] * fb;
+                    den = den * fa + li[k] * fb;
+                    m = mn;
+                }
+            }
+        }
+        out[(size_t)h * D + tid] = num / den;
+    }
+    if (tid == 0) {
+        __hip_atomic_store(L.done + h, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (APPEND) L.n[h] = n + 1;
+    }
+}
+
 // Online-softmax update of one row's state with NT tokens t0 + j * ROWS + row
 // (those at or past t_end masked); k/v hold their d/16 elements of the lane.
 template <int D, int NT, int ROWS>
@@ -220,13 +293,14 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
             out[(size_t)h * D + tid] = o / z;
         } else {
             float* pp = part + (size_t)item * (D + 2);
-            pp[tid] = o;
+            agent_store(pp + tid, o);
             if (tid == 0) {
-                pp[D] = mx;
-                pp[D + 1] = z;
+                agent_store(pp + D, mx);
+                agent_store(pp + D + 1, z);
             }
         }
     }
+    if constexpr (CHUNKED) chunk_merge<D, APPEND>(L, h, n, out, part, tid);
 }
 
 }  // namespace dev

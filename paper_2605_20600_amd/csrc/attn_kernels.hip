@@ -8,8 +8,8 @@
 //            dispatch order (one head group per launch) and may read up to a
 //            padded length with the rows past their own length masked (the
 //            other two strategies of Sec. 5.1 for heads of unequal length).
-//   k_merge  merge of the chunks of every head of a chunked launch, and the
-//            commit of the fused append's length.
+//            In a chunked launch the last chunk of a head to finish merges
+//            the head's chunks.
 //
 // The block itself (rows of d/8 lanes, all loads of a pass issued before
 // use, online softmax, merge through LDS) is attn_block in attn_block.h.
@@ -49,30 +49,6 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
                                         0, qscale, (int)blockIdx.x - layer * BH);
 }
 
-// Merge of the chunks of every head: a kernel of its own, since plain device
-// memory is only coherent across the XCDs' L2 caches at kernel boundaries.
-// With `commit`, the length grows by the token the attention appended.
-template <int D>
-__global__ __launch_bounds__(D) void k_merge(LayerDev L, float* __restrict__ out,
-                                             const float* __restrict__ part, int commit) {
-    constexpr int PS = D + 2;
-    const int h = blockIdx.x, tid = threadIdx.x;
-    const int i0 = L.item_start[h], i1 = L.item_start[h + 1];
-    float mx = -INFINITY;
-    for (int i = i0; i < i1; ++i) mx = fmaxf(mx, part[(size_t)i * PS + D]);
-    float num = 0.f, den = 0.f;
-    for (int i = i0; i < i1; ++i) {
-        const float mi = part[(size_t)i * PS + D];
-        if (mi != -INFINITY) {
-            const float f = __builtin_amdgcn_exp2f(mi - mx);
-            num += f * part[(size_t)i * PS + tid];
-            den += f * part[(size_t)i * PS + D + 1];
-        }
-    }
-    out[(size_t)h * D + tid] = num / den;
-    if (commit && tid == 0) L.n[h] = L.n[h] + 1;
-}
-
 inline int last_error() { return (int)hipGetLastError(); }
 
 template <int D, int T, bool CHUNKED, int TPR>
@@ -90,9 +66,6 @@ void attn_launch(const LayerDev& L, const Shape& s, const AppendArgs& a, const u
         hipExtLaunchKernelGGL((k_attn<D, false, T, CHUNKED, TPR>), grid, block, 0, st, ev0, ev1, 0, L,
                               s.C, a, q, out, partials, p.use_order, p.order_base, p.pad_len,
                               qscale);
-    if (CHUNKED)
-        hipLaunchKernelGGL(k_merge<D>, dim3(s.BH), dim3(D), 0, st, L, out, partials,
-                           a.k != nullptr ? 1 : 0);
 }
 
 template <int D, int T>

@@ -143,6 +143,7 @@ __device__ inline void prefill_head(const LayerDev& L, int h, int nheads, int C,
             L.nstar[h] = 0;
             L.label[h] = 0;
             L.order[h] = h;
+            L.done[h] = 0;
         }
         for (int i = tid; i < d; i += nthreads) L.qsum[(size_t)h * d + i] = 0.0;
     }

@@ -386,7 +386,8 @@ int resident_threads(int heads) {
 // The attention launches of one layer step (appended: the step's token is
 // attended from the input).  Returns their number (1 or 2).
 //  VARLEN, fewer heads than CUs: the layer's chunk table, chunks of one pass
-//    balanced across heads of unequal length, merged by a second kernel.
+//    balanced across heads of unequal length, merged by the last chunk of
+//    each head to finish.
 //  VARLEN otherwise: one block per head over all its passes (no merge, the
 //    append fused), at the largest block size at which every head's block is
 //    resident at once (beyond that 256-thread blocks); longest heads first
@@ -562,7 +563,7 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
                           "attention launch");
     }
     // the append is fused into the attention (its length committed by the
-    // attention block or by the merge kernel)
+    // head's block, or by the last of its chunks to finish)
     take_events(h, time_it, L.grouped ? HEADKV_TIMED_ATTN_APPEND : HEADKV_TIMED_ATTN_APPEND_DENSE,
                 fused_step_bytes(h, L, a.accumulate != 0), &e0, &e1);
     st = hip_status(launch_attention(h, L, D, a, q, out, stream, e0, e1),

@@ -42,7 +42,7 @@ inline size_t segment_bytes(int C, int cap, int d) {
 }
 
 struct MetaLayout {
-    size_t seg_off, cap, n, budget, nstar, label, order, qsum, items, item_start, qring, total;
+    size_t seg_off, cap, n, budget, nstar, label, order, done, qsum, items, item_start, qring, total;
     int max_items, ring_len;
 
     // max_items: largest chunk table of a layer (every head at its largest
@@ -60,6 +60,7 @@ struct MetaLayout {
         nstar = take(sizeof(int32_t) * BH);
         label = take(sizeof(int32_t) * BH);
         order = take(sizeof(int32_t) * BH);
+        done = take(sizeof(int32_t) * BH);
         qsum = take(sizeof(double) * (size_t)BH * d);
         items = take(sizeof(uint32_t) * (size_t)max_items);
         item_start = take(sizeof(int32_t) * ((size_t)BH + 1));
@@ -78,6 +79,8 @@ struct LayerDev {
     int32_t* nstar;       // n* from grouping
     int32_t* label;       // 1 = local head
     int32_t* order;       // attention dispatch order of the heads (longest first)
+    int32_t* done;        // chunks of each head finished in the running chunked
+                          // launch (zero between launches)
     double* qsum;         // [BH][d] running sum of the queries of this window
     // chunk table: entry = head << 8 | chunk, the chunks of a head contiguous;
     // head h owns entries item_start[h] .. item_start[h+1]-1
@@ -103,6 +106,7 @@ inline LayerDev make_layer_dev(void* kv, void* meta, const MetaLayout& m) {
     L.nstar = reinterpret_cast<int32_t*>(b + m.nstar);
     L.label = reinterpret_cast<int32_t*>(b + m.label);
     L.order = reinterpret_cast<int32_t*>(b + m.order);
+    L.done = reinterpret_cast<int32_t*>(b + m.done);
     L.qsum = reinterpret_cast<double*>(b + m.qsum);
     L.items = reinterpret_cast<uint32_t*>(b + m.items);
     L.item_start = reinterpret_cast<int32_t*>(b + m.item_start);
@@ -167,7 +171,8 @@ constexpr size_t kUpdateLdsBudget = 156 * 1024;
 struct AttnPlan {
     int threads;     // 1024, 512 or 256
     int chunked;     // 0: one block per head, every pass; 1: one block per entry
-                     //    of the chunk table (chunks of one pass) + merge kernel
+                     //    of the chunk table (chunks of one pass), merged by
+                     //    the last chunk of each head
     int items;       // entries of the chunk table (chunked)
     int heads;       // blocks of a launch with one block per head
     int use_order;   // one block per head: head = order[order_base + block]
