@@ -11,7 +11,10 @@ seeded, and resident in HBM before timing starts.
 Prints one JSON line.  `value` is visual tokens generated per second over the
 whole job (batch x 2352 per step); `roofline` rates the decode-attention
 kernel (the dominant one) against MI355X's 8 TB/s HBM peak with algorithmic
-bytes; `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
+bytes; `cpu_baseline` times the fp64 CPU oracle on a bounded sample;
+`all_layer_launch` (layouts of 256 to 1024 heads) times, outside the timed
+region, the last step's attention as one launch per layer and as one launch
+for all layers, which shows the per-launch share of the roofline gap.
 """
 from __future__ import annotations
 
@@ -232,23 +235,17 @@ def label_stability(wl, thresholds):
                       "reference_threshold": thresholds[0], "rows": rows}), flush=True)
 
 
-def all_layer_launch(wl, reps: int = 20):
-    """Attention of the last step of a generation, over all layers: one launch
-    per layer (as a decoder runs it) vs one launch for all layers, same
-    results; times from events on the launch stream, per layer."""
-    import numpy as np
+def compare_layer_launches(wl, sess, inp, reps: int = 20):
+    """Attention of the session's last step over all layers: one launch per
+    layer (as a decoder runs it) vs one launch for all layers, same results;
+    times from events on the launch stream, per layer."""
     import torch
     from paper_2605_20600_amd import binding as B
-    from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation_native
-    inp = DeviceInputs(wl)
-    sess = new_session(wl)
     L = wl.layers
-    outs = {l: torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32, device="cuda")
-            for l in range(L)}
-    run_generation_native(sess, inp, outs)
     q = [inp.q[l][wl.num_visual - 1] for l in range(L)]
-    o1 = [torch.empty_like(outs[l]) for l in range(L)]
-    o2 = [torch.empty_like(outs[l]) for l in range(L)]
+    o1 = [torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32, device="cuda")
+          for _ in range(L)]
+    o2 = [torch.empty_like(x) for x in o1]
     st = sess.stream()
 
     def per_layer():
@@ -277,11 +274,26 @@ def all_layer_launch(wl, reps: int = 20):
         _, count = sess.export_retained(l)
         tokens += int(count.sum()) + C * wl.batch * wl.heads
     per_layer_bytes = (tokens * 2 * d * 2 + L * wl.batch * wl.heads * (2 * d + 4 * d)) / L
-    line = {"workload": wl.name + "_shape", "step": wl.num_visual - 1, "layers": L,
-            "alg_bytes_per_layer": per_layer_bytes, "max_abs_diff": same,
-            "per_layer_launch_us": res["per_layer"], "all_layers_launch_us_per_layer": res["all_layers"],
-            "per_layer_launch_gbps": per_layer_bytes / (res["per_layer"] * 1e-6) / 1e9,
-            "all_layers_launch_gbps": per_layer_bytes / (res["all_layers"] * 1e-6) / 1e9}
+    gbps = lambda us: per_layer_bytes / (us * 1e-6) / 1e9
+    return {"step": wl.num_visual - 1, "layers": L, "alg_bytes_per_layer": per_layer_bytes,
+            "max_abs_diff": same,
+            "per_layer_launch_us": res["per_layer"], "per_layer_launch_gbps": gbps(res["per_layer"]),
+            "all_layers_launch_us_per_layer": res["all_layers"],
+            "all_layers_launch_gbps": gbps(res["all_layers"]),
+            "all_layers_launch_frac": gbps(res["all_layers"]) / HBM_PEAK_GBPS}
+
+
+def all_layer_launch(wl):
+    """--all-layer-launch: a fresh session through one generation, then the
+    comparison of compare_layer_launches as one JSON line."""
+    import torch
+    from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation_native
+    inp = DeviceInputs(wl)
+    sess = new_session(wl)
+    outs = {l: torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32, device="cuda")
+            for l in range(wl.layers)}
+    run_generation_native(sess, inp, outs)
+    line = {"workload": wl.name + "_shape", **compare_layer_launches(wl, sess, inp)}
     print(json.dumps(line), flush=True)
 
 
@@ -395,6 +407,16 @@ def main():
               f"{v['share_of_timed_ms']:.1%} of timed kernel time", file=sys.stderr, flush=True)
     print(f"# {dropped} launches untimed", file=sys.stderr, flush=True)
 
+    # outside the timed region: the last step's attention as one launch per
+    # layer and as one launch for all layers (the per-launch cost)
+    layers_cmp = None
+    if (args.method == "headkv" and args.attn_strategy == "varlen"
+            and 256 <= wl.batch * wl.heads <= 1024):
+        layers_cmp = compare_layer_launches(wl, sess, inp)
+        print(f"# last step, per layer: {layers_cmp['per_layer_launch_us']:.2f} us per launch, "
+              f"{layers_cmp['all_layers_launch_us_per_layer']:.2f} us per layer in one launch",
+              file=sys.stderr, flush=True)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, args.cpu_seconds)
@@ -443,6 +465,7 @@ def main():
             "alg_bytes_per_launch": avg_bytes,
         },
         "cpu_baseline": cpu,
+        "all_layer_launch": layers_cmp,
         "kernels": {k.replace("<d", f"<{wl.head_dim}"): v for k, v in kinds.items()},
     }
     print(json.dumps(line), flush=True)
