@@ -186,6 +186,9 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = tid / LPR, col = tid % LPR;
     const Vec qraw = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
+    // the head's segment, capacity and length, read together up front
+    const int64_t seg = L.seg_off[h];
+    const int cap = L.cap[h];
     // n_given: the length as the caller already knows it (a kernel that has
     // just changed it), else the one in memory
     const int n = n_given >= 0 ? n_given : L.n[h];
@@ -196,8 +199,8 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     // the block whose range holds the new token (always the one block of a head
     // that is not chunked) performs the append
     const bool owner = APPEND && (!CHUNKED || (t_begin <= len - 1 && len - 1 < t_end));
-    const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + L.seg_off[h]);
-    const uint16_t* V = K + (size_t)(C + L.cap[h]) * D;
+    const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + seg);
+    const uint16_t* V = K + (size_t)(C + cap) * D;
     // K (or V) row of token `tok`: the step's new token comes from the input
     auto krow = [&](int tok) {
         return (APPEND && tok == len - 1) ? a.k + (size_t)h * D : K + (size_t)tok * D;
@@ -250,20 +253,22 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
         __builtin_amdgcn_sched_barrier(0);
         attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, t_end, qf, m, l, acc);
     }
-    // merge the rows of each wavefront
+    // merge the rows of each wavefront; every exchange of a step is issued
+    // before the first is used (one lane-exchange latency per step, not ten)
 #pragma unroll
     for (int off = LPR; off <= 32; off <<= 1) {
         const float mo = __shfl_xor(m, off);
         const float lo = __shfl_xor(l, off);
+        float ao[VPL];
+#pragma unroll
+        for (int e = 0; e < VPL; ++e) ao[e] = __shfl_xor(acc[e], off);
+        __builtin_amdgcn_sched_barrier(0);
         const float mn = fmaxf(m, mo);
         const float fa = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mn);
         const float fb = (mo == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mo - mn);
         l = l * fa + lo * fb;
 #pragma unroll
-        for (int e = 0; e < VPL; ++e) {
-            const float ao = __shfl_xor(acc[e], off);
-            acc[e] = acc[e] * fa + ao * fb;
-        }
+        for (int e = 0; e < VPL; ++e) acc[e] = acc[e] * fa + ao[e] * fb;
         m = mn;
     }
     __shared__ float sm[WAVES], sl[WAVES];
@@ -279,15 +284,25 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     __syncthreads();  // every wavefront has read n before the append changes it
     if (owner && !CHUNKED) append_commit(L, h, n, tid);
     if (tid < D) {
+        // all LDS reads first: the merge runs on two wavefronts at the very end
+        // of the block, where each serial LDS latency adds to the launch
+        float mw[WAVES], lw[WAVES], xw[WAVES];
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) {
+            mw[w] = sm[w];
+            lw[w] = sl[w];
+            xw[w] = sacc[w][tid];
+        }
+        __builtin_amdgcn_sched_barrier(0);
         float mx = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) mx = fmaxf(mx, sm[w]);
+        for (int w = 0; w < WAVES; ++w) mx = fmaxf(mx, mw[w]);
         float o = 0.f, z = 0.f;
 #pragma unroll
         for (int w = 0; w < WAVES; ++w) {
-            const float f = (sm[w] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sm[w] - mx);
-            o += f * sacc[w][tid];
-            z += f * sl[w];
+            const float f = (mw[w] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mw[w] - mx);
+            o += f * xw[w];
+            z += f * lw[w];
         }
         if (!CHUNKED) {
             out[(size_t)h * D + tid] = o / z;
