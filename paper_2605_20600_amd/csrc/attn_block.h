@@ -8,8 +8,9 @@
 // the first one is used (row indices past the end are clamped to the last
 // token and their logits masked, so no load sits behind a branch), the K rows
 // before the V rows.  K/V are read once per step, so the loads are
-// non-temporal.  The softmax is online per row; rows are merged with
-// cross-lane swaps and the wavefronts through LDS.  With an append, the step's
+// non-temporal.  The softmax is online, with one running max per wavefront:
+// the rows of a wavefront are summed with lane exchanges, and the wavefronts
+// merged through LDS.  With an append, the step's
 // token is attended from the input and written into the cache by the block
 // whose range holds it.
 #pragma once
@@ -118,6 +119,9 @@ __device__ __forceinline__ void chunk_merge(const LayerDev& L, int h, int n,
 
 // Online-softmax update of one row's state with NT tokens t0 + j * ROWS + row
 // (those at or past t_end masked); k/v hold their d/16 elements of the lane.
+// The running max is the wavefront's (the same in all its rows), taken over
+// the logits before the V rows are used, so that the rows of a wavefront
+// merge at the end by plain sums.
 template <int D, int NT, int ROWS>
 __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec (&kk)[NT],
                                                 const typename AttnRegs<D>::Vec (&vv)[NT],
@@ -139,6 +143,8 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
         s[j] = (t0 + j * ROWS + row < t_end) ? dp : -INFINITY;
         mx = fmaxf(mx, s[j]);
     }
+#pragma unroll
+    for (int off = AttnRegs<D>::LPR; off <= 32; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
     if (mx != -INFINITY) {
         const float f = __builtin_amdgcn_exp2f(m - mx);  // m = -inf gives 0
         l *= f;
@@ -253,23 +259,18 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
         __builtin_amdgcn_sched_barrier(0);
         attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, t_end, qf, m, l, acc);
     }
-    // merge the rows of each wavefront; every exchange of a step is issued
-    // before the first is used (one lane-exchange latency per step, not ten)
+    // merge the rows of each wavefront: they share its max, so by sums; every
+    // exchange of a step is issued before the first is used
 #pragma unroll
     for (int off = LPR; off <= 32; off <<= 1) {
-        const float mo = __shfl_xor(m, off);
         const float lo = __shfl_xor(l, off);
         float ao[VPL];
 #pragma unroll
         for (int e = 0; e < VPL; ++e) ao[e] = __shfl_xor(acc[e], off);
         __builtin_amdgcn_sched_barrier(0);
-        const float mn = fmaxf(m, mo);
-        const float fa = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mn);
-        const float fb = (mo == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mo - mn);
-        l = l * fa + lo * fb;
+        l += lo;
 #pragma unroll
-        for (int e = 0; e < VPL; ++e) acc[e] = acc[e] * fa + ao[e] * fb;
-        m = mn;
+        for (int e = 0; e < VPL; ++e) acc[e] += ao[e];
     }
     __shared__ float sm[WAVES], sl[WAVES];
     __shared__ float sacc[WAVES][D];
