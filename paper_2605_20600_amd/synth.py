@@ -124,6 +124,8 @@ def amplitudes(wl: Workload, seed: int = SEED_AMP) -> np.ndarray:
         np.put_along_axis(amp, chosen, np.float32(3.0), axis=-1)
     else:
         raise ValueError(wl.amp_mode)
+    if wl.amp_scale != 1.0:
+        amp *= np.float32(wl.amp_scale)
     return amp
 
 

@@ -49,6 +49,7 @@ class Workload:
     tau: float = 0.9
     cfg_pairs: bool = False    # rows 2i / 2i+1: cond / uncond of one guidance pair
     score_mode: int = 0        # 0: Eq. 6 mean logit; 1: summed window attention weights
+    amp_scale: float = 1.0     # factor on every positional amplitude (larger logits)
 
     @property
     def row_len(self) -> int:          # R, including the row-end token

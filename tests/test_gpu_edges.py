@@ -96,6 +96,23 @@ def test_few_long_heads_split_d64():
     _run(wl, budgets=[[1000, 900]], steps=[0, 300, 599, 600, 601, 800, 1023])
 
 
+def test_large_logits():
+    # amplitudes x4: a planted head's logit for its own position is ~600 nats
+    # (exp overflows fp32 past ~88), so every merge of the softmax -- passes,
+    # rows, wavefronts, chunks -- must rescale to a common max
+    _run(W.TINY.with_(amp_scale=4.0))
+
+
+def test_large_logits_many_heads_several_passes():
+    # the same amplitudes over 320 heads of up to 1056 tokens: one block per
+    # head, more blocks than compute units, up to three passes per block
+    wl = W.TINY.with_(batch=8, heads=40, grid_rows=32, grid_cols=32, period=32,
+                      group_threshold=600, budget_mode=W.BUDGET_OVERRIDE, amp_scale=4.0)
+    rng = np.random.default_rng(11)
+    bud = rng.integers(1, 1025, size=(8, 40))
+    _run(wl, budgets=bud, slices=((0, 0), (0, 7)), steps=[0, 511, 599, 600, 601, 900, 1023])
+
+
 def test_limits_prefix_capacity_and_length():
     # the documented limits at once: a 2048-token prefix, 16384 visual tokens
     # and heads holding HEADKV_MAX_CAPACITY = 4608 visual tokens (budget 4480 +
