@@ -123,11 +123,13 @@ typedef struct headkv_ctx* headkv_t;
  *   dense_kv_bytes: per layer, the cache before grouping (every head holds
  *                   its prefix and up to group_threshold visual tokens);
  *   meta_bytes:     per layer, segment table, lengths, labels, budgets,
- *                   query sums, the attention dispatch order and the
- *                   attention chunk table;
+ *                   query sums, the attention dispatch order, the
+ *                   attention chunk table and its per-head counters of
+ *                   finished chunks (zero between launches);
  *   workspace_bytes: one buffer shared by all layers: attention partials of
  *                   layers with fewer heads than compute units, which cut
- *                   each head into chunks of one pass. */
+ *                   each head into chunks of one pass (the last chunk of a
+ *                   head to finish merges them in the same kernel). */
 headkv_status headkv_plan(const headkv_config* cfg, size_t* dense_kv_bytes,
                           size_t* meta_bytes, size_t* workspace_bytes);
 
