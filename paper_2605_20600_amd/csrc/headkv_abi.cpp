@@ -423,9 +423,14 @@ int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
     // with more than one block per CU, longest heads first (after grouping;
     // before it every head has the same length): the first round of dispatch
     // gives every CU one of the long heads, the second one of the short ones
-    // (Janus, 2 blocks per CU: 13.25 -> 12.42 us)
+    // (Janus, 512 heads, 2 blocks per CU: 13.35 -> 12.28 us; stress, 2048
+    // heads in two rounds: 20,900 -> 24,200 tokens/s).  With more rounds the
+    // dispatcher balances by itself and the order's load sits in front of
+    // every round (LlamaGen shape, 5120 heads in five rounds: 31.2 us sorted,
+    // 30.0 us in head order)
     const int t = resident_threads(BH);
-    const bool by_length = L.grouped ? BH > kCus : BH > attn_resident_blocks(t);
+    const int rounds = (BH + attn_resident_blocks(t) - 1) / attn_resident_blocks(t);
+    const bool by_length = (L.grouped ? BH > kCus : BH > attn_resident_blocks(t)) && rounds <= 2;
     out[0] = whole(t, BH, by_length ? 1 : 0, 0, 0);
     return 1;
 }
