@@ -430,7 +430,7 @@ int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
     // 30.0 us in head order)
     const int t = resident_threads(BH);
     const int rounds = (BH + attn_resident_blocks(t) - 1) / attn_resident_blocks(t);
-    const bool by_length = (L.grouped ? BH > kCus : BH > attn_resident_blocks(t)) && rounds <= 2;
+    const bool by_length = L.grouped && BH > kCus && rounds <= 2;
     out[0] = whole(t, BH, by_length ? 1 : 0, 0, 0);
     return 1;
 }
