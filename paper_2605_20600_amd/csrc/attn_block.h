@@ -10,9 +10,8 @@
 // before the V rows.  K/V are read once per step, so the loads are
 // non-temporal.  The softmax is online, with one running max per wavefront:
 // the rows of a wavefront are summed with lane exchanges, and the wavefronts
-// merged through LDS.  With an append, the step's
-// token is attended from the input and written into the cache by the block
-// whose range holds it.
+// merged through LDS.  With an append, the step's token is attended from the
+// input and written into the cache by the block whose range holds it.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -165,8 +164,9 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
 }
 
 // The work of one attention block; `item` is its index among the blocks of
-// the layer.  TPR tokens per row and pass: 8, or 4 when every head fits in
-// half a pass, or 9 when that gives one pass where 8 would need two.
+// the layer.  TPR tokens per row and pass: 8, or 4 (6) when every head fits
+// in half (three quarters of) a pass, or 9 when that gives one pass where 8
+// would need two.
 template <int D, bool APPEND, int T, bool CHUNKED, int TPR>
 __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const AppendArgs& a,
                                            const uint16_t* __restrict__ q,

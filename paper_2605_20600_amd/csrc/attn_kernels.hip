@@ -78,6 +78,8 @@ void attn_dispatch_t(const LayerDev& L, const Shape& s, const AppendArgs& a, con
         attn_launch<D, T, false, kAttnTpr>(L, s, a, q, out, partials, p, st, ev0, ev1);
     else if (p.tpr == kAttnTprWide)
         attn_launch<D, T, false, kAttnTprWide>(L, s, a, q, out, partials, p, st, ev0, ev1);
+    else if (p.tpr == kAttnTprShort)
+        attn_launch<D, T, false, kAttnTprShort>(L, s, a, q, out, partials, p, st, ev0, ev1);
     else
         attn_launch<D, T, false, kAttnTpr / 2>(L, s, a, q, out, partials, p, st, ev0, ev1);
 }
@@ -106,6 +108,9 @@ void layers_launch(const LayersArg& a, int layers, const MetaLayout& ml, const S
                            qscale);
     else if (tpr == kAttnTprWide)
         hipLaunchKernelGGL((k_attn_layers<D, T, kAttnTprWide>), grid, block, 0, st, a, ml, s.BH,
+                           s.C, qscale);
+    else if (tpr == kAttnTprShort)
+        hipLaunchKernelGGL((k_attn_layers<D, T, kAttnTprShort>), grid, block, 0, st, a, ml, s.BH,
                            s.C, qscale);
     else
         hipLaunchKernelGGL((k_attn_layers<D, T, kAttnTpr / 2>), grid, block, 0, st, a, ml, s.BH,

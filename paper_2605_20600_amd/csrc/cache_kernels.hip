@@ -807,6 +807,10 @@ void update_attn_tpr(const LayerDev& L, const Shape& s, const AppendArgs& a, int
     if (tpr == kAttnTpr)
         update_attn_launch<D, T, kAttnTpr>(L, s, a, recent_len, rs_num, rs_den, u, step, lds_cap,
                                            sqrt_d, q, out, use_order, pad_len, lds, st, e0, e1);
+    else if (tpr == kAttnTprShort)
+        update_attn_launch<D, T, kAttnTprShort>(L, s, a, recent_len, rs_num, rs_den, u, step,
+                                                lds_cap, sqrt_d, q, out, use_order, pad_len, lds,
+                                                st, e0, e1);
     else if (tpr == kAttnTprWide)
         update_attn_launch<D, T, kAttnTprWide>(L, s, a, recent_len, rs_num, rs_den, u, step,
                                                lds_cap, sqrt_d, q, out, use_order, pad_len, lds,

@@ -21,6 +21,9 @@ constexpr int kAttnTpr = 8;  // tokens per 16-lane row per attention pass
 // A wider pass (9 tokens per row, still under 128 VGPRs) for launches whose
 // longest head just misses one pass of 8: one pass instead of two.
 constexpr int kAttnTprWide = 9;
+// Three quarters of a pass, for launches whose longest head fits it: fewer
+// clamped duplicate loads than a pass of 8.
+constexpr int kAttnTprShort = 6;
 constexpr int kCus = 256;    // MI355X compute units
 // Attention blocks have 1024, 512 or 256 threads; 1024 threads of at most 128
 // VGPRs fill a CU, so a CU holds 1024 / threads blocks at once.  A token row
@@ -179,8 +182,9 @@ struct AttnPlan {
     int order_base;
     int pad_len;     // one block per head: read rows up to this length, those
                      // past the head's own length masked (0: none)
-    int tpr;         // tokens per row and pass: kAttnTpr, or half of it (one
-                     // block per head, every head within half a pass)
+    int tpr;         // tokens per row and pass: kAttnTpr, or 3/4 or half of it
+                     // (one block per head, every head within that pass), or
+                     // kAttnTprWide
 };
 // Per-layer pointers of a multi-layer attention launch (up to kMaxLayersPerLaunch).
 constexpr int kMaxLayersPerLaunch = 64;
