@@ -148,7 +148,8 @@ def test_tiny_linear_uniform_budgets():
 @pytest.mark.parametrize("rho", [(1, 8), (1, 6), (1, 4)])
 def test_lumina768_sampled(rho):
     wl = W.LUMINA768.with_(rho=rho)
-    _run_and_check(wl, [0, 31], [(0, 0), (31, 7)], _steps(wl, extra=(127, 1000)))
+    # steps 127 and 200: the full cache in half and three-quarter passes
+    _run_and_check(wl, [0, 31], [(0, 0), (31, 7)], _steps(wl, extra=(127, 200, 1000)))
 
 
 @pytest.mark.parametrize("seed", [7, 2024])
