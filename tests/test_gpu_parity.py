@@ -354,12 +354,14 @@ def test_prefill_attention_then_decode():
         assert np.abs(out[0, h].cpu().double().numpy() - ref).max() <= ATOL
 
 
-def test_decode_attn_layers_matches_per_layer():
-    # one launch for several layers gives the per-layer results
+@pytest.mark.parametrize("t_end", [200, 300 + 2 * 49 + 5])
+def test_decode_attn_layers_matches_per_layer(t_end):
+    # one launch for several layers gives the per-layer results: in the
+    # full-cache phase (heads of 328 tokens, three-quarter passes) and after
+    # two updates
     wl = W.LUMINA768.with_(layers=3)
     inp = DeviceInputs(wl)
     sess = new_session(wl)
-    t_end = wl.group_threshold + 2 * wl.period + 5
     run_generation(sess, inp, steps=t_end)
     t = t_end - 1
     q = [inp.q[l][t] for l in range(3)]
