@@ -201,13 +201,21 @@ def cpu_baseline(wl, seconds_target: float):
         for x, inp in zip(slices[:n_slices], prepared):
             run_slice(*x, inp, pool)
         wall = time.perf_counter() - t0
+    # the same oracle on one thread: the first slice again
+    with ThreadPoolExecutor(max_workers=1) as pool1:
+        t0 = time.perf_counter()
+        run_slice(*slices[0], first, pool1)
+        wall1 = time.perf_counter() - t0
     heads = n_slices * wl.heads
     # a visual token of the workload = one step of all layers x heads of one batch row
     tokens = heads * wl.num_visual / (wl.layers * wl.heads)
+    tokens1 = wl.heads * wl.num_visual / (wl.layers * wl.heads)
     return {"value": tokens / wall, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": (f"{n_slices} (layer, batch row) slices = {heads} heads through grouping, "
                        f"budgets and all {wl.num_visual} steps, fp64, {wall:.2f} s wall on "
-                       f"{threads} threads; scaled to all {wl.layers}x{wl.heads} heads per token")}
+                       f"{threads} threads; scaled to all {wl.layers}x{wl.heads} heads per token"),
+            "single_thread": {"value": tokens1 / wall1, "unit": "tokens/s", "cores": 1,
+                              "sample": f"one slice ({wl.heads} heads), {wall1:.2f} s on one thread"}}
 
 
 def label_stability(wl, thresholds):
