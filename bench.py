@@ -55,8 +55,11 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="approximate CPU work of the oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--timing-every", type=int, default=16,
-                   help="time the attention launch of every n-th step")
+    # every launch timed with events costs a few microseconds of the whole
+    # job's time; 64 is prime to the update periods of the workloads (24, 49,
+    # 65), so the sampled steps still include update steps and full-cache steps
+    p.add_argument("--timing-every", type=int, default=64,
+                   help="time the launches of every n-th step")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 512 MiB device copy five times (calibrates the HBM "
                         "byte counters of a profiler run) and exit")
