@@ -22,13 +22,14 @@ import argparse
 import json
 import os
 import sys
-import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+# the oracle's host threads: at most the GPU machine's CPU share for one GPU
+CPU_THREADS_CAP = 16
 METRIC = "compressed-KV decode attention tokens/s and achieved HBM GB/s (% peak), 768px shape"
 
 
@@ -76,6 +77,13 @@ def parse():
                    help="write the attention kernel's traffic record from four rocprofv3 --pmc "
                         "output folders (kernel FETCH_SIZE, kernel WRITE_SIZE, copy probe "
                         "FETCH_SIZE, copy probe WRITE_SIZE) and exit; no GPU needed")
+    p.add_argument("--kernel-trace-record", metavar="DIR",
+                   help="write the attention kernel's per-phase duration record from a "
+                        "rocprofv3 --kernel-trace output folder of the default run and exit; "
+                        "no GPU needed")
+    p.add_argument("--no-per-config", action="store_true",
+                   help="skip the per_config field (one generation each of Lumina-768 at "
+                        "rho 1/6 and 1/4, Janus-Pro-7B, Lumina-1024 and the stress shape)")
     p.add_argument("--traffic-kernel", default="k_attn<128, true, 1024, false, 8>",
                    help="kernel name the traffic record is taken for")
     return p.parse_args()
@@ -160,6 +168,93 @@ def write_traffic_record(dirs, kernel: str):
     print(json.dumps(rec))
 
 
+KTRACE_RECORD = os.path.join(ROOT, "profiles", "k_attn_lumina768_b8_rho1-8_rocprof.json")
+
+
+def write_kernel_trace_record(run_dir: str, layers: int = 32):
+    """Per-phase durations of the decode kernels from the kernel_trace.csv of
+    a rocprofv3 --kernel-trace run of this benchmark's default workload.  The
+    dispatches are taken in start order: a prefill attention starts a
+    generation in the full-cache phase, and the grouping step's `layers`-th
+    head scoring starts its compressed phase.  The fused append + attention
+    launches of each phase, and the update steps' append + update + attention
+    launches, are summarised separately; the attention launches of the grouping
+    step itself and of the after-run comparisons (no append) are left out.
+    Written to profiles/ with the attention sources' SHA-256."""
+    import csv
+    import glob
+    import re
+    import statistics
+    files = glob.glob(os.path.join(run_dir, "**", "*kernel_trace.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no kernel_trace.csv under {run_dir}")
+    rows = []
+    with open(files[0]) as fh:
+        for r in csv.DictReader(fh):
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"]))
+    rows.sort()
+    attn = re.compile(r"k_attn<(\d+), (true|false), (\d+), (true|false), (\d+)>")
+    buckets = {"compressed_fused": [], "full_cache_fused": [], "update_attn": []}
+    spans = {}
+    phase, scores = None, 0
+    for t0, t1, name in rows:
+        if "k_prefill_attn" in name:
+            phase, scores = "full_cache", 0
+            continue
+        if "k_score" in name:
+            scores += 1
+            if scores == layers:
+                phase = "compressed"
+            continue
+        m = attn.search(name)
+        key = None
+        if m and m.group(2) == "true" and phase is not None:
+            key = phase + "_fused"
+        elif "k_update_attn<" in name and phase == "compressed":
+            key = "update_attn"
+        if key is None:
+            continue
+        buckets[key].append((t0, t1))
+        if key != "full_cache_fused":
+            lo, hi, n = spans.get(phase, (t0, t1, 0))
+            spans[phase] = (min(lo, t0), max(hi, t1), n + 1)
+    rec = {"workload": "lumina_mgpt_768_shape b8 rho=1/8 (bench.py default)",
+           "attn_source_sha256": attn_source_sha256(), "layers": layers,
+           "trace": os.path.basename(files[0])}
+    for key, v in buckets.items():
+        d = [t1 - t0 for t0, t1 in v]
+        rec[key] = None if not d else {
+            "calls": len(d), "avg_ns": statistics.mean(d), "median_ns": statistics.median(d),
+            "min_ns": min(d), "max_ns": max(d)}
+    if "compressed" in spans:
+        lo, hi, n = spans["compressed"]
+        busy = sum(t1 - t0 for k in ("compressed_fused", "update_attn") for t0, t1 in buckets[k])
+        rec["compressed_phase"] = {"launches": n, "span_ns": hi - lo,
+                                   "kernel_ns": busy, "gap_ns_per_launch": (hi - lo - busy) / n}
+    with open(KTRACE_RECORD, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps(rec))
+
+
+def rocprof_roofline(alg_bytes: float):
+    """The headline kernel's profiler-measured fraction of the HBM peak: the
+    compressed phase's average fused-launch duration from the committed
+    kernel-trace record, if that was taken with the current kernel sources."""
+    try:
+        rec = json.load(open(KTRACE_RECORD))
+    except OSError:
+        return {"frac_rocprof": None}
+    c = rec.get("compressed_fused")
+    if rec.get("attn_source_sha256") != attn_source_sha256() or not c:
+        return {"frac_rocprof": None,
+                "rocprof_note": "kernel-trace record taken with other attention sources"}
+    us = c["avg_ns"] * 1e-3
+    return {"frac_rocprof": alg_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS,
+            "avg_launch_us_rocprof": us, "launches_rocprof": c["calls"],
+            "rocprof_record": os.path.relpath(KTRACE_RECORD, ROOT)}
+
+
 def cpu_baseline(wl, seconds_target: float):
     """The fp64 oracle through grouping, budgets and whole generations of
     sampled (layer, batch row) slices, one head per host thread (the C code
@@ -169,7 +264,7 @@ def cpu_baseline(wl, seconds_target: float):
     import oracle
     from paper_2605_20600_amd import synth
 
-    threads = min(16, os.cpu_count() or 1)
+    threads = min(CPU_THREADS_CAP, os.cpu_count() or 1)
     t_g = wl.group_threshold - 1
     ov = synth.budget_override(wl)
 
@@ -214,6 +309,7 @@ def cpu_baseline(wl, seconds_target: float):
     tokens = heads * wl.num_visual / (wl.layers * wl.heads)
     tokens1 = wl.heads * wl.num_visual / (wl.layers * wl.heads)
     return {"value": tokens / wall, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "threads_cap": CPU_THREADS_CAP, "cpu_count": os.cpu_count(),
             "sample": (f"{n_slices} (layer, batch row) slices = {heads} heads through grouping, "
                        f"budgets and all {wl.num_visual} steps, fp64, {wall:.2f} s wall on "
                        f"{threads} threads; scaled to all {wl.layers}x{wl.heads} heads per token"),
@@ -308,6 +404,141 @@ def all_layer_launch(wl):
     print(json.dumps(line), flush=True)
 
 
+KIND_NAMES = ["k_attn<d, append> (headkv_decode_step, compressed cache)",
+              "k_attn<d> (after an update)",
+              "k_update<d> (append + periodic update)",
+              "k_prefill_attn<d> (prefix store + causal attention, headkv_prefill_attn)",
+              "k_attn<d, append> (headkv_decode_step, full cache before grouping)",
+              "k_update_attn<d> (append + periodic update + attention, one launch)"]
+
+
+def launches_per_generation(wl, fused_update: bool):
+    """Launches of each timed kind in one generation (all layers): the
+    library times only every n-th step's launches, so the kinds' shares of a
+    generation's kernel time are their average durations times these counts."""
+    t_g, P, N, L = wl.group_threshold - 1, wl.period, wl.num_visual, wl.layers
+    upd = sum(1 for t in range(t_g + 1, N) if (t - t_g) % P == 0)
+    comp = (N - 1 - t_g) - upd
+    return {0: comp * L, 1: 0 if fused_update else upd * L, 2: 0 if fused_update else upd * L,
+            3: L if wl.prefix_len > 0 else 0, 4: t_g * L, 5: upd * L if fused_update else 0}
+
+
+def run_workload(wl, args, steps: int, warmup: int, labels_mode: str = "headkv",
+                 strategy: str = "varlen", compare_launches: bool = False, say=print):
+    """Whole generations of one workload with the step loop in the library:
+    warm-up, then `steps` timed generations.  Returns the per-kind kernel
+    statistics, the whole-job rate and (optionally) the per-layer vs
+    all-layer launch comparison."""
+    import torch
+    from paper_2605_20600_amd import binding as B
+    from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation_native
+    t0 = time.perf_counter()
+    inp = DeviceInputs(wl)
+    torch.cuda.synchronize()
+    say(f"# {wl.name} inputs: {inp.nbytes() / 1e9:.2f} GB on device in "
+        f"{time.perf_counter() - t0:.1f} s")
+    labels = None
+    if labels_mode == "full":
+        for l in inp.layers:
+            inp.override[l] = torch.full((wl.batch * wl.heads,), wl.num_visual, dtype=torch.int32,
+                                         device="cuda")
+    elif labels_mode == "uniform":
+        labels = {l: torch.zeros(wl.batch * wl.heads, dtype=torch.uint8, device="cuda")
+                  for l in inp.layers}
+    sess = new_session(wl, attn_strategy=B.ATTN_STRATEGIES[strategy])
+    outs = {l: torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32, device="cuda")
+            for l in inp.layers}
+    pre_out = {l: torch.empty((wl.batch, wl.heads, wl.prefix_len, wl.head_dim),
+                              dtype=torch.float32, device="cuda") for l in inp.layers}
+    for i in range(warmup):
+        run_generation_native(sess, inp, outs, label_override=labels, prefill_out=pre_out)
+        torch.cuda.synchronize()
+        say(f"# {wl.name} warmup {i + 1}/{warmup} done")
+    # timed region: whole generations, the step loop in the library.  Every
+    # `timing_every`-th step's launches are timed with HIP events that take
+    # the kernel's own start and end timestamps (every prefill launch too)
+    per_gen = ((wl.num_visual + args.timing_every - 1) // args.timing_every * 2 + 1) * wl.layers
+    B.headkv_timing_reserve(sess.h, per_gen * steps)
+    B.headkv_timing_collect(sess.h)              # discard warm-up records
+    torch.cuda.synchronize()
+    # events between the generations, on the stream they run on, give each
+    # generation's own time
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    t_start = time.perf_counter()
+    marks[0].record()
+    for i in range(steps):
+        run_generation_native(sess, inp, outs, timing_every=args.timing_every,
+                              label_override=labels, prefill_out=pre_out)
+        marks[i + 1].record()
+        say(f"# {wl.name} step {i + 1}/{steps} issued")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(steps)]
+    per_kind, dropped = B.headkv_timing_collect(sess.h)
+    fused_update = per_kind[5][1] > 0
+    counts = launches_per_generation(wl, fused_update)
+    kinds = {}
+    for k, (name, (kms, kn, kb)) in enumerate(zip(KIND_NAMES, per_kind)):
+        if kn:
+            avg_us = kms / kn * 1e3
+            kinds[name] = {"launches_timed": kn, "avg_us": avg_us, "alg_bytes_per_launch": kb / kn,
+                           "achieved_gbps": kb / kn / (avg_us * 1e-6) / 1e9,
+                           "launches_per_generation": counts[k],
+                           "est_ms_per_generation": avg_us * counts[k] * 1e-3}
+    C, d = wl.prefix_len, wl.head_dim
+    if KIND_NAMES[3] in kinds:
+        k = kinds[KIND_NAMES[3]]
+        k["causal_flops_per_launch"] = wl.batch * wl.heads * 4 * d * C * (C + 1) / 2
+        k["achieved_tflops"] = k["causal_flops_per_launch"] / (k["avg_us"] * 1e-6) / 1e12
+    total = sum(v["est_ms_per_generation"] for v in kinds.values())
+    for v in kinds.values():
+        v["share_of_generation_kernel_time"] = v["est_ms_per_generation"] / total
+    dominant = max(kinds, key=lambda k: kinds[k]["est_ms_per_generation"])
+    for k, v in kinds.items():
+        say(f"# {wl.name} {k}: {v['launches_timed']} timed launches, avg {v['avg_us']:.2f} us, "
+            f"{v['alg_bytes_per_launch'] / 1e6:.2f} MB algorithmic -> {v['achieved_gbps']:.0f} GB/s, "
+            f"~{v['share_of_generation_kernel_time']:.1%} of a generation's kernel time")
+    layers_cmp = None
+    if compare_launches and 256 <= wl.batch * wl.heads <= 1024:
+        layers_cmp = compare_layer_launches(wl, sess, inp)
+        say(f"# last step, per layer: {layers_cmp['per_layer_launch_us']:.2f} us per launch, "
+            f"{layers_cmp['all_layers_launch_us_per_layer']:.2f} us per layer in one launch")
+    res = {"tokens_per_s": wl.batch * wl.num_visual * steps / elapsed,
+           "elapsed_s": elapsed, "step_ms": step_ms, "kinds": kinds, "dominant": dominant,
+           "dropped": dropped, "layers_cmp": layers_cmp}
+    sess.close()
+    del inp, outs, pre_out, sess
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+# workloads of the per_config field: the other budget ratios of the headline
+# shape and the other shapes, one warm-up and one timed generation each
+PER_CONFIG = (("lumina_mgpt_768", (1, 6)), ("lumina_mgpt_768", (1, 4)), ("janus_pro_7b", None),
+              ("lumina_mgpt_1024", None), ("stress_768_b64_p1", None))
+
+
+def per_config(args, say):
+    from paper_2605_20600_amd import workloads as W
+    out = []
+    for name, rho in PER_CONFIG:
+        wl = W.ALL[name] if rho is None else W.ALL[name].with_(rho=rho)
+        r = run_workload(wl, args, steps=1, warmup=1, say=say)
+        dom = r["kinds"][r["dominant"]]
+        out.append({"workload": wl.name + "_shape", "batch": wl.batch,
+                    "rho": f"{wl.rho[0]}/{wl.rho[1]}",
+                    "budget_mode": ["paper", "override", "layer_total"][wl.budget_mode],
+                    "tokens_per_s": r["tokens_per_s"], "ms_per_generation": r["step_ms"][0],
+                    "kernel": r["dominant"].replace("<d", f"<{wl.head_dim}"),
+                    "avg_launch_us": dom["avg_us"], "alg_bytes_per_launch": dom["alg_bytes_per_launch"],
+                    "achieved_gbps": dom["achieved_gbps"],
+                    "frac": dom["achieved_gbps"] / HBM_PEAK_GBPS,
+                    "launches_timed": dom["launches_timed"]})
+        say(f"# per_config {out[-1]}")
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -316,6 +547,9 @@ def main():
         sys.exit(2)
     if args.traffic_record:
         write_traffic_record(args.traffic_record, args.traffic_kernel)
+        return
+    if args.kernel_trace_record:
+        write_kernel_trace_record(args.kernel_trace_record)
         return
     import torch
     if args.copy_probe:
@@ -328,8 +562,8 @@ def main():
         return
     from paper_2605_20600_amd import workloads as W
     from paper_2605_20600_amd import binding as B
-    from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation_native
 
+    say = lambda m: print(m, file=sys.stderr, flush=True)
     wl = W.ALL[args.workload]
     if args.label_stability:
         label_stability(wl, [int(x) for x in args.label_stability.split(",")])
@@ -344,110 +578,51 @@ def main():
     if args.score_mode == "attn_sum":
         wl = wl.with_(score_mode=B.HEADKV_SCORE_ATTN_SUM)
     rho_s = f"{wl.rho[0]}/{wl.rho[1]}"
-    dev = torch.cuda.current_device()
-    torch.cuda.set_device(dev)
-    t0 = time.perf_counter()
-    inp = DeviceInputs(wl)
-    torch.cuda.synchronize()
-    print(f"# inputs: {inp.nbytes() / 1e9:.2f} GB on device in {time.perf_counter() - t0:.1f} s",
-          file=sys.stderr, flush=True)
-    labels = None
-    if args.method == "full":
-        for l in inp.layers:
-            inp.override[l] = torch.full((wl.batch * wl.heads,), wl.num_visual, dtype=torch.int32,
-                                         device="cuda")
-    elif args.method == "uniform":
-        labels = {l: torch.zeros(wl.batch * wl.heads, dtype=torch.uint8, device="cuda")
-                  for l in inp.layers}
-    sess = new_session(wl, attn_strategy=B.ATTN_STRATEGIES[args.attn_strategy])
-    outs = {l: torch.empty((wl.batch, wl.heads, wl.head_dim), dtype=torch.float32, device="cuda")
-            for l in inp.layers}
-    pre_out = {l: torch.empty((wl.batch, wl.heads, wl.prefix_len, wl.head_dim),
-                              dtype=torch.float32, device="cuda") for l in inp.layers}
-
-    for i in range(args.warmup):
-        run_generation_native(sess, inp, outs, label_override=labels, prefill_out=pre_out)
-        torch.cuda.synchronize()
-        print(f"# warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
-
-    # timed region: K whole generations, the step loop in the library.  Every
-    # `timing_every`-th step's fused append + attention launch (one kernel) is
-    # timed with HIP events that take the kernel's own start and end.
-    per_gen = ((wl.num_visual + args.timing_every - 1) // args.timing_every * 2 + 1) * wl.layers
-    B.headkv_timing_reserve(sess.h, per_gen * args.steps)
-    B.headkv_timing_collect(sess.h)              # discard warm-up records
-    torch.cuda.synchronize()
-    # events between the generations, on the stream they run on, give each
-    # generation's own time (the median is reported beside the whole-job rate)
-    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t_start = time.perf_counter()
-    marks[0].record()
-    for i in range(args.steps):
-        run_generation_native(sess, inp, outs, timing_every=args.timing_every,
-                              label_override=labels, prefill_out=pre_out)
-        marks[i + 1].record()
-        print(f"# step {i + 1}/{args.steps} issued", file=sys.stderr, flush=True)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    step_ms = [marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps)]
-    per_kind, dropped = B.headkv_timing_collect(sess.h)
-    C, d = wl.prefix_len, wl.head_dim
-    pre_flops = wl.batch * wl.heads * 4 * d * C * (C + 1) / 2  # causal QK^T and PV
-    names = ["k_attn<d, append> (headkv_decode_step, compressed cache)",
-             "k_attn<d> (after an update)",
-             "k_update<d> (append + periodic update)",
-             "k_prefill_attn<d> (prefix store + causal attention, headkv_prefill_attn)",
-             "k_attn<d, append> (headkv_decode_step, full cache before grouping)",
-             "k_update_attn<d> (append + periodic update + attention, one launch)"]
-    kinds = {}
-    for name, (kms, kn, kb) in zip(names, per_kind):
-        if kn:
-            kinds[name] = {"launches": kn, "avg_us": kms / kn * 1e3, "alg_bytes_per_launch": kb / kn,
-                           "achieved_gbps": kb / kn / (kms / kn * 1e-3) / 1e9,
-                           "share_of_timed_ms": kms}
-    if names[3] in kinds:
-        k = kinds[names[3]]
-        k["causal_flops_per_launch"] = pre_flops
-        k["achieved_tflops"] = pre_flops / (k["avg_us"] * 1e-6) / 1e12
-    total_ms = sum(v["share_of_timed_ms"] for v in kinds.values())
-    for v in kinds.values():
-        v["share_of_timed_ms"] = v["share_of_timed_ms"] / total_ms
-    dominant = max(kinds, key=lambda k: kinds[k]["share_of_timed_ms"])
+    torch.cuda.set_device(torch.cuda.current_device())
+    headline = (wl.name == "lumina_mgpt_768" and rho_s == "1/8" and args.method == "headkv"
+                and args.attn_strategy == "varlen" and args.score_mode == "mean_logit")
+    r = run_workload(wl, args, args.steps, args.warmup, labels_mode=args.method,
+                     strategy=args.attn_strategy,
+                     compare_launches=args.method == "headkv" and args.attn_strategy == "varlen",
+                     say=say)
+    print(f"# {r['dropped']} launches untimed", file=sys.stderr, flush=True)
+    kinds, dominant = r["kinds"], r["dominant"]
     dom = kinds[dominant]
-    avg_us, avg_bytes, n_launch = dom["avg_us"], dom["alg_bytes_per_launch"], dom["launches"]
     achieved = dom["achieved_gbps"]
-    tokens = wl.batch * wl.num_visual * args.steps
-    ms_per_step = elapsed / args.steps * 1e3
-    for k, v in kinds.items():
-        print(f"# {k}: {v['launches']} timed launches, avg {v['avg_us']:.2f} us, "
-              f"{v['alg_bytes_per_launch'] / 1e6:.2f} MB algorithmic -> {v['achieved_gbps']:.0f} GB/s, "
-              f"{v['share_of_timed_ms']:.1%} of timed kernel time", file=sys.stderr, flush=True)
-    print(f"# {dropped} launches untimed", file=sys.stderr, flush=True)
 
-    # outside the timed region: the last step's attention as one launch per
-    # layer and as one launch for all layers (the per-launch cost)
-    layers_cmp = None
-    if (args.method == "headkv" and args.attn_strategy == "varlen"
-            and 256 <= wl.batch * wl.heads <= 1024):
-        layers_cmp = compare_layer_launches(wl, sess, inp)
-        print(f"# last step, per layer: {layers_cmp['per_layer_launch_us']:.2f} us per launch, "
-              f"{layers_cmp['all_layers_launch_us_per_layer']:.2f} us per layer in one launch",
-              file=sys.stderr, flush=True)
-
+    cfgs = None
+    if headline and not args.no_per_config:
+        cfgs = per_config(args, say)
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, args.cpu_seconds)
 
+    roof = {
+        "bound": "hbm",
+        "achieved": achieved,
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": achieved / HBM_PEAK_GBPS,
+        "traffic": (measured_traffic() if headline and dominant == KIND_NAMES[0] else None),
+        "kernel": dominant.replace("<d", f"<{wl.head_dim}"),
+        "frac_events": achieved / HBM_PEAK_GBPS,
+        "timed_every_nth_step": args.timing_every,
+        "launches": dom["launches_timed"],
+        "avg_launch_us": dom["avg_us"],
+        "alg_bytes_per_launch": dom["alg_bytes_per_launch"],
+    }
+    if headline and dominant == KIND_NAMES[0]:
+        roof.update(rocprof_roofline(dom["alg_bytes_per_launch"]))
     line = {
         "metric": METRIC,
-        "value": tokens / elapsed,
+        "value": r["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "ms_per_step_each": step_ms,
-        "ms_per_step_median": sorted(step_ms)[len(step_ms) // 2],
+        "ms_per_step": r["elapsed_s"] / args.steps * 1e3,
+        "ms_per_step_each": r["step_ms"],
+        "ms_per_step_median": sorted(r["step_ms"])[len(r["step_ms"]) // 2],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -468,23 +643,10 @@ def main():
             "group_threshold": wl.group_threshold, "recent_window": wl.recent_len,
             "kv_storage": "bf16", "accumulate": "fp32 (attention), fp64 (grouping, eviction)",
         },
-        "roofline": {
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": (measured_traffic() if wl.name == "lumina_mgpt_768" and rho_s == "1/8"
-                        and args.method == "headkv" and args.attn_strategy == "varlen"
-                        and dominant == names[0] else None),
-            "kernel": dominant.replace("<d", f"<{wl.head_dim}"),
-            "timed_every_nth_step": args.timing_every,
-            "launches": n_launch,
-            "avg_launch_us": avg_us,
-            "alg_bytes_per_launch": avg_bytes,
-        },
+        "roofline": roof,
         "cpu_baseline": cpu,
-        "all_layer_launch": layers_cmp,
+        "per_config": cfgs,
+        "all_layer_launch": r["layers_cmp"],
         "kernels": {k.replace("<d", f"<{wl.head_dim}"): v for k, v in kinds.items()},
     }
     print(json.dumps(line), flush=True)

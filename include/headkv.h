@@ -163,6 +163,7 @@ headkv_status headkv_prefill_attn(headkv_t h, int32_t layer, const uint16_t* q_c
  * (Eqs. 2-6): each local head keeps its newest `budget` visual tokens; each
  * global head keeps its recent window and evicts from its history the
  * lowest-scored tokens of the long-range and near-range parts, M/2 each.
+ * q, k and v must be 16-byte aligned (HEADKV_ERR_INVALID_ARG otherwise).
  * Steps must be consecutive from 0.  A step past t_g before grouping is
  * HEADKV_ERR_STATE. */
 headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step,
@@ -175,7 +176,7 @@ headkv_status headkv_append_and_evict(headkv_t h, int32_t layer, int32_t step,
  * accumulated backward from the newest token; n* is the smallest count whose
  * mass reaches tau, and the head is local iff n* < local_window.
  * Writes n_star ([B][H] int32, device) and is_local ([B][H] uint8, device,
- * 1 = local). */
+ * 1 = local).  q must be 16-byte aligned. */
 headkv_status headkv_score_heads(headkv_t h, int32_t layer, const uint16_t* q,
                                  int32_t* n_star, uint8_t* is_local, void* stream);
 
@@ -188,12 +189,19 @@ headkv_status headkv_score_heads(headkv_t h, int32_t layer, const uint16_t* q,
  * recent window included and the prefix not counted.
  * Each head then needs prefix_len + min(budget + period, N) slots (with
  * HEADKV_ATTN_PADDED, the largest of these for every head of the layer); the
- * total, with alignment, is written to *ragged_bytes_needed.  If ragged_kv is NULL
- * or ragged_bytes is smaller, the call returns HEADKV_ERR_CAPACITY after
- * setting *ragged_bytes_needed and changes no state: allocate and call again.
- * Otherwise the first update runs (Eqs. 2-6), the retained tokens are copied
- * into ragged_kv (device, caller-owned from now on), and the dense buffer of
- * this layer is no longer used.  Waits for `stream` once. */
+ * total, with alignment, is written to *ragged_bytes_needed.  Both calls of the
+ * two-call pattern first run the budget kernel, which writes `budgets` and the
+ * layer's device copy of the labels and budgets, and wait for `stream` to read
+ * the budgets back.  If ragged_kv is NULL or ragged_bytes is smaller, the call
+ * then returns HEADKV_ERR_CAPACITY after setting *ragged_bytes_needed: the
+ * layer stays in its dense layout, nothing else has changed, and a second call
+ * with a large enough buffer (the same labels give the same budgets) completes
+ * the grouping.  Otherwise the first update runs (Eqs. 2-6), the retained
+ * tokens are copied into ragged_kv (device, 256-byte aligned, caller-owned from
+ * now on), and the dense buffer of this layer is no longer used.  If a HIP
+ * call fails after the budgets were read back (HEADKV_ERR_HIP), the layer's
+ * metadata may be half-way to the new layout: every later call on the layer
+ * returns HEADKV_ERR_STATE until headkv_prefill runs again. */
 headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is_local,
                                     const int32_t* budget_override, int32_t* budgets,
                                     void* ragged_kv, size_t ragged_bytes,
@@ -202,7 +210,8 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
 /* Decode attention, Eq. (1), of the current step for every (b, h) of
  * `layer`: o = softmax(q K^T / sqrt(d)) V over the prefix and the head's
  * retained visual tokens (the current token included).  q: [B][H][d] bf16,
- * out: [B][H][d] fp32, both device.  bf16 storage, fp32 accumulation. */
+ * out: [B][H][d] fp32, both device and 16-byte aligned.  bf16 storage, fp32
+ * accumulation. */
 headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q,
                                  float* out, void* stream);
 
@@ -235,7 +244,8 @@ headkv_status headkv_decode_step(headkv_t h, int32_t layer, int32_t step, const 
 /* Runs headkv_decode_step for steps [step_begin, step_end) of every layer,
  * step by step and layer by layer, from one host call.  q, k, v: host arrays
  * of num_layers device pointers, each to [steps][B][H][d] bf16 with
- * step_stride elements between consecutive steps; out: host array of
+ * step_stride elements between consecutive steps (a multiple of 8, so that
+ * every step's rows stay 16-byte aligned); out: host array of
  * num_layers device pointers to [B][H][d] fp32, overwritten every step.
  * timing_every > 0: every step t with t % timing_every == 0 whose attention is
  * one kernel launch is timed with the kernel's own start/end timestamps (see

@@ -157,12 +157,15 @@ def run_head(q, k, v, kc, vc, t_g: int, P: int, is_local: bool, budget: int,
 
 def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
              want_out: bool = True, snap_steps: Sequence[int] = (),
-             seed: Optional[int] = None, label_override=None, budget_override=None) -> Dict:
+             seed: Optional[int] = None, label_override=None, budget_override=None,
+             inputs: Optional[Dict] = None) -> Dict:
     """The whole compressed decode of one (layer, b) slice of a workload.
 
     Grouping runs for every head of the slice (budgets of the layer-total mode
     depend on all labels), then each requested head is run through the
-    generation.  Inputs come from the shared seeded generator.  With
+    generation.  Inputs come from the shared seeded generator, or from
+    `inputs` ({h: (q, k, v, kc, vc)} CPU tensors of every head of the slice,
+    for tests that plant values the generator does not draw).  With
     wl.cfg_pairs the row's budgets and update policies follow the labels of
     its pair's conditional row (b rounded down to even); "labels" and
     "n_star" stay the row's own grouping result."""
@@ -171,13 +174,15 @@ def simulate(wl, layer: int, b: int, heads: Optional[List[int]] = None,
     H = wl.heads
     heads = list(range(H)) if heads is None else list(heads)
     t_g = wl.group_threshold - 1
-    inputs = {}
     labels = np.zeros(H, np.int32)
     n_star = np.zeros(H, np.int32)
     margins = np.zeros(H, np.float64)
     mass = np.zeros(H, np.float64)
+    given = inputs
+    inputs = {}
     for h in range(H):
-        q, k, v, kc, vc = synth.head_inputs(wl, layer, b, h, **kw)
+        q, k, v, kc, vc = (synth.head_inputs(wl, layer, b, h, **kw) if given is None
+                           else given[h])
         inputs[h] = (q, k, v, kc, vc)
         K = torch.cat([kc, k[: t_g + 1]], dim=0)
         g = group_head(q[t_g], K, wl.tau, wl.local_window)

@@ -1,4 +1,6 @@
-"""Builds libheadkv.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree."""
+"""Builds libheadkv.so (HIP kernels + C ABI) for gfx950 with hipcc, in-tree,
+and the measurement tool stream_probe (launch floor and streaming ceiling at
+the attention kernel's launch shape; not part of the library)."""
 from __future__ import annotations
 
 import os
@@ -10,6 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libheadkv.so")
+PROBE = os.path.join(HERE, "stream_probe")
 SOURCES = ["cache_kernels.hip", "attn_kernels.hip", "prefill_attn.hip", "headkv_abi.cpp"]
 
 HIPCC_FLAGS = [
@@ -45,6 +48,12 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    tmp = PROBE + f".tmp{os.getpid()}"
+    cmd = [hipcc(), *HIPCC_FLAGS, os.path.join(CSRC, "stream_probe.hip"), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, PROBE)
     return LIB
 
 

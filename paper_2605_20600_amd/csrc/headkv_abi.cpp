@@ -343,6 +343,9 @@ headkv_status prepare_append(headkv_t h, int32_t layer, int32_t step, const uint
     headkv_status st = check_layer(h, layer);
     if (st) return st;
     if (!q || !k || !v) return fail(HEADKV_ERR_INVALID_ARG, "q / k / v is NULL");
+    // the kernels read q, k and v rows with 16-byte vector loads
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16))
+        return fail(HEADKV_ERR_INVALID_ARG, "q / k / v not 16-byte aligned");
     Layer& L = h->layers[layer];
     const headkv_config& c = h->cfg;
     if (!L.prefilled) return fail(HEADKV_ERR_STATE, "append before prefill");
@@ -543,12 +546,13 @@ double update_bytes(headkv_t h, const Layer& L) {
 headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const uint16_t* q,
                                const uint16_t* k, const uint16_t* v, float* out, void* stream,
                                bool time_it) {
+    if (!out) return fail(HEADKV_ERR_INVALID_ARG, "out is NULL");
+    if (!aligned(out, 16)) return fail(HEADKV_ERR_INVALID_ARG, "out not 16-byte aligned");
     AppendArgs a;
     bool update = false;
     int u = 0;
     headkv_status st = prepare_append(h, layer, step, q, k, v, &a, &update, &u);
     if (st) return st;
-    if (!out) return fail(HEADKV_ERR_INVALID_ARG, "out is NULL");
     Layer& L = h->layers[layer];
     const headkv_config& c = h->cfg;
     if (!L.grouped && step == h->t_g)
@@ -610,6 +614,9 @@ headkv_status headkv_run_steps(headkv_t h, int32_t step_begin, int32_t step_end,
     if (!q || !k || !v || !out) return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer array");
     if (step_begin < 0 || step_end < step_begin || step_stride < 0 || timing_every < 0)
         return fail(HEADKV_ERR_INVALID_ARG, "bad step range, stride or timing interval");
+    // every step's rows must keep the 16-byte alignment of the first
+    if ((step_stride * (int64_t)sizeof(uint16_t)) % 16 != 0)
+        return fail(HEADKV_ERR_INVALID_ARG, "step_stride is not a multiple of 8 elements");
     const int NL = h->cfg.num_layers;
     for (int t = step_begin; t < step_end; ++t) {
         const bool time_it = timing_every > 0 && t % timing_every == 0;
@@ -672,6 +679,7 @@ headkv_status headkv_score_heads(headkv_t h, int32_t layer, const uint16_t* q, i
     headkv_status st = check_layer(h, layer);
     if (st) return st;
     if (!q || !n_star || !is_local) return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer");
+    if (!aligned(q, 16)) return fail(HEADKV_ERR_INVALID_ARG, "q not 16-byte aligned");
     Layer& L = h->layers[layer];
     if (!L.prefilled || L.grouped || L.last_step != h->t_g)
         return fail(HEADKV_ERR_STATE, "score_heads runs once, right after the append of step group_threshold - 1");
@@ -782,8 +790,13 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
                         "relayout launch");
     }
     headkv_status st_wait = hip_status(hipStreamSynchronize(s), "stream wait");
-    if (st) return st;
-    if (st_wait) return st_wait;
+    if (st || st_wait) {
+        // the metadata may already describe the per-head segments while the
+        // move into them did not run: nothing may use this layer until it is
+        // prefilled again
+        L.prefilled = false;
+        return fail(st ? st : st_wait, g_err + " (the layer must be prefilled again)");
+    }
     L.ragged = ragged_kv;
     L.grouped = true;
     L.budget.assign(bud.begin(), bud.end());
@@ -801,6 +814,8 @@ headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, f
     headkv_status st = check_layer(h, layer);
     if (st) return st;
     if (!q || !out) return fail(HEADKV_ERR_INVALID_ARG, "q / out is NULL");
+    if (!aligned(q, 16) || !aligned(out, 16))
+        return fail(HEADKV_ERR_INVALID_ARG, "q / out not 16-byte aligned");
     Layer& L = h->layers[layer];
     if (!L.prefilled || L.last_step < 0) return fail(HEADKV_ERR_STATE, "decode_attn before the first append");
     if (!L.grouped && L.last_step == h->t_g)
@@ -822,11 +837,15 @@ headkv_status headkv_decode_attn_layers(headkv_t h, int32_t layer_begin, int32_t
     const int BH = h->shape.BH;
     if (BH < kCus || h->cfg.attn_strategy != HEADKV_ATTN_VARLEN)
         return fail(HEADKV_ERR_UNSUPPORTED, "multi-layer attention needs >= 256 heads and the varlen strategy");
+    for (int i = 0; i < n; ++i) {
+        if (!q[i] || !out[i]) return fail(HEADKV_ERR_INVALID_ARG, "NULL layer pointer");
+        if (!aligned(q[i], 16) || !aligned(out[i], 16))
+            return fail(HEADKV_ERR_INVALID_ARG, "q / out not 16-byte aligned");
+    }
     LayersArg args{};
     int len_max = 0;
     for (int i = 0; i < n; ++i) {
         Layer& L = h->layers[layer_begin + i];
-        if (!q[i] || !out[i]) return fail(HEADKV_ERR_INVALID_ARG, "NULL layer pointer");
         if (!L.prefilled || L.last_step < 0)
             return fail(HEADKV_ERR_STATE, "decode_attn before the first append");
         if (!L.grouped && L.last_step == h->t_g)

@@ -127,6 +127,40 @@ def test_bad_arguments_are_rejected():
         B.headkv_destroy(h)
 
 
+def test_misaligned_vectors_are_rejected():
+    # the kernels read q, k, v rows and write outputs with 16-byte vector
+    # accesses: every per-step vector must be 16-byte aligned
+    h, cfg = _handle()
+    try:
+        I = B.HEADKV_ERR_INVALID_ARG
+        assert _status("headkv_append_and_evict", h, 0, 0, FAKE + 2, FAKE, FAKE, None) == I
+        assert _status("headkv_append_and_evict", h, 0, 0, FAKE, FAKE + 8, FAKE, None) == I
+        assert _status("headkv_append_and_evict", h, 0, 0, FAKE, FAKE, FAKE + 4, None) == I
+        assert _status("headkv_decode_step", h, 0, 0, FAKE, FAKE, FAKE, FAKE + 4, None) == I
+        assert _status("headkv_decode_step", h, 0, 0, FAKE + 2, FAKE, FAKE, FAKE, None) == I
+        assert _status("headkv_decode_attn", h, 0, FAKE + 2, FAKE, None) == I
+        assert _status("headkv_decode_attn", h, 0, FAKE, FAKE + 4, None) == I
+        assert _status("headkv_score_heads", h, 0, FAKE + 2, FAKE, FAKE, None) == I
+        arr = (ctypes.c_void_p * 1)(FAKE)
+        # a step stride of 3 elements would misalign every other step's rows
+        assert _status("headkv_run_steps", h, 0, 1, arr, arr, arr, 3, arr, 0, None) == I
+        bad = (ctypes.c_void_p * 1)(FAKE + 2)
+        assert _status("headkv_run_steps", h, 0, 1, bad, arr, arr, 256, arr, 0, None) == I
+        # aligned arguments get past the checks to the call-order error
+        assert _status("headkv_decode_attn", h, 0, FAKE, FAKE, None) == B.HEADKV_ERR_STATE
+    finally:
+        B.headkv_destroy(h)
+    wl = W.LUMINA768.with_(layers=2)
+    h = B.headkv_create(make_config(wl), [FAKE] * 2, [FAKE + 4096] * 2, FAKE)
+    try:
+        ok = (ctypes.c_void_p * 2)(FAKE, FAKE)
+        bad = (ctypes.c_void_p * 2)(FAKE, FAKE + 4)
+        assert _status("headkv_decode_attn_layers", h, 0, 2, ok, bad, None) == \
+            B.HEADKV_ERR_INVALID_ARG
+    finally:
+        B.headkv_destroy(h)
+
+
 def test_override_mode_requires_budgets():
     wl = W.TINY.with_(budget_mode=W.BUDGET_OVERRIDE)
     h, cfg = _handle(wl)

@@ -8,6 +8,7 @@ import torch
 import oracle
 from paper_2605_20600_amd import binding as B, synth, workloads as W
 from paper_2605_20600_amd.runner import DeviceInputs, new_session, run_generation
+from parity_report import assert_same_retained
 
 pytestmark = pytest.mark.gpu
 ATOL = 2e-2
@@ -31,11 +32,12 @@ def _run(wl, layer=0, slices=((0, 0),), budgets=None, fused=True, steps=None, **
         assert np.array_equal(res["is_local"][layer][sl].cpu().numpy(), ref["labels"])
         assert np.array_equal(res["n_star"][layer][sl].cpu().numpy(), ref["n_star"])
         assert np.array_equal(res["budgets"][layer][sl].cpu().numpy(), ref["budgets"])
+        masks = [res["snap"][(t, layer)][0][sl].cpu().numpy() for t in steps]
+        assert_same_retained(steps, masks, ref, range(H), wl.period, wl.group_threshold - 1,
+                             f"{wl.name} b {b}:")
         for i, t in enumerate(steps):
-            mask = res["snap"][(t, layer)][0][sl].cpu().numpy()
             out = res["out"][(t, layer)][b].cpu().double().numpy()
             for h in range(H):
-                assert np.array_equal(mask[h], ref["snaps"][h][i]), (b, h, t)
                 err = float(np.abs(out[h] - ref["out"][h][t]).max())
                 worst = max(worst, err)
                 assert err <= ATOL, (b, h, t, err)
