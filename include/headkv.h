@@ -134,7 +134,11 @@ headkv_status headkv_plan(const headkv_config* cfg, size_t* dense_kv_bytes,
                           size_t* meta_bytes, size_t* workspace_bytes);
 
 /* Creates a host handle.  dense_kv, meta: host arrays of num_layers device
- * pointers; workspace: one device pointer.  No device work is done. */
+ * pointers; workspace: one device pointer, or NULL for a handle whose callers
+ * cannot allocate: a call whose attention would need the workspace (a layer
+ * with fewer batch x heads than compute units) then returns HEADKV_ERR_STATE,
+ * and headkv_decode_attn_noalloc runs that attention instead.  No device
+ * work is done. */
 headkv_status headkv_create(const headkv_config* cfg, void* const* dense_kv,
                             void* const* meta, void* workspace, headkv_t* out);
 
@@ -214,6 +218,21 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
  * accumulation. */
 headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q,
                                  float* out, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * attention of headkv_decode_attn, same arguments and results, with no
+ * workspace.  A layer with fewer (batch x heads) than compute units splits
+ * each head into chunks whose partial results headkv_decode_attn keeps in the
+ * handle's workspace; this call keeps them in a static device array of
+ * 4 MiB that the library holds on each GPU it runs on until the process ends
+ * (HEADKV_ERR_CAPACITY if a layer's chunks need more: entries x (head_dim + 2)
+ * x 4 bytes).  It calls no hipMalloc, hipFree or allocating routine.  Every
+ * call on one GPU shares that GPU's array (the current device's), so calls
+ * that overlap on one GPU, on any streams or handles, race; calls ordered on
+ * one stream do not. */
+headkv_status headkv_decode_attn_noalloc(headkv_t h, int32_t layer, const uint16_t* q,
+                                         float* out, void* stream);
 
 /* Decode attention of layers [layer_begin, layer_end) in one launch, with the
  * results of headkv_decode_attn on each.  q, out: host arrays (indexed by

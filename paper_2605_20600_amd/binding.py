@@ -47,7 +47,8 @@ ATTN_STRATEGIES = {"varlen": HEADKV_ATTN_VARLEN, "padded": HEADKV_ATTN_PADDED,
 EXPORTED = (
     "headkv_plan", "headkv_create", "headkv_destroy", "headkv_prefill", "headkv_prefill_attn",
     "headkv_append_and_evict", "headkv_score_heads", "headkv_assign_budgets",
-    "headkv_decode_attn", "headkv_decode_attn_layers", "headkv_decode_step",
+    "headkv_decode_attn", "headkv_decode_attn_noalloc", "headkv_decode_attn_layers",
+    "headkv_decode_step",
     "headkv_export_retained",
     "headkv_run_steps", "headkv_timing_reserve", "headkv_timing_collect",
     "headkv_last_error",
@@ -98,6 +99,7 @@ def load() -> ctypes.CDLL:
         "headkv_score_heads": [P, I, P, P, P, P],
         "headkv_assign_budgets": [P, I, P, P, P, P, Z, ctypes.POINTER(Z), P],
         "headkv_decode_attn": [P, I, P, P, P],
+        "headkv_decode_attn_noalloc": [P, I, P, P, P],
         "headkv_decode_step": [P, I, I, P, P, P, P, P],
         "headkv_decode_attn_layers": [P, I, I, P, P, P],
         "headkv_export_retained": [P, I, P, P, P],
@@ -184,6 +186,11 @@ def headkv_assign_budgets(h: int, layer: int, is_local: int, budget_override: Op
 
 def headkv_decode_attn(h: int, layer: int, q: int, out: int, stream: int = 0) -> None:
     _check(load().headkv_decode_attn(h, layer, q, out, stream), "headkv_decode_attn")
+
+
+def headkv_decode_attn_noalloc(h: int, layer: int, q: int, out: int, stream: int = 0) -> None:
+    _check(load().headkv_decode_attn_noalloc(h, layer, q, out, stream),
+           "headkv_decode_attn_noalloc")
 
 
 def headkv_decode_attn_layers(h: int, layer_begin: int, layer_end: int, q: Sequence[int],

@@ -13,7 +13,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libheadkv.so")
 PROBE = os.path.join(HERE, "stream_probe")
-SOURCES = ["cache_kernels.hip", "attn_kernels.hip", "prefill_attn.hip", "headkv_abi.cpp"]
+SOURCES = ["cache_kernels.hip", "attn_kernels.hip", "prefill_attn.hip", "scratch.hip",
+           "headkv_abi.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra",

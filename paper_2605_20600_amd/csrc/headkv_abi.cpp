@@ -17,6 +17,7 @@
 
 #include "../../include/headkv.h"
 #include "layout.h"
+#include "scratch.h"
 
 using namespace headkv;
 
@@ -234,8 +235,11 @@ headkv_status headkv_create(const headkv_config* cfg, void* const* dense_kv, voi
                             void* workspace, headkv_t* out) {
     headkv_status st = validate_config(cfg);
     if (st) return st;
-    if (!dense_kv || !meta || !workspace || !out) return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer");
-    if (!aligned(workspace, 256)) return fail(HEADKV_ERR_INVALID_ARG, "workspace not 256-byte aligned");
+    if (!dense_kv || !meta || !out) return fail(HEADKV_ERR_INVALID_ARG, "NULL pointer");
+    // a NULL workspace is allowed: chunked attention then needs the
+    // allocation-free entry point
+    if (workspace && !aligned(workspace, 256))
+        return fail(HEADKV_ERR_INVALID_ARG, "workspace not 256-byte aligned");
     for (int l = 0; l < cfg->num_layers; ++l) {
         if (!dense_kv[l] || !meta[l]) return fail(HEADKV_ERR_INVALID_ARG, "NULL layer buffer");
         if (!aligned(dense_kv[l], 256) || !aligned(meta[l], 256))
@@ -453,19 +457,26 @@ int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
     return 1;
 }
 
-// Launches the attention of a layer step; the event pair brackets the first
-// kernel's start and the last kernel's end.
-int launch_attention(headkv_t h, const Layer& L, const LayerDev& D, const AppendArgs& a,
-                     const uint16_t* q, float* out, void* stream, void* e0, void* e1) {
+// Launches the attention of a layer step with the split-K partials of chunked
+// plans in `partials` (the handle's workspace, or the allocation-free entry
+// point's scratch); the event pair brackets the first kernel's start and the
+// last kernel's end.
+headkv_status launch_attention(headkv_t h, const Layer& L, const LayerDev& D, const AppendArgs& a,
+                               const uint16_t* q, float* out, float* partials, void* stream,
+                               void* e0, void* e1, const char* what) {
     AttnPlan plans[2];
     const int np = attn_plans(h, L, a.k != nullptr, plans);
-    float* ws = static_cast<float*>(h->ws);
+    for (int i = 0; i < np; ++i)
+        if (plans[i].chunked && partials == nullptr)
+            return fail(HEADKV_ERR_STATE,
+                        "the handle has no workspace and this layer's attention is split into "
+                        "chunks: use headkv_decode_attn_noalloc");
     for (int i = 0; i < np; ++i) {
-        const int e = launch_attn(D, h->shape, a, q, out, ws, plans[i], stream, i == 0 ? e0 : nullptr,
-                                  i == np - 1 ? e1 : nullptr);
-        if (e) return e;
+        const int e = launch_attn(D, h->shape, a, q, out, partials, plans[i], stream,
+                                  i == 0 ? e0 : nullptr, i == np - 1 ? e1 : nullptr);
+        if (e) return hip_status(e, what);
     }
-    return 0;
+    return ok();
 }
 
 }  // namespace
@@ -583,15 +594,15 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
                         "append + update launch");
         if (st) return st;
         take_events(h, time_it, HEADKV_TIMED_ATTN, attn_bytes(h, L), &e0, &e1);
-        return hip_status(launch_attention(h, L, D, none, q, out, stream, e0, e1),
-                          "attention launch");
+        return launch_attention(h, L, D, none, q, out, static_cast<float*>(h->ws), stream, e0, e1,
+                                "attention launch");
     }
     // the append is fused into the attention (its length committed by the
     // head's block, or by the last of its chunks to finish)
     take_events(h, time_it, L.grouped ? HEADKV_TIMED_ATTN_APPEND : HEADKV_TIMED_ATTN_APPEND_DENSE,
                 fused_step_bytes(h, L, a.accumulate != 0), &e0, &e1);
-    st = hip_status(launch_attention(h, L, D, a, q, out, stream, e0, e1),
-                    "append + attention launch");
+    st = launch_attention(h, L, D, a, q, out, static_cast<float*>(h->ws), stream, e0, e1,
+                          "append + attention launch");
     if (st) return st;
     commit_append(h, L, step, update);
     return ok();
@@ -809,8 +820,11 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     return ok();
 }
 
-headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, float* out,
-                                 void* stream) {
+}  // extern "C"
+
+namespace {
+
+headkv_status check_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, float* out) {
     headkv_status st = check_layer(h, layer);
     if (st) return st;
     if (!q || !out) return fail(HEADKV_ERR_INVALID_ARG, "q / out is NULL");
@@ -820,9 +834,49 @@ headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, f
     if (!L.prefilled || L.last_step < 0) return fail(HEADKV_ERR_STATE, "decode_attn before the first append");
     if (!L.grouped && L.last_step == h->t_g)
         return fail(HEADKV_ERR_STATE, "assign_budgets must run before attention at step group_threshold - 1");
+    return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, float* out,
+                                 void* stream) {
+    headkv_status st = check_decode_attn(h, layer, q, out);
+    if (st) return st;
+    const Layer& L = h->layers[layer];
     AppendArgs none{};
-    return hip_status(launch_attention(h, L, dev_of(h, L), none, q, out, stream, nullptr, nullptr),
-                      "attention launch");
+    return launch_attention(h, L, dev_of(h, L), none, q, out, static_cast<float*>(h->ws), stream,
+                            nullptr, nullptr, "attention launch");
+}
+
+headkv_status headkv_decode_attn_noalloc(headkv_t h, int32_t layer, const uint16_t* q, float* out,
+                                         void* stream) {
+    headkv_status st = check_decode_attn(h, layer, q, out);
+    if (st) return st;
+    const Layer& L = h->layers[layer];
+    AttnPlan plans[2];
+    const int np = attn_plans(h, L, false, plans);
+    bool chunked = false;
+    for (int i = 0; i < np; ++i) {
+        if (!plans[i].chunked) continue;
+        chunked = true;
+        const size_t need = (size_t)plans[i].items * (h->cfg.head_dim + 2) * sizeof(float);
+        if (need > kScratchBytes)
+            return fail(HEADKV_ERR_CAPACITY, "the layer's chunked attention needs " +
+                                                 std::to_string(need) + " bytes of partials, more "
+                                                 "than the " + std::to_string(kScratchBytes) +
+                                                 "-byte scratch: use headkv_decode_attn");
+    }
+    void* scratch = nullptr;
+    if (chunked) {
+        st = hip_status(scratch_address(&scratch), "scratch address");
+        if (st) return st;
+    }
+    AppendArgs none{};
+    return launch_attention(h, L, dev_of(h, L), none, q, out, static_cast<float*>(scratch), stream,
+                            nullptr, nullptr, "attention launch");
 }
 
 headkv_status headkv_decode_attn_layers(headkv_t h, int32_t layer_begin, int32_t layer_end,

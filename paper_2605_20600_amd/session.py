@@ -38,7 +38,9 @@ class Session:
     """Owns the device buffers of one handle (dense per-layer caches, metadata,
     workspace, and the per-head segment buffers allocated at grouping)."""
 
-    def __init__(self, cfg: B.HeadKVConfig, device: str = "cuda"):
+    def __init__(self, cfg: B.HeadKVConfig, device: str = "cuda", workspace: bool = True):
+        """workspace=False creates the handle without a workspace (chunked
+        attention then goes through headkv_decode_attn_noalloc)."""
         self.cfg = cfg
         self.device = device
         dense_b, meta_b, ws_b = B.headkv_plan(cfg)
@@ -47,10 +49,12 @@ class Session:
                                           for _ in range(L)]
         self.meta: List[torch.Tensor] = [torch.zeros(meta_b, dtype=torch.uint8, device=device)
                                          for _ in range(L)]
-        self.ws = torch.empty(max(ws_b, 256), dtype=torch.uint8, device=device)
+        self.ws = (torch.empty(max(ws_b, 256), dtype=torch.uint8, device=device) if workspace
+                   else None)
         self.ragged: List[Optional[torch.Tensor]] = [None] * L
         self.h = B.headkv_create(cfg, [t.data_ptr() for t in self.dense],
-                                 [t.data_ptr() for t in self.meta], self.ws.data_ptr())
+                                 [t.data_ptr() for t in self.meta],
+                                 None if self.ws is None else self.ws.data_ptr())
         BH = cfg.batch * cfg.num_heads
         self.n_star = [torch.zeros(BH, dtype=torch.int32, device=device) for _ in range(L)]
         self.is_local = [torch.zeros(BH, dtype=torch.uint8, device=device) for _ in range(L)]
@@ -113,6 +117,12 @@ class Session:
         if out is None:
             out = torch.empty(q.shape, dtype=torch.float32, device=self.device)
         B.headkv_decode_attn(self.h, layer, q.data_ptr(), out.data_ptr(), self.stream())
+        return out
+
+    def decode_attn_noalloc(self, layer: int, q, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=self.device)
+        B.headkv_decode_attn_noalloc(self.h, layer, q.data_ptr(), out.data_ptr(), self.stream())
         return out
 
     def decode_step(self, layer: int, step: int, q, k, v,
