@@ -123,7 +123,8 @@ typedef struct headkv_ctx* headkv_t;
  *   dense_kv_bytes: per layer, the cache before grouping (every head holds
  *                   its prefix and up to group_threshold visual tokens);
  *   meta_bytes:     per layer, segment table, lengths, labels, budgets,
- *                   query sums, the attention dispatch order, the
+ *                   the last `period` queries of every head (the window an
+ *                   update scores against), the attention dispatch order, the
  *                   attention chunk table and its per-head counters of
  *                   finished chunks (zero between launches);
  *   workspace_bytes: one buffer shared by all layers: attention partials of
@@ -161,8 +162,8 @@ headkv_status headkv_prefill_attn(headkv_t h, int32_t layer, const uint16_t* q_c
                                   void* stream);
 
 /* Cache append K <- [K, k_t], V <- [V, v_t] (Sec. 3, KV Cache) for visual
- * step `step` of `layer`; q, k, v: [B][H][d] bf16, device.  q_t is added to
- * the head's sum of the past-P queries (Eq. 6).  When the layer is grouped and
+ * step `step` of `layer`; q, k, v: [B][H][d] bf16, device.  q_t joins the
+ * head's window of the past-P queries (Eq. 6).  When the layer is grouped and
  * (step - t_g) is a positive multiple of P, the periodic update follows
  * (Eqs. 2-6): each local head keeps its newest `budget` visual tokens; each
  * global head keeps its recent window and evicts from its history the

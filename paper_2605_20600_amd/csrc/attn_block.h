@@ -11,7 +11,8 @@
 // non-temporal.  The softmax is online, with one running max per wavefront:
 // the rows of a wavefront are summed with lane exchanges, and the wavefronts
 // merged through LDS.  With an append, the step's token is attended from the
-// input and written into the cache by the block whose range holds it.
+// input by wavefront 0 of the block whose range holds it (as the first token
+// of its online softmax), which also writes it into the cache.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -59,12 +60,10 @@ __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0 | (0x
 // End of a chunk of a chunked launch: the chunks of a head count themselves
 // in L.done[h] once their partials (o, m, l) are out, and the chunk that
 // arrives last merges them -- m = max m_i, o = sum_i o_i 2^(m_i - m) /
-// sum_i l_i 2^(m_i - m) -- writes the head's output, commits the fused
-// append's length (every chunk read n before it counted itself) and clears the
-// counter for the next launch.
-template <int D, bool APPEND>
-__device__ __forceinline__ void chunk_merge(const LayerDev& L, int h, int n,
-                                            float* __restrict__ out,
+// sum_i l_i 2^(m_i - m) -- writes the head's output and clears the counter
+// for the next launch.
+template <int D>
+__device__ __forceinline__ void chunk_merge(const LayerDev& L, int h, float* __restrict__ out,
                                             const float* __restrict__ part, int tid) {
     constexpr int PS = D + 2;
     __shared__ int last;
@@ -110,10 +109,7 @@ __device__ __forceinline__ void chunk_merge(const LayerDev& L, int h, int n,
         }
         out[(size_t)h * D + tid] = num / den;
     }
-    if (tid == 0) {
-        __hip_atomic_store(L.done + h, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (APPEND) L.n[h] = n + 1;
-    }
+    if (tid == 0) __hip_atomic_store(L.done + h, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Online-softmax update of one row's state with NT tokens t0 + j * ROWS + row
@@ -191,73 +187,122 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = tid / LPR, col = tid % LPR;
-    const Vec qraw = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
     // the head's segment, capacity and length, read together up front
     const int64_t seg = L.seg_off[h];
     const int cap = L.cap[h];
     // n_given: the length as the caller already knows it (a kernel that has
     // just changed it), else the one in memory
-    const int n = n_given >= 0 ? n_given : L.n[h];
-    const int len = C + n + (APPEND ? 1 : 0);
+    const int n = n_given >= 0 ? n_given : head_len(L, h);
+    // Everything the first K/V load waits for comes in two rounds of scalar
+    // loads: the kernel arguments, then the metadata with the rest of them.
+    // Left to itself, the compiler fetches arguments late, each behind the
+    // previous wait (up to four rounds); an empty asm statement that takes
+    // these values pins them before any load that follows.  (Placed before the
+    // metadata loads, it would make them vector loads.)
+    asm volatile("" ::"s"(q), "s"(seg), "s"(cap), "s"(n), "s"(C), "s"(pad_len), "s"(qscale));
+    if (APPEND) asm volatile("" ::"s"(a.k), "s"(a.v), "s"(L.qring), "s"(L.ring_len));
+    const Vec qraw = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
+    // the cache holds len_c tokens; with the append, the step's token is
+    // attended as token len_c, from the input
+    const int len_c = C + n;
+    const int len = len_c + (APPEND ? 1 : 0);
     const int t_end = CHUNKED ? min(len, t_begin + TP) : len;
-    // padding strategy: rows up to pad_len are read, those past len masked
-    const int t_stop = CHUNKED ? t_end : max(len, pad_len);
+    // cache rows this block streams: [t_begin, s_end); the padding strategy
+    // reads the rows of the layer's longest head (pad_len attended tokens, the
+    // appended one included, which comes from the input), those past s_end
+    // masked
+    const int s_end = min(t_end, len_c);
+    const int s_stop = CHUNKED ? s_end : max(s_end, pad_len - (APPEND ? 1 : 0));
     // the block whose range holds the new token (always the one block of a head
-    // that is not chunked) performs the append
-    const bool owner = APPEND && (!CHUNKED || (t_begin <= len - 1 && len - 1 < t_end));
-    const uint16_t* K = reinterpret_cast<const uint16_t*>(L.kv + seg);
-    const uint16_t* V = K + (size_t)(C + cap) * D;
-    // K (or V) row of token `tok`: the step's new token comes from the input
-    auto krow = [&](int tok) {
-        return (APPEND && tok == len - 1) ? a.k + (size_t)h * D : K + (size_t)tok * D;
-    };
-    auto vrow = [&](int tok) {
-        return (APPEND && tok == len - 1) ? a.v + (size_t)h * D : V + (size_t)tok * D;
-    };
+    // that is not chunked) performs the append; its wavefront 0 attends the
+    // token and moves its K/V row.  The head's length is not stored: the host
+    // counts the appended tokens
+    const bool owner = APPEND && (!CHUNKED || (t_begin <= len_c && len_c < t_end));
+    const bool newtok = owner && wave == 0;
+    uint16_t* K = reinterpret_cast<uint16_t*>(L.kv + seg);
+    uint16_t* V = K + (size_t)(C + cap) * D;
 
-    // the append's loads go out before the K/V stream and its stores right
-    // after (the attention reads the new token from the input, never from row
-    // C+n); n itself changes once no block reads it
-    AppendVals av;
-    if (owner) av = append_load(L, D, h, a, tid);
+    // the append's loads (the new token's K/V row, by wavefront 0) go out
+    // before the K/V stream and its stores right after it
+    Vec kn, vn;
+    if (newtok) {
+        kn = *reinterpret_cast<const Vec*>(a.k + (size_t)h * D + col * VPL);
+        vn = *reinterpret_cast<const Vec*>(a.v + (size_t)h * D + col * VPL);
+    }
     float m = -INFINITY, l = 0.f;
     float acc[VPL];
 #pragma unroll
     for (int e = 0; e < VPL; ++e) acc[e] = 0.f;
     float qf[VPL];
-    // first pass: the append's store and q's conversion go between its loads
-    // and their first use
-    if (t_begin < t_stop) {  // a chunk past the head's length reads nothing
-        Vec kk[TPR], vv[TPR];
-        // all K rows of the pass, then all V rows: the logits and their max
-        // are computed while the V rows are still arriving
-#pragma unroll
-        for (int j = 0; j < TPR; ++j)
-            kk[j] = nt_load<NW>(krow(min(t_begin + j * ROWS + row, t_stop - 1)) + col * VPL);
-#pragma unroll
-        for (int j = 0; j < TPR; ++j)
-            vv[j] = nt_load<NW>(vrow(min(t_begin + j * ROWS + row, t_stop - 1)) + col * VPL);
-        // keep every load of the pass ahead of its first use
-        __builtin_amdgcn_sched_barrier(0);
-        if (owner) append_store(L, C, D, h, n, a, av, tid);
+    // q in fp32, pre-scaled; then the append's stores, and the new token as the
+    // first token of the softmax: every row of wavefront 0 holds its K/V row,
+    // so each computes its logit and takes it as the starting max; row 0
+    // counts it and writes its K/V row, its position and q's row of the query
+    // ring
+    auto begin = [&]() {
+        // an opaque copy of q, so that its conversion (common to both
+        // branches below) is not hoisted in front of the K/V loads, where it
+        // would wait for q
+        Vec qv = qraw;
+        static_assert(NW == 4, "four words per lane");
+        asm volatile("" : "+v"(qv.w[0]), "+v"(qv.w[1]), "+v"(qv.w[2]), "+v"(qv.w[3]));
 #pragma unroll
         for (int e = 0; e < NW; ++e) {
-            qf[2 * e] = bf_lo(qraw.w[e]) * qscale;
-            qf[2 * e + 1] = bf_hi(qraw.w[e]) * qscale;
+            qf[2 * e] = bf_lo(qv.w[e]) * qscale;
+            qf[2 * e + 1] = bf_hi(qv.w[e]) * qscale;
         }
-        attn_accumulate<D, TPR, ROWS>(kk, vv, t_begin, row, t_end, qf, m, l, acc);
+        if (newtok) {
+            float dp = 0.f;
+#pragma unroll
+            for (int e = 0; e < NW; ++e) {
+                dp += qf[2 * e] * bf_lo(kn.w[e]);
+                dp += qf[2 * e + 1] * bf_hi(kn.w[e]);
+            }
+            m = lanes_sum<LPR>(dp);
+            if (row == 0) {
+                *reinterpret_cast<Vec*>(K + (size_t)len_c * D + col * VPL) = kn;
+                *reinterpret_cast<Vec*>(V + (size_t)len_c * D + col * VPL) = vn;
+                *reinterpret_cast<Vec*>(ring_slot(L, D, h, a.step) + col * VPL) = qraw;
+                if (col == 0) reinterpret_cast<int32_t*>(V + (size_t)(C + cap) * D)[n] = a.step;
+                l = 1.f;
+#pragma unroll
+                for (int e = 0; e < NW; ++e) {
+                    acc[2 * e] = bf_lo(vn.w[e]);
+                    acc[2 * e + 1] = bf_hi(vn.w[e]);
+                }
+            }
+        }
+    };
+    // first pass, straight-line code from its loads to its use (a join in
+    // between would make the compiler wait for every load at it): all K rows,
+    // then all V rows, so that the logits and their max are computed while the
+    // V rows are still arriving.  A chunk past the head's cached length reads
+    // nothing.
+    Vec kk[TPR], vv[TPR];
+    if (t_begin < s_stop) {
+#pragma unroll
+        for (int j = 0; j < TPR; ++j)
+            kk[j] = nt_load<NW>(K + (size_t)min(t_begin + j * ROWS + row, s_stop - 1) * D + col * VPL);
+#pragma unroll
+        for (int j = 0; j < TPR; ++j)
+            vv[j] = nt_load<NW>(V + (size_t)min(t_begin + j * ROWS + row, s_stop - 1) * D + col * VPL);
+        // keep every load of the pass ahead of its first use
+        __builtin_amdgcn_sched_barrier(0);
+        begin();
+        attn_accumulate<D, TPR, ROWS>(kk, vv, t_begin, row, s_end, qf, m, l, acc);
+    } else {
+        begin();
     }
     // further passes of a head longer than one pass
-    for (int t0 = t_begin + TP; t0 < t_stop; t0 += TP) {
-        Vec kk[TPR], vv[TPR];
+    for (int t0 = t_begin + TP; t0 < s_stop; t0 += TP) {
 #pragma unroll
         for (int j = 0; j < TPR; ++j)
-            kk[j] = nt_load<NW>(krow(min(t0 + j * ROWS + row, t_stop - 1)) + col * VPL);
+            kk[j] = nt_load<NW>(K + (size_t)min(t0 + j * ROWS + row, s_stop - 1) * D + col * VPL);
 #pragma unroll
         for (int j = 0; j < TPR; ++j)
-            vv[j] = nt_load<NW>(vrow(min(t0 + j * ROWS + row, t_stop - 1)) + col * VPL);
+            vv[j] = nt_load<NW>(V + (size_t)min(t0 + j * ROWS + row, s_stop - 1) * D + col * VPL);
         __builtin_amdgcn_sched_barrier(0);
-        attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, t_end, qf, m, l, acc);
+        attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, s_end, qf, m, l, acc);
     }
     // merge the rows of each wavefront: they share its max, so by sums; every
     // exchange of a step is issued before the first is used
@@ -282,8 +327,7 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
             sl[wave] = l;
         }
     }
-    __syncthreads();  // every wavefront has read n before the append changes it
-    if (owner && !CHUNKED) append_commit(L, h, n, tid);
+    __syncthreads();
     if (tid < D) {
         // all LDS reads first: the merge runs on two wavefronts at the very end
         // of the block, where each serial LDS latency adds to the launch
@@ -316,7 +360,7 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
             }
         }
     }
-    if constexpr (CHUNKED) chunk_merge<D, APPEND>(L, h, n, out, part, tid);
+    if constexpr (CHUNKED) chunk_merge<D>(L, h, out, part, tid);
 }
 
 }  // namespace dev

@@ -43,7 +43,8 @@ template <int D, int T, int TPR>
 __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_attn_layers(
     LayersArg args, MetaLayout ml, int BH, int C, float qscale) {
     const int layer = (int)blockIdx.x / BH;
-    const LayerDev L = make_layer_dev(args.kv[layer], args.meta[layer], ml);
+    LayerDev L = make_layer_dev(args.kv[layer], args.meta[layer], ml);
+    L.dn = args.dn[layer];
     const AppendArgs none{};
     attn_block<D, false, T, false, TPR>(L, C, none, args.q[layer], args.out[layer], nullptr, 0, 0,
                                         0, qscale, (int)blockIdx.x - layer * BH);

@@ -44,10 +44,8 @@ __global__ __launch_bounds__(kBlock) void k_prefill(LayerDev L, int C, int d, co
 }
 
 __global__ void k_append(LayerDev L, int C, int d, AppendArgs a) {
-    const int h = blockIdx.x, n = L.n[h];
-    append_token(L, C, d, h, n, a, threadIdx.x);
-    __syncthreads();
-    append_commit(L, h, n, threadIdx.x);
+    const int h = blockIdx.x;
+    append_token(L, C, d, h, head_len(L, h), a, threadIdx.x);
 }
 
 // ------------------------------------------------------------ head grouping
@@ -149,13 +147,20 @@ __global__ void k_budgets(LayerDev L, int H, int N, const uint8_t* is_local,
 // ------------------------------------------------------------------- update
 // LDS of one update block, sized by the host from the largest source capacity
 // of the launch (`cap`) and the number of visual positions (`N`).
+// Steps of the query ring staged through LDS at a time when an update sums
+// its window (Eq. 6 scores).
+constexpr int kRingChunk = 64;
+
 struct UpdateLds {
     static __host__ __device__ int words(int N) { return (N + 31) >> 5; }
     static __host__ __device__ size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
+    static __host__ __device__ int stage_steps(int P) { return P < kRingChunk ? P : kRingChunk; }
     // bitmap | word prefix | order (u16) | evict (u8) | positions (i32) |
     // scores (f64, also two int lists) | query sum (f64 [d]), or with
-    // attention-sum scores G queries (f64 [G][d]) | with attention-sum scores:
-    // weights of the cache for each query of a group (f64 [G][C + cap])
+    // attention-sum scores G queries (f64 [G][d]) | with Eq. 6 scores: ring
+    // rows of the window staged for its sum (bf16 [min(P, kRingChunk)][d]);
+    // with attention-sum scores: weights of the cache for each query of a
+    // group (f64 [G][C + cap])
     static __host__ __device__ size_t off_wpre(int N) { return a16(4 * (size_t)words(N)); }
     static __host__ __device__ size_t off_order(int N) { return off_wpre(N) + a16(4 * (size_t)words(N)); }
     static __host__ __device__ size_t off_evict(int N, int cap) { return off_order(N) + a16(2 * (size_t)cap); }
@@ -165,8 +170,9 @@ struct UpdateLds {
     static __host__ __device__ size_t off_w(int N, int cap, int d, int g) {
         return off_qs(N, cap) + a16(8 * (size_t)d * g);
     }
-    static __host__ __device__ size_t bytes(int N, int cap, int d, int C, bool attn, int g) {
-        return off_w(N, cap, d, attn ? g : 1) + (attn ? a16(8 * (size_t)g * ((size_t)C + cap)) : 0);
+    static __host__ __device__ size_t bytes(int N, int cap, int d, int C, bool attn, int g, int P) {
+        return off_w(N, cap, d, attn ? g : 1) +
+               (attn ? a16(8 * (size_t)g * ((size_t)C + cap)) : a16(2 * (size_t)d * stage_steps(P)));
     }
 };
 
@@ -448,19 +454,14 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
     double* qs = reinterpret_cast<double*>(lds + UpdateLds::off_qs(N, lds_cap));
     int32_t* pos = reinterpret_cast<int32_t*>(lds + UpdateLds::off_pos(N, lds_cap));
     const int tid = threadIdx.x;
-    const int n0 = L.n[h];
+    const int n0 = head_len(L, h);
     const int B = L.budget[h];
     const int local = L.label[h];
     // the step's append, then the update that follows it; the update takes the
-    // new token's position and the new query sum from the append's own values
-    // rather than reading them back from memory
+    // new token's position from the append's own values rather than reading it
+    // back from memory (the ring slot it wrote is read back by the same thread)
     const bool app = a.k != nullptr;
-    double qs_new = 0.0;
-    if (app) {
-        const AppendVals av = append_load(L, D, h, a, tid);
-        append_store(L, C, D, h, n0, a, av, tid);
-        qs_new = av.qs_old + bf_f64(av.qbits);  // the query sum append_store wrote
-    }
+    if (app) append_token(L, C, D, h, n0, a, tid);
     const int n = n0 + (app ? 1 : 0);
     // Eq. (2): history = retained tokens older than the recent window
     const int w_eff = recent_len < B ? recent_len : B;
@@ -468,7 +469,9 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
     const int keep = B - w_eff;
     const int M = T > keep ? T - keep : 0;
     if (!relayout && M == 0) {
-        if (app && tid == 0) L.n[h] = n;
+        // every head's length is written at an update (the host's count of
+        // appended tokens starts again from it)
+        if (tid == 0) L.n[h] = n;
         return n;
     }
 
@@ -538,8 +541,38 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
             // 1/(P sqrt(d)) is dropped, the order is that of (sum q) . k, summed
             // over the dims in order in fp64.  Each thread reads half of its row's
             // 16-byte chunks together and then walks them in order.
-            for (int i = tid; i < D; i += NT)
-                qs[i] = (app && a.accumulate) ? qs_new : L.qsum[(size_t)h * D + i];
+            // the window's query sum, q_{w0} + ... + q_step in step order in
+            // fp64: up to kRingChunk ring rows at a time are loaded in one
+            // round (every load issued before the first LDS store) and staged
+            // through LDS, then each of D threads adds its dim's column
+            {
+                uint16_t* stage = reinterpret_cast<uint16_t*>(lds + UpdateLds::off_w(N, lds_cap, D, 1));
+                constexpr int PER = (kRingChunk * kRow16 + NT - 1) / NT;
+                const int P = L.ring_len;
+                const int w0 = step - P + 1 > 0 ? step - P + 1 : 0;
+                double qacc = 0.0;
+                for (int c0 = w0; c0 <= step; c0 += kRingChunk) {
+                    const int cn = step + 1 - c0 < kRingChunk ? step + 1 - c0 : kRingChunk;
+                    uint4 buf[PER];
+#pragma unroll
+                    for (int k = 0; k < PER; ++k) {
+                        const int v = tid + k * NT;
+                        if (v < cn * kRow16)
+                            buf[k] = reinterpret_cast<const uint4*>(
+                                ring_slot(L, D, h, c0 + v / kRow16))[v % kRow16];
+                    }
+#pragma unroll
+                    for (int k = 0; k < PER; ++k) {
+                        const int v = tid + k * NT;
+                        if (v < cn * kRow16) reinterpret_cast<uint4*>(stage)[v] = buf[k];
+                    }
+                    __syncthreads();
+                    if (tid < D)
+                        for (int j = 0; j < cn; ++j) qacc = qacc + bf_f64(stage[j * D + tid]);
+                    __syncthreads();
+                }
+                if (tid < D) qs[tid] = qacc;
+            }
             __syncthreads();
             for (int r = r_lo + tid; r < r_hi; r += NT) {
                 const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + order[r]) * D);
@@ -678,7 +711,7 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_u
 __global__ __launch_bounds__(kBlock) void k_export(LayerDev L, int C, int d, int N, uint8_t* mask,
                                                    int32_t* count) {
     const int h = blockIdx.x, tid = threadIdx.x;
-    const int n = L.n[h];
+    const int n = head_len(L, h);
     SegPtrs s = seg_ptrs(L.kv + L.seg_off[h], C, L.cap[h], d);
     for (int p = tid; p < N; p += kBlock) mask[(size_t)h * N + p] = 0;
     __syncthreads();
@@ -724,7 +757,7 @@ int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
 // has that many and their weights fit in the LDS, else 1.
 int update_query_group(int N, int cap, int d, int C, bool attn_scores, int period) {
     if (!attn_scores || period < kQueryGroup) return 1;
-    return UpdateLds::bytes(N, cap, d, C, true, kQueryGroup) <= kUpdateLdsBudget ? kQueryGroup : 1;
+    return UpdateLds::bytes(N, cap, d, C, true, kQueryGroup, period) <= kUpdateLdsBudget ? kQueryGroup : 1;
 }
 
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
@@ -733,9 +766,9 @@ int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const 
                   void* stream, void* ev_start, void* ev_stop) {
     hipStream_t st = (hipStream_t)stream;
     hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
-    const bool attn = L.qring != nullptr;
+    const bool attn = L.attn_scores != 0;
     const int G = update_query_group(s.N, lds_cap, s.d, s.C, attn, L.ring_len);
-    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, attn, G);
+    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, attn, G, L.ring_len);
     // allow the update block more than 64 KB of dynamic LDS (gfx950: 160 KB)
     static const bool lds_ok = [] {
         const int max_lds = 160 * 1024;
@@ -845,7 +878,7 @@ int launch_update_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, i
                        int tpr, void* stream, void* ev_start, void* ev_stop) {
     hipStream_t st = (hipStream_t)stream;
     hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
-    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, false, 1);
+    const size_t lds = UpdateLds::bytes(s.N, lds_cap, s.d, s.C, false, 1, L.ring_len);
     if (s.d == 128)
         update_attn_threads<128>(L, s, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q,
                                  out, use_order, pad_len, threads, tpr, lds, st, e0, e1);
@@ -855,8 +888,8 @@ int launch_update_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, i
     return last_error();
 }
 
-size_t update_lds_bytes(int N, int cap, int d, int C, bool attn_scores) {
-    return UpdateLds::bytes(N, cap, d, C, attn_scores, 1);
+size_t update_lds_bytes(int N, int cap, int d, int C, bool attn_scores, int period) {
+    return UpdateLds::bytes(N, cap, d, C, attn_scores, 1, period);
 }
 
 int launch_export(const LayerDev& L, const Shape& s, uint8_t* mask, int32_t* count,

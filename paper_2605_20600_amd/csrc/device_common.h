@@ -78,49 +78,50 @@ __device__ __forceinline__ SegPtrs seg_ptrs(char* seg, int C, int cap, int d) {
 
 // ------------------------------------------------------------------- append
 // K <- [K, k_t], V <- [V, v_t] for head h by the threads tid < d of a block:
-// row C+n, pos[n] = step, the query sum of the update window.  Split in a
-// load half and a store half so that a caller can put other loads between
-// them; the length n is changed by append_commit once no thread reads it.
-// The load half only issues loads (no loaded value is used before the store
-// half), so that a caller's loads are not held behind their latency.
+// row C+n, pos[n] = step, and q_t into the head's ring of the last P queries
+// (the window an update scores against, Eq. 6).  Split in a load half and a
+// store half so that a caller can put other loads between them.  The length
+// itself is not stored: the host counts the appended tokens (LayerDev::dn),
+// and only prefill and the periodic update write n.  The load half only
+// issues loads (no loaded value is used before the store half), so that a
+// caller's loads are not held behind their latency.
 struct AppendVals {
     uint16_t k = 0, v = 0, qbits = 0;
-    double qs_old = 0.0;
 };
 
-__device__ __forceinline__ AppendVals append_load(const LayerDev& L, int d, int h,
-                                                  const AppendArgs& a, int tid) {
+__device__ __forceinline__ uint16_t* ring_slot(const LayerDev& L, int d, int h, int step) {
+    return L.qring + ((size_t)h * L.ring_len + step % L.ring_len) * d;
+}
+
+__device__ __forceinline__ AppendVals append_load(int d, int h, const AppendArgs& a, int tid) {
     AppendVals r;
     if (tid < d) {
+        r.qbits = a.q[(size_t)h * d + tid];
         r.k = a.k[(size_t)h * d + tid];
         r.v = a.v[(size_t)h * d + tid];
-        if (a.accumulate || L.qring) r.qbits = a.q[(size_t)h * d + tid];
-        if (a.accumulate && !a.reset) r.qs_old = L.qsum[(size_t)h * d + tid];
     }
     return r;
 }
 
 __device__ __forceinline__ void append_store(const LayerDev& L, int C, int d, int h, int n,
                                              const AppendArgs& a, const AppendVals& r, int tid) {
-#pragma clang fp contract(off)
     if (tid >= d) return;
     SegPtrs s = seg_ptrs(L.kv + L.seg_off[h], C, L.cap[h], d);
     const size_t row = (size_t)(C + n) * d;
     s.K[row + tid] = r.k;
     s.V[row + tid] = r.v;
-    if (a.accumulate) L.qsum[(size_t)h * d + tid] = r.qs_old + bf_f64(r.qbits);  // 0 + q on a reset
-    if (L.qring) L.qring[((size_t)h * L.ring_len + a.step % L.ring_len) * d + tid] = r.qbits;
+    ring_slot(L, d, h, a.step)[tid] = r.qbits;
     if (tid == 0) s.pos[n] = a.step;
 }
 
 __device__ __forceinline__ void append_token(const LayerDev& L, int C, int d, int h, int n,
                                              const AppendArgs& a, int tid) {
-    append_store(L, C, d, h, n, a, append_load(L, d, h, a, tid), tid);
+    append_store(L, C, d, h, n, a, append_load(d, h, a, tid), tid);
 }
 
-__device__ __forceinline__ void append_commit(const LayerDev& L, int h, int n, int tid) {
-    if (tid == 0) L.n[h] = n + 1;
-}
+// Current length of head h: n as the last kernel that set it wrote it, plus
+// the tokens appended since (one per step, for every head alike).
+__device__ __forceinline__ int head_len(const LayerDev& L, int h) { return L.n[h] + L.dn; }
 
 // Step 1 for head h of the dense layout, by the nthreads threads of a block:
 // layer state reset (segment, capacity, length 0, labels, query sum, the
@@ -145,7 +146,6 @@ __device__ inline void prefill_head(const LayerDev& L, int h, int nheads, int C,
             L.order[h] = h;
             L.done[h] = 0;
         }
-        for (int i = tid; i < d; i += nthreads) L.qsum[(size_t)h * d + i] = 0.0;
     }
     if (r1 <= r0) return;
     SegPtrs s = seg_ptrs(L.kv + (int64_t)h * seg_bytes, C, dense_cap, d);

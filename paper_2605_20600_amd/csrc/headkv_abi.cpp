@@ -42,6 +42,9 @@ struct Layer {
     bool grouped = false;
     int last_step = -1;
     std::vector<int> n, budget, cap;
+    // tokens every head appended since the device lengths were last written
+    // (by prefill or an update); kernels take the length as n[h] + dn
+    int dn = 0;
     std::vector<uint8_t> label_local;  // labels used by the updates (host copy)
     int chunk_threads = kAttnMaxThreads;  // block size the chunk table is cut for
     int items = 0;                        // entries of the chunk table
@@ -109,7 +112,7 @@ headkv_status validate_config(const headkv_config* c) {
         return fail(HEADKV_ERR_INVALID_ARG, "unknown score_mode");
     if (c->score_mode == HEADKV_SCORE_ATTN_SUM &&
         update_lds_bytes(c->num_visual, std::min(c->num_visual, HEADKV_MAX_CAPACITY), c->head_dim,
-                         c->prefix_len, true) > kUpdateLdsBudget)
+                         c->prefix_len, true, c->period) > kUpdateLdsBudget)
         return fail(HEADKV_ERR_UNSUPPORTED, "attention-sum scores: prefix + capacity too large for LDS");
     if (c->cfg_pairs && c->batch % 2 != 0)
         return fail(HEADKV_ERR_INVALID_ARG, "cfg_pairs needs an even batch");
@@ -145,8 +148,8 @@ Plan make_plan(const headkv_config& c) {
     // the largest capacity any head can have, dense or after grouping
     const int max_cap = std::max(p.dense_cap, std::min(c.num_visual, HEADKV_MAX_CAPACITY));
     const int per_head = chunks_of(c.prefix_len, max_cap, kAttnMinThreads, c.head_dim);
-    p.ml.compute(p.BH, c.head_dim, p.BH * per_head,
-                 c.score_mode == HEADKV_SCORE_ATTN_SUM ? c.period : 0);
+    p.ml.compute(p.BH, c.head_dim, p.BH * per_head, c.period,
+                 c.score_mode == HEADKV_SCORE_ATTN_SUM ? 1 : 0);
     // partial (max, sum, weighted V) of every chunk table entry
     p.ws_bytes = align_up((size_t)p.BH * per_head * (c.head_dim + 2) * sizeof(float), 256);
     return p;
@@ -196,7 +199,9 @@ headkv_status hip_status(int e, const char* what) {
 double sqrt_d(headkv_t h) { return std::sqrt((double)h->cfg.head_dim); }
 
 LayerDev dev_of(headkv_t h, const Layer& L) {
-    return make_layer_dev(L.grouped ? L.ragged : L.dense, L.meta, h->ml);
+    LayerDev D = make_layer_dev(L.grouped ? L.ragged : L.dense, L.meta, h->ml);
+    D.dn = L.dn;
+    return D;
 }
 
 // Event pair for a sampled launch of `kind`, or nullptrs.
@@ -293,6 +298,7 @@ headkv_status prefill_impl(headkv_t h, int32_t layer, const uint16_t* q_c, const
     L.ragged = nullptr;
     L.last_step = -1;
     L.n.assign(h->shape.BH, 0);
+    L.dn = 0;
     L.cap.assign(h->shape.BH, h->dense_cap);
     L.budget.assign(h->shape.BH, 0);
     L.label_local.assign(h->shape.BH, 0);
@@ -359,15 +365,13 @@ headkv_status prepare_append(headkv_t h, int32_t layer, int32_t step, const uint
         return fail(HEADKV_ERR_STATE, "heads must be grouped at step group_threshold - 1");
     for (int i = 0; i < h->shape.BH; ++i)
         if (L.n[i] >= L.cap[i]) return fail(HEADKV_ERR_CAPACITY, "head capacity exhausted");
-    // window of the past-P queries that the next update scores against (Eq. 6)
+    // every append writes q into the head's ring of the last P queries, the
+    // window that the next update scores against (Eq. 6)
     const int P = c.period;
-    const int first = std::max(0, h->t_g - P + 1);
     a->q = q;
     a->k = k;
     a->v = v;
     a->step = step;
-    a->accumulate = step >= first ? 1 : 0;
-    a->reset = (step == first) || (step > h->t_g && (step - h->t_g - 1) % P == 0);
     *update = L.grouped && step > h->t_g && (step - h->t_g) % P == 0;
     *u = (step - h->t_g) / P;
     return ok();
@@ -376,6 +380,8 @@ headkv_status prepare_append(headkv_t h, int32_t layer, int32_t step, const uint
 // Host mirror after the append (and update) of `step`.
 void commit_append(headkv_t h, Layer& L, int32_t step, bool update) {
     for (int i = 0; i < h->shape.BH; ++i) L.n[i] += 1;
+    // the update kernel writes every head's length; an append alone does not
+    L.dn = update ? 0 : L.dn + 1;
     if (update)
         for (int i = 0; i < h->shape.BH; ++i) L.n[i] = std::min(L.n[i], L.budget[i]);
     L.last_step = step;
@@ -512,14 +518,14 @@ namespace {
 // Algorithmic HBM bytes of the kernels of a decode step, from the host mirror
 // (n before the step's append).
 //   fused append + attention: K and V of the prefix, the retained tokens and
-//   the new token; q in, the output out; the new K/V row and its position
-//   written; the fp64 query sum read and written when accumulating.
-double fused_step_bytes(headkv_t h, const Layer& L, bool accumulate) {
+//   the new token; q in, the output out; the new K/V row, its position and q's
+//   ring row written.
+double fused_step_bytes(headkv_t h, const Layer& L) {
     const headkv_config& c = h->cfg;
     const double d = c.head_dim;
     double tokens = 0;
     for (int n : L.n) tokens += c.prefix_len + n + 1;
-    const double per_head = d * 2 + d * 4 + 2 * d * 2 + 4 + (accumulate ? 2 * d * 8 : 0);
+    const double per_head = d * 2 + d * 4 + 3 * d * 2 + 4;
     return tokens * 2 * d * 2 + h->shape.BH * per_head;
 }
 
@@ -533,9 +539,9 @@ double attn_bytes(headkv_t h, const Layer& L) {
 }
 
 //   append + periodic update: the append (q, k, v in; K/V row, position and
-//   query sum written); every head's positions; for a global head that evicts,
-//   the keys of its history and its query sum; and at most M K/V rows and
-//   positions moved by the compaction.
+//   q's ring row written); every head's positions; for a global head that
+//   evicts, the keys of its history and the window's queries from the ring;
+//   and at most M K/V rows and positions moved by the compaction.
 double update_bytes(headkv_t h, const Layer& L) {
     const headkv_config& c = h->cfg;
     const double d = c.head_dim;
@@ -545,9 +551,9 @@ double update_bytes(headkv_t h, const Layer& L) {
         const int w_eff = std::min(c.recent_len, B);
         const int T = std::max(0, n - w_eff);
         const int M = std::max(0, T - (B - w_eff));
-        b += 3 * 2 * d + 2 * 2 * d + 4 + 2 * 8 * d + 4.0 * n;
+        b += 3 * 2 * d + 3 * 2 * d + 4 + 4.0 * n;
         if (M > 0) {
-            if (!L.label_local[i]) b += T * 2 * d + 8 * d;
+            if (!L.label_local[i]) b += T * 2 * d + std::min(c.period, L.last_step + 2) * 2 * d;
             b += M * (2 * 2 * 2 * d + 8);
         }
     }
@@ -594,13 +600,13 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
                         "append + update launch");
         if (st) return st;
         take_events(h, time_it, HEADKV_TIMED_ATTN, attn_bytes(h, L), &e0, &e1);
-        return launch_attention(h, L, D, none, q, out, static_cast<float*>(h->ws), stream, e0, e1,
-                                "attention launch");
+        // over the lengths the update wrote (D still counts the step's append)
+        return launch_attention(h, L, dev_of(h, L), none, q, out, static_cast<float*>(h->ws),
+                                stream, e0, e1, "attention launch");
     }
-    // the append is fused into the attention (its length committed by the
-    // head's block, or by the last of its chunks to finish)
+    // the append is fused into the attention; the host counts it (dn)
     take_events(h, time_it, L.grouped ? HEADKV_TIMED_ATTN_APPEND : HEADKV_TIMED_ATTN_APPEND_DENSE,
-                fused_step_bytes(h, L, a.accumulate != 0), &e0, &e1);
+                fused_step_bytes(h, L), &e0, &e1);
     st = launch_attention(h, L, D, a, q, out, static_cast<float*>(h->ws), stream, e0, e1,
                           "append + attention launch");
     if (st) return st;
@@ -794,6 +800,7 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     // first update, fused with the move from the dense buffer into the segments
     if (!st) {
         LayerDev Dnew = make_layer_dev(ragged_kv, L.meta, h->ml);
+        Dnew.dn = L.dn;  // the lengths it moves: prefill's 0 plus every append since
         AppendArgs none{};
         st = hip_status(launch_update(Dnew, h->shape, none, static_cast<const char*>(L.dense), 1,
                                       h->dense_seg, h->dense_cap, c.recent_len, c.rs_num, c.rs_den,
@@ -817,6 +824,7 @@ headkv_status headkv_assign_budgets(headkv_t h, int32_t layer, const uint8_t* is
     L.items = (int)items.size();
     L.n_global = n_global;
     for (int i = 0; i < BH; ++i) L.n[i] = std::min(L.n[i], L.budget[i]);
+    L.dn = 0;  // the relayout wrote every head's length
     return ok();
 }
 
@@ -906,6 +914,7 @@ headkv_status headkv_decode_attn_layers(headkv_t h, int32_t layer_begin, int32_t
             return fail(HEADKV_ERR_STATE, "assign_budgets must run before attention at step group_threshold - 1");
         args.kv[i] = L.grouped ? L.ragged : L.dense;
         args.meta[i] = L.meta;
+        args.dn[i] = L.dn;
         args.q[i] = q[i];
         args.out[i] = out[i];
         len_max = std::max(len_max, h->cfg.prefix_len + *std::max_element(L.n.begin(), L.n.end()));

@@ -45,15 +45,17 @@ inline size_t segment_bytes(int C, int cap, int d) {
 }
 
 struct MetaLayout {
-    size_t seg_off, cap, n, budget, nstar, label, order, done, qsum, items, item_start, qring, total;
-    int max_items, ring_len;
+    size_t seg_off, cap, n, budget, nstar, label, order, done, items, item_start, qring, total;
+    int max_items, ring_len, attn_scores;
 
     // max_items: largest chunk table of a layer (every head at its largest
     // capacity, in chunks of the smallest attention pass); ring_len: queries
-    // kept per head for the attention-sum eviction scores (0: none).
-    void compute(int BH, int d, int max_items_, int ring_len_) {
+    // kept per head, the update period (the window of Eq. 6); attn_scores: 1
+    // when global heads are scored by the window's attention weights.
+    void compute(int BH, int d, int max_items_, int ring_len_, int attn_scores_ = 0) {
         max_items = max_items_;
         ring_len = ring_len_;
+        attn_scores = attn_scores_;
         size_t o = 0;
         auto take = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
         seg_off = take(sizeof(int64_t) * BH);
@@ -64,7 +66,6 @@ struct MetaLayout {
         label = take(sizeof(int32_t) * BH);
         order = take(sizeof(int32_t) * BH);
         done = take(sizeof(int32_t) * BH);
-        qsum = take(sizeof(double) * (size_t)BH * d);
         items = take(sizeof(uint32_t) * (size_t)max_items);
         item_start = take(sizeof(int32_t) * ((size_t)BH + 1));
         qring = take(sizeof(uint16_t) * (size_t)BH * ring_len * d);
@@ -77,22 +78,24 @@ struct LayerDev {
     char* kv;             // base of the layer's current KV buffer
     int64_t* seg_off;     // byte offset of each head's segment in kv
     int32_t* cap;         // visual slots of each head
-    int32_t* n;           // occupied visual slots
+    int32_t* n;           // occupied visual slots as of the last kernel that set them
+                          // (prefill, an update): the length is n[h] + dn
     int32_t* budget;      // visual-token budget (after grouping)
     int32_t* nstar;       // n* from grouping
     int32_t* label;       // 1 = local head
     int32_t* order;       // attention dispatch order of the heads (longest first)
     int32_t* done;        // chunks of each head finished in the running chunked
                           // launch (zero between launches)
-    double* qsum;         // [BH][d] running sum of the queries of this window
     // chunk table: entry = head << 8 | chunk, the chunks of a head contiguous;
     // head h owns entries item_start[h] .. item_start[h+1]-1
     uint32_t* items;
     int32_t* item_start;  // [BH + 1]
-    // attention-sum scores only: the queries of the last ring_len steps,
-    // [BH][ring_len][d] bf16, step t in slot t % ring_len (else nullptr)
+    // the queries of the last ring_len steps, [BH][ring_len][d] bf16, step t
+    // in slot t % ring_len: the window that an update scores against
     uint16_t* qring;
     int ring_len;
+    int attn_scores;      // 1: attention-sum scores instead of Eq. 6
+    int dn;               // tokens every head appended since n was written
 };
 
 #if defined(__HIPCC__)
@@ -110,11 +113,12 @@ inline LayerDev make_layer_dev(void* kv, void* meta, const MetaLayout& m) {
     L.label = reinterpret_cast<int32_t*>(b + m.label);
     L.order = reinterpret_cast<int32_t*>(b + m.order);
     L.done = reinterpret_cast<int32_t*>(b + m.done);
-    L.qsum = reinterpret_cast<double*>(b + m.qsum);
     L.items = reinterpret_cast<uint32_t*>(b + m.items);
     L.item_start = reinterpret_cast<int32_t*>(b + m.item_start);
-    L.qring = m.ring_len > 0 ? reinterpret_cast<uint16_t*>(b + m.qring) : nullptr;
+    L.qring = reinterpret_cast<uint16_t*>(b + m.qring);
     L.ring_len = m.ring_len;
+    L.attn_scores = m.attn_scores;
+    L.dn = 0;
     return L;
 }
 
@@ -130,8 +134,6 @@ struct AppendArgs {
     const uint16_t* k;
     const uint16_t* v;
     int step;            // visual position of the token
-    int accumulate;      // add q to the head's query sum
-    int reset;           // the query sum restarts with this q
 };
 
 // Also writes the dense layout's chunk table: dense_chunks chunks per head.
@@ -153,7 +155,7 @@ int launch_budgets(const LayerDev& L, const Shape& s, const uint8_t* is_local,
                    int recent_len, int rho_num, int rho_den, int cfg_pairs, void* stream);
 // a.k == nullptr: no append.  step: the visual step of the update.
 // lds_cap: largest visual capacity among the launch's source segments.
-// With L.qring, global heads are scored by the window's attention weights.
+// With L.attn_scores, global heads are scored by the window's attention weights.
 int launch_update(const LayerDev& L, const Shape& s, const AppendArgs& a, const char* src_kv,
                   int relayout, int64_t dense_seg_bytes, int dense_cap, int recent_len,
                   int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
@@ -166,7 +168,7 @@ int launch_update_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, i
                        const uint16_t* q, float* out, int use_order, int pad_len, int threads,
                        int tpr, void* stream, void* ev_start, void* ev_stop);
 // Dynamic LDS of one update block (C: prefix rows, with attention-sum scores).
-size_t update_lds_bytes(int N, int cap, int d, int C, bool attn_scores);
+size_t update_lds_bytes(int N, int cap, int d, int C, bool attn_scores, int period);
 // Dynamic LDS an update block may take: the CU's 160 KB less a margin for the
 // kernel's static LDS (block scans, radix histogram, reductions).
 constexpr size_t kUpdateLdsBudget = 156 * 1024;
@@ -191,6 +193,7 @@ constexpr int kMaxLayersPerLaunch = 64;
 struct LayersArg {
     void* kv[kMaxLayersPerLaunch];
     void* meta[kMaxLayersPerLaunch];
+    int dn[kMaxLayersPerLaunch];
     const uint16_t* q[kMaxLayersPerLaunch];
     float* out[kMaxLayersPerLaunch];
 };
