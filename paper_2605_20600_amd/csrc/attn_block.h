@@ -57,13 +57,14 @@ __device__ __forceinline__ float agent_load(const float* p) {
 // have completed
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8)); }
 
-// End of a chunk of a chunked launch: the chunks of a head count themselves
-// in L.done[h] once their partials (o, m, l) are out, and the chunk that
-// arrives last merges them -- m = max m_i, o = sum_i o_i 2^(m_i - m) /
-// sum_i l_i 2^(m_i - m) -- writes the head's output and clears the counter
-// for the next launch.
+// End of a chunk of a chunked launch: the nch chunks of a head that hold
+// tokens count themselves in L.done[h] once their partials (o, m, l) are out,
+// and the chunk that arrives last merges them -- m = max m_i, o = sum_i o_i
+// 2^(m_i - m) / sum_i l_i 2^(m_i - m) -- writes the head's output and clears
+// the counter for the next launch.
 template <int D>
-__device__ __forceinline__ void chunk_merge(const LayerDev& L, int h, float* __restrict__ out,
+__device__ __forceinline__ void chunk_merge(const LayerDev& L, int h, int nch,
+                                            float* __restrict__ out,
                                             const float* __restrict__ part, int tid) {
     constexpr int PS = D + 2;
     __shared__ int last;
@@ -72,10 +73,10 @@ __device__ __forceinline__ void chunk_merge(const LayerDev& L, int h, float* __r
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     wait_vmem();
     __syncthreads();
-    const int i0 = L.item_start[h], i1 = L.item_start[h + 1];
+    const int i0 = L.item_start[h], i1 = i0 + nch;
     if (tid == 0)
         last = __hip_atomic_fetch_add(L.done + h, 1, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT) == i1 - i0 - 1;
+                                      __HIP_MEMORY_SCOPE_AGENT) == nch - 1;
     __syncthreads();
     if (!last) return;
     wait_vmem();
@@ -206,6 +207,11 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     // attended as token len_c, from the input
     const int len_c = C + n;
     const int len = len_c + (APPEND ? 1 : 0);
+    // chunked: only the chunks that hold tokens take part (a chunk past the
+    // head's length has nothing to do), and the only chunk of a head that
+    // fits in one writes the output itself, without partials
+    const int nch = len > TP ? (len + TP - 1) / TP : 1;
+    if (CHUNKED && t_begin >= nch * TP) return;
     const int t_end = CHUNKED ? min(len, t_begin + TP) : len;
     // cache rows this block streams: [t_begin, s_end); the padding strategy
     // reads the rows of the layer's longest head (pad_len attended tokens, the
@@ -349,7 +355,7 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
             o += f * xw[w];
             z += f * lw[w];
         }
-        if (!CHUNKED) {
+        if (!CHUNKED || nch == 1) {
             out[(size_t)h * D + tid] = o / z;
         } else {
             float* pp = part + (size_t)item * (D + 2);
@@ -360,7 +366,7 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
             }
         }
     }
-    if constexpr (CHUNKED) chunk_merge<D>(L, h, out, part, tid);
+    if (CHUNKED && nch > 1) chunk_merge<D>(L, h, nch, out, part, tid);
 }
 
 }  // namespace dev

@@ -154,7 +154,9 @@ constexpr int kRingChunk = 64;
 struct UpdateLds {
     static __host__ __device__ int words(int N) { return (N + 31) >> 5; }
     static __host__ __device__ size_t a16(size_t x) { return (x + 15) & ~(size_t)15; }
-    static __host__ __device__ int stage_steps(int P) { return P < kRingChunk ? P : kRingChunk; }
+    // staged ring rows: the window's first chunk, rounded up to whole groups of
+    // eight rows (read eight at a time)
+    static __host__ __device__ int stage_steps(int P) { return ((P < kRingChunk ? P : kRingChunk) + 7) & ~7; }
     // bitmap | word prefix | order (u16) | evict (u8) | positions (i32) |
     // scores (f64, also two int lists) | query sum (f64 [d]), or with
     // attention-sum scores G queries (f64 [G][d]) | with Eq. 6 scores: ring
@@ -458,10 +460,14 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
     const int B = L.budget[h];
     const int local = L.label[h];
     // the step's append, then the update that follows it; the update takes the
-    // new token's position from the append's own values rather than reading it
-    // back from memory (the ring slot it wrote is read back by the same thread)
+    // new token's position and query from the append's own values rather than
+    // reading them back from memory
     const bool app = a.k != nullptr;
-    if (app) append_token(L, C, D, h, n0, a, tid);
+    AppendVals av;
+    if (app) {
+        av = append_load(D, h, a, tid);
+        append_store(L, C, D, h, n0, a, av, tid);
+    }
     const int n = n0 + (app ? 1 : 0);
     // Eq. (2): history = retained tokens older than the recent window
     const int w_eff = recent_len < B ? recent_len : B;
@@ -473,6 +479,24 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
         // appended tokens starts again from it)
         if (tid == 0) L.n[h] = n;
         return n;
+    }
+    // Eq. 6 window of a global head that evicts: steps w0..step of the query
+    // ring (the step's own query, when this kernel appends it, from the
+    // append's values).  The first kRingChunk rows are loaded now, so that
+    // their round trip overlaps the ranking below.
+    constexpr int PER = (kRingChunk * kRow16 + NT - 1) / NT;
+    const int w0 = step - L.ring_len + 1 > 0 ? step - L.ring_len + 1 : 0;
+    const int wlast = app ? step - 1 : step;  // last step read from the ring
+    const bool window = !ATTN_SUM && !local && M > 0;
+    uint4 wbuf[PER];
+    if (window) {
+        const int cn = wlast + 1 - w0 < kRingChunk ? wlast + 1 - w0 : kRingChunk;
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int v = tid + k * NT;
+            if (v < cn * kRow16)
+                wbuf[k] = reinterpret_cast<const uint4*>(ring_slot(L, D, h, w0 + v / kRow16))[v % kRow16];
+        }
     }
 
     const int src_cap = relayout ? dense_cap : L.cap[h];
@@ -542,35 +566,44 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
             // over the dims in order in fp64.  Each thread reads half of its row's
             // 16-byte chunks together and then walks them in order.
             // the window's query sum, q_{w0} + ... + q_step in step order in
-            // fp64: up to kRingChunk ring rows at a time are loaded in one
-            // round (every load issued before the first LDS store) and staged
-            // through LDS, then each of D threads adds its dim's column
+            // fp64: up to kRingChunk ring rows at a time (the first chunk loaded
+            // above) are staged through LDS, then each of D threads adds its
+            // dim's column
             {
                 uint16_t* stage = reinterpret_cast<uint16_t*>(lds + UpdateLds::off_w(N, lds_cap, D, 1));
-                constexpr int PER = (kRingChunk * kRow16 + NT - 1) / NT;
-                const int P = L.ring_len;
-                const int w0 = step - P + 1 > 0 ? step - P + 1 : 0;
                 double qacc = 0.0;
-                for (int c0 = w0; c0 <= step; c0 += kRingChunk) {
-                    const int cn = step + 1 - c0 < kRingChunk ? step + 1 - c0 : kRingChunk;
-                    uint4 buf[PER];
+                for (int c0 = w0; c0 <= wlast; c0 += kRingChunk) {
+                    const int cn = wlast + 1 - c0 < kRingChunk ? wlast + 1 - c0 : kRingChunk;
+                    if (c0 != w0) {
 #pragma unroll
-                    for (int k = 0; k < PER; ++k) {
-                        const int v = tid + k * NT;
-                        if (v < cn * kRow16)
-                            buf[k] = reinterpret_cast<const uint4*>(
-                                ring_slot(L, D, h, c0 + v / kRow16))[v % kRow16];
+                        for (int k = 0; k < PER; ++k) {
+                            const int v = tid + k * NT;
+                            if (v < cn * kRow16)
+                                wbuf[k] = reinterpret_cast<const uint4*>(
+                                    ring_slot(L, D, h, c0 + v / kRow16))[v % kRow16];
+                        }
                     }
 #pragma unroll
                     for (int k = 0; k < PER; ++k) {
                         const int v = tid + k * NT;
-                        if (v < cn * kRow16) reinterpret_cast<uint4*>(stage)[v] = buf[k];
+                        if (v < cn * kRow16) reinterpret_cast<uint4*>(stage)[v] = wbuf[k];
                     }
                     __syncthreads();
+                    // eight LDS reads in flight ahead of the in-order adds (the
+                    // stage holds whole groups of eight rows; rows past cn are
+                    // read and not added)
                     if (tid < D)
-                        for (int j = 0; j < cn; ++j) qacc = qacc + bf_f64(stage[j * D + tid]);
+                        for (int j0 = 0; j0 < cn; j0 += 8) {
+                            uint16_t x[8];
+#pragma unroll
+                            for (int j = 0; j < 8; ++j) x[j] = stage[(j0 + j) * D + tid];
+#pragma unroll
+                            for (int j = 0; j < 8; ++j)
+                                if (j0 + j < cn) qacc = qacc + bf_f64(x[j]);
+                        }
                     __syncthreads();
                 }
+                if (app && tid < D) qacc = qacc + bf_f64(av.qbits);
                 if (tid < D) qs[tid] = qacc;
             }
             __syncthreads();
