@@ -86,6 +86,13 @@ def parse():
                         "rho 1/6 and 1/4, Janus-Pro-7B, Lumina-1024 and the stress shape)")
     p.add_argument("--traffic-kernel", default="k_attn<128, true, 1024, false, 8>",
                    help="kernel name the traffic record is taken for")
+    p.add_argument("--traffic-out", default=None,
+                   help="path of the traffic record (default: the headline kernel's under profiles/)")
+    p.add_argument("--traffic-workload", default="lumina_mgpt_768_shape b8 rho=1/8",
+                   help="workload label of the traffic record")
+    p.add_argument("--counter-summary", nargs=2, metavar=("DIR", "KERNEL"),
+                   help="print the mean per dispatch of every counter of a rocprofv3 --pmc "
+                        "output folder for one kernel and exit; no GPU needed")
     return p.parse_args()
 
 
@@ -119,9 +126,10 @@ def measured_traffic():
     return rec["traffic_bytes_per_dispatch"] if ok else None
 
 
-def counter_mean(run_dir: str, kernel_substr: str):
-    """Mean value per dispatch of the one counter of a rocprofv3 --pmc run
-    (its counter_collection.csv), over the dispatches of the named kernel."""
+def counter_mean(run_dir: str, kernel_substr: str, counter: str | None = None):
+    """Mean value per dispatch of a counter of a rocprofv3 --pmc run (its
+    counter_collection.csv), over the dispatches of the named kernel; without
+    `counter`, the run must hold one counter."""
     import csv
     import glob
     files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
@@ -130,18 +138,41 @@ def counter_mean(run_dir: str, kernel_substr: str):
     total, n = 0.0, 0
     with open(files[0]) as fh:
         for row in csv.DictReader(fh):
-            if kernel_substr in row.get("Kernel_Name", ""):
-                total += float(row["Counter_Value"])
-                n += 1
+            if kernel_substr not in row.get("Kernel_Name", ""):
+                continue
+            if counter is not None and row.get("Counter_Name") != counter:
+                continue
+            total += float(row["Counter_Value"])
+            n += 1
     if n == 0:
         raise SystemExit(f"no dispatch of {kernel_substr!r} in {files[0]}")
     return total / n, n
 
 
-def write_traffic_record(dirs, kernel: str):
-    """Writes the traffic record from four rocprofv3 --pmc runs: FETCH_SIZE and
-    WRITE_SIZE of the attention kernel, then of the copy probe (whose bytes
-    are known), which scale the counters to bytes."""
+def counter_summary(run_dir: str, kernel_substr: str):
+    """Mean per dispatch of every counter of a rocprofv3 --pmc run, over the
+    dispatches of the named kernel, as one JSON line."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {run_dir}")
+    names = set()
+    with open(files[0]) as fh:
+        for row in csv.DictReader(fh):
+            if kernel_substr in row.get("Kernel_Name", ""):
+                names.add(row["Counter_Name"])
+    out = {"kernel": kernel_substr, "run": os.path.basename(os.path.normpath(run_dir))}
+    for c in sorted(names):
+        out[c], out["dispatches"] = counter_mean(run_dir, kernel_substr, c)
+    print(json.dumps(out))
+
+
+def write_traffic_record(dirs, kernel: str, out_path: str = TRAFFIC_RECORD,
+                         workload: str = "lumina_mgpt_768_shape b8 rho=1/8"):
+    """Writes a traffic record from four rocprofv3 --pmc runs: FETCH_SIZE and
+    WRITE_SIZE of the kernel, then of the copy probe (whose bytes are known),
+    which scale the counters to bytes."""
     fetch, n = counter_mean(dirs[0], kernel)
     write, _ = counter_mean(dirs[1], kernel)
     copy_fetch, _ = counter_mean(dirs[2], "copyBuffer")  # the runtime's copy kernel
@@ -150,7 +181,7 @@ def write_traffic_record(dirs, kernel: str):
     fs, ws = probe / (copy_fetch * 1024), probe / (copy_write * 1024)
     rec = {
         "kernel": kernel,
-        "workload": "lumina_mgpt_768_shape b8 rho=1/8",
+        "workload": workload,
         "attn_source_sha256": attn_source_sha256(),
         "dispatches_sampled": n,
         "fetch_kib_per_dispatch": fetch,
@@ -162,7 +193,7 @@ def write_traffic_record(dirs, kernel: str):
         "write_scale": ws,
         "traffic_bytes_per_dispatch": fetch * 1024 * fs + write * 1024 * ws,
     }
-    with open(TRAFFIC_RECORD, "w") as f:
+    with open(out_path, "w") as f:
         json.dump(rec, f, indent=1)
         f.write("\n")
     print(json.dumps(rec))
@@ -546,7 +577,11 @@ def main():
               "shards by batch row or head with no communication, see DESIGN.md", file=sys.stderr)
         sys.exit(2)
     if args.traffic_record:
-        write_traffic_record(args.traffic_record, args.traffic_kernel)
+        write_traffic_record(args.traffic_record, args.traffic_kernel,
+                             args.traffic_out or TRAFFIC_RECORD, args.traffic_workload)
+        return
+    if args.counter_summary:
+        counter_summary(*args.counter_summary)
         return
     if args.kernel_trace_record:
         write_kernel_trace_record(args.kernel_trace_record)
