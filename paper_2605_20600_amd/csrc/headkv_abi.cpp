@@ -148,7 +148,10 @@ Plan make_plan(const headkv_config& c) {
     // the largest capacity any head can have, dense or after grouping
     const int max_cap = std::max(p.dense_cap, std::min(c.num_visual, HEADKV_MAX_CAPACITY));
     const int per_head = chunks_of(c.prefix_len, max_cap, kAttnMinThreads, c.head_dim);
-    p.ml.compute(p.BH, c.head_dim, p.BH * per_head, c.period,
+    // ring of the window queries: an update's window never holds more than
+    // min(P, N) steps (with P > N the grouping step's update is the only one,
+    // and its window starts at step 0 either way)
+    p.ml.compute(p.BH, c.head_dim, p.BH * per_head, std::min(c.period, c.num_visual),
                  c.score_mode == HEADKV_SCORE_ATTN_SUM ? 1 : 0);
     // partial (max, sum, weighted V) of every chunk table entry
     p.ws_bytes = align_up((size_t)p.BH * per_head * (c.head_dim + 2) * sizeof(float), 256);

@@ -62,6 +62,19 @@ def test_period_not_dividing_rows(fused):
     _run(W.TINY.with_(period=7, group_threshold=50), fused=fused)
 
 
+def test_period_longer_than_generation():
+    # P > N: the grouping step's update is the only one, and its window of
+    # past queries starts at step 0 (the library keeps min(P, N) of them)
+    _run(W.TINY.with_(period=300))
+
+
+@pytest.mark.parametrize("fused", [True, False])
+def test_window_longer_than_one_staging_chunk(fused):
+    # a window of 100 queries is summed in two chunks of the update's LDS stage
+    # (64 + 36 steps), the grouping window in one (steps 0..63)
+    _run(W.TINY.with_(period=100, group_threshold=64), fused=fused)
+
+
 @pytest.mark.parametrize("r_s", [(0, 1), (1, 1), (3, 10), (4, 5)])
 def test_stratification_ratio(r_s):
     _run(W.TINY.with_(r_s=r_s), r_s=r_s)
