@@ -125,12 +125,13 @@ typedef struct headkv_ctx* headkv_t;
  *   meta_bytes:     per layer, segment table, lengths, labels, budgets,
  *                   the last `period` queries of every head (the window an
  *                   update scores against), the attention dispatch order, the
- *                   attention chunk table and its per-head counters of
- *                   finished chunks (zero between launches);
- *   workspace_bytes: one buffer shared by all layers: attention partials of
- *                   layers with fewer heads than compute units, which cut
- *                   each head into chunks of one pass (the last chunk of a
- *                   head to finish merges them in the same kernel). */
+ *                   attention chunk table;
+ *   workspace_bytes: one buffer shared by all layers: the merge words of the
+ *                   attention of layers with fewer heads than compute units,
+ *                   which cut each head into chunks of one pass and merge
+ *                   them in the same kernel.  The library zeroes it before
+ *                   its first use and every launch leaves it zero; callers
+ *                   must not write it while a handle uses it. */
 headkv_status headkv_plan(const headkv_config* cfg, size_t* dense_kv_bytes,
                           size_t* meta_bytes, size_t* workspace_bytes);
 
@@ -227,8 +228,8 @@ headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q,
  * each head into chunks whose partial results headkv_decode_attn keeps in the
  * handle's workspace; this call keeps them in a static device array of
  * 4 MiB that the library holds on each GPU it runs on until the process ends
- * (HEADKV_ERR_CAPACITY if a layer's chunks need more: entries x (head_dim + 2)
- * x 4 bytes).  It calls no hipMalloc, hipFree or allocating routine.  Every
+ * (HEADKV_ERR_CAPACITY if a layer's chunks need more: entries x head_dim x
+ * 8 bytes).  It calls no hipMalloc, hipFree or allocating routine.  Every
  * call on one GPU shares that GPU's array (the current device's), so calls
  * that overlap on one GPU, on any streams or handles, race; calls ordered on
  * one stream do not. */

@@ -44,73 +44,69 @@ __device__ __forceinline__ Words<NW> nt_load(const uint16_t* p) {
     return w;
 }
 
-// Plain stores can stay in the writing XCD's L2, which another XCD does not
-// see before the kernel ends; agent-scope atomic stores and loads reach the
-// memory every XCD shares, without flushing or invalidating a whole L2.
-__device__ __forceinline__ void agent_store(float* p, float v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float agent_load(const float* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// s_waitcnt with vmcnt(0) only: this wavefront's global loads and stores
-// have completed
-__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8)); }
+// Merge of the chunks of a head, column by column: lane tid < D of a chunk
+// holds its column's normalised output o = sum_j p_j v_j / sum_j p_j and the
+// chunk's log2-sum-exp s = m + log2(l).  Chunks are the leaves of a binary
+// tree over chunk indices; at every inner node the two subtrees' (o, s) meet
+// through one 64-bit atomic exchange on the node's word (the first to arrive
+// leaves its pair there and is done; the second receives it, clears the word,
+// merges left with right and goes up), and the chunk that completes the root
+// writes the head's output.  The partner's data comes back in the atomic's
+// own return value, so nothing waits for another chunk's stores, and the
+// fixed left-right order makes the result independent of arrival order.  The
+// node whose right subtree starts at chunk c owns the words of slot i0 + c
+// (one per column; c = 1 .. nch - 1 name the nch - 1 inner nodes); a word is
+// zero between launches, and a pair never packs to zero: its high half is
+// bits(s) XOR kPartKey, a signalling-NaN pattern that no arithmetic result
+// carries.
+constexpr uint32_t kPartKey = 0x7fbadbadu;
 
-// End of a chunk of a chunked launch: the nch chunks of a head that hold
-// tokens count themselves in L.done[h] once their partials (o, m, l) are out,
-// and the chunk that arrives last merges them -- m = max m_i, o = sum_i o_i
-// 2^(m_i - m) / sum_i l_i 2^(m_i - m) -- writes the head's output and clears
-// the counter for the next launch.
+__device__ __forceinline__ uint64_t pair_pack(float o, float s) {
+    return ((uint64_t)(__float_as_uint(s) ^ kPartKey) << 32) | (uint64_t)__float_as_uint(o);
+}
+// (o, s) <- (o, s) merged with (ob, sb), in that order
+__device__ __forceinline__ void pair_merge(float& o, float& s, float ob, float sb) {
+    const float mx = fmaxf(s, sb);
+    const float wa = __builtin_amdgcn_exp2f(s - mx);
+    const float wb = __builtin_amdgcn_exp2f(sb - mx);
+    const float w = wa + wb;
+    o = (o * wa + ob * wb) / w;
+    s = mx + __builtin_amdgcn_logf(w);
+}
+
+// Chunk c of the nch chunks of head h, column tid < D with (o, s): climbs the
+// tree while it is the second to reach a node.  i0: the head's first slot
+// (item_start[h]); part: D words per slot.
 template <int D>
-__device__ __forceinline__ void chunk_merge(const LayerDev& L, int h, int nch,
+__device__ __forceinline__ void chunk_merge(int h, int nch, int c, int i0, float o, float s,
                                             float* __restrict__ out,
-                                            const float* __restrict__ part, int tid) {
-    constexpr int PS = D + 2;
-    __shared__ int last;
-    // this wavefront's partial stores are complete before the barrier, so
-    // before the count
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    wait_vmem();
-    __syncthreads();
-    const int i0 = L.item_start[h], i1 = i0 + nch;
-    if (tid == 0)
-        last = __hip_atomic_fetch_add(L.done + h, 1, __ATOMIC_RELAXED,
-                                      __HIP_MEMORY_SCOPE_AGENT) == nch - 1;
-    __syncthreads();
-    if (!last) return;
-    wait_vmem();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-    if (tid < D) {
-        // the partials of up to CB chunks are loaded together (indices past
-        // the head's last chunk re-read it and are skipped), then merged
-        // online
-        constexpr int CB = 4;
-        float m = -INFINITY, num = 0.f, den = 0.f;
-        for (int i = i0; i < i1; i += CB) {
-            float mi[CB], oi[CB], li[CB];
-#pragma unroll
-            for (int k = 0; k < CB; ++k) {
-                const float* pp = part + (size_t)min(i + k, i1 - 1) * PS;
-                mi[k] = agent_load(pp + D);
-                oi[k] = agent_load(pp + tid);
-                li[k] = agent_load(pp + D + 1);
-            }
-#pragma unroll
-            for (int k = 0; k < CB; ++k) {
-                if (i + k < i1 && mi[k] != -INFINITY) {
-                    const float mn = fmaxf(m, mi[k]);
-                    const float fa = __builtin_amdgcn_exp2f(m - mn);  // m = -inf gives 0
-                    const float fb = __builtin_amdgcn_exp2f(mi[k] - mn);
-                    num = num * fa + oi[k] * fb;
-                    den = den * fa + li[k] * fb;
-                    m = mn;
-                }
-            }
+                                            uint64_t* __restrict__ part, int tid) {
+    int c0 = c;  // first chunk of the subtree that (o, s) covers
+    for (int lvl = 0;; ++lvl) {
+        const int size = 1 << lvl;
+        if (c0 == 0 && size >= nch) {
+            out[(size_t)h * D + tid] = o;
+            return;
         }
-        out[(size_t)h * D + tid] = num / den;
+        const bool left = ((c0 >> lvl) & 1) == 0;
+        const int right = left ? c0 + size : c0;  // first chunk of the right subtree
+        if (right >= nch) continue;               // no right subtree: up a level
+        uint64_t* w = part + (size_t)(i0 + right) * D + tid;
+        const uint64_t other =
+            __hip_atomic_exchange(w, pair_pack(o, s), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (other == 0) return;  // the other subtree's chunk goes on
+        __hip_atomic_store(w, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        float ob = __uint_as_float((uint32_t)other);
+        float sb = __uint_as_float((uint32_t)(other >> 32) ^ kPartKey);
+        if (left) {
+            pair_merge(o, s, ob, sb);
+        } else {
+            pair_merge(ob, sb, o, s);
+            o = ob;
+            s = sb;
+            c0 -= size;
+        }
     }
-    if (tid == 0) __hip_atomic_store(L.done + h, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Online-softmax update of one row's state with NT tokens t0 + j * ROWS + row
@@ -167,7 +163,7 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
 template <int D, bool APPEND, int T, bool CHUNKED, int TPR>
 __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const AppendArgs& a,
                                            const uint16_t* __restrict__ q,
-                                           float* __restrict__ out, float* __restrict__ part,
+                                           float* __restrict__ out, uint64_t* __restrict__ part,
                                            int use_order, int order_base, int pad_len,
                                            float qscale, int item, int n_given = -1) {
     using Vec = typename AttnRegs<D>::Vec;
@@ -194,6 +190,7 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     // n_given: the length as the caller already knows it (a kernel that has
     // just changed it), else the one in memory
     const int n = n_given >= 0 ? n_given : head_len(L, h);
+    const int i0 = CHUNKED ? L.item_start[h] : 0;  // the head's first chunk slot
     // Everything the first K/V load waits for comes in two rounds of scalar
     // loads: the kernel arguments, then the metadata with the rest of them.
     // Left to itself, the compiler fetches arguments late, each behind the
@@ -201,6 +198,7 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     // these values pins them before any load that follows.  (Placed before the
     // metadata loads, it would make them vector loads.)
     asm volatile("" ::"s"(q), "s"(seg), "s"(cap), "s"(n), "s"(C), "s"(pad_len), "s"(qscale));
+    if (CHUNKED) asm volatile("" ::"s"(i0), "s"(part));
     if (APPEND) asm volatile("" ::"s"(a.k), "s"(a.v), "s"(L.qring), "s"(L.ring_len));
     const Vec qraw = *reinterpret_cast<const Vec*>(q + (size_t)h * D + col * VPL);
     // the cache holds len_c tokens; with the append, the step's token is
@@ -355,18 +353,12 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
             o += f * xw[w];
             z += f * lw[w];
         }
-        if (!CHUNKED || nch == 1) {
+        if (!CHUNKED || nch == 1)
             out[(size_t)h * D + tid] = o / z;
-        } else {
-            float* pp = part + (size_t)item * (D + 2);
-            agent_store(pp + tid, o);
-            if (tid == 0) {
-                agent_store(pp + D, mx);
-                agent_store(pp + D + 1, z);
-            }
-        }
+        else
+            chunk_merge<D>(h, nch, t_begin / TP, i0, o / z, mx + __builtin_amdgcn_logf(z), out,
+                           part, tid);
     }
-    if (CHUNKED && nch > 1) chunk_merge<D>(L, h, nch, out, part, tid);
 }
 
 }  // namespace dev

@@ -8,14 +8,15 @@
 //            dispatch order (one head group per launch) and may read up to a
 //            padded length with the rows past their own length masked (the
 //            other two strategies of Sec. 5.1 for heads of unequal length).
-//            In a chunked launch the last chunk of a head to finish merges
-//            the head's chunks.
+//            In a chunked launch the chunks of a head merge their results
+//            through a tree of atomic exchanges, in the same kernel.
 //
 // The block itself (rows of d/8 lanes, all loads of a pass issued before
 // use, online softmax, merge through LDS) is attn_block in attn_block.h.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -33,7 +34,7 @@ using namespace dev;
 template <int D, bool APPEND, int T, bool CHUNKED, int TPR>
 __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_attn(
     LayerDev L, int C, AppendArgs a, const uint16_t* __restrict__ q, float* __restrict__ out,
-    float* __restrict__ part, int use_order, int order_base, int pad_len, float qscale) {
+    uint64_t* __restrict__ part, int use_order, int order_base, int pad_len, float qscale) {
     attn_block<D, APPEND, T, CHUNKED, TPR>(L, C, a, q, out, part, use_order, order_base, pad_len,
                                            qscale, (int)blockIdx.x);
 }
@@ -50,11 +51,17 @@ __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_a
                                         0, qscale, (int)blockIdx.x - layer * BH);
 }
 
+// Sets n words to zero: a partial buffer before its first chunked launch.
+__global__ __launch_bounds__(256) void k_zero(uint64_t* __restrict__ p, size_t n) {
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256)
+        p[i] = 0u;
+}
+
 inline int last_error() { return (int)hipGetLastError(); }
 
 template <int D, int T, bool CHUNKED, int TPR>
 void attn_launch(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
-                 float* out, float* partials, const AttnPlan& p, hipStream_t st, hipEvent_t ev0,
+                 float* out, uint64_t* partials, const AttnPlan& p, hipStream_t st, hipEvent_t ev0,
                  hipEvent_t ev1) {
     const float qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
     const dim3 grid(CHUNKED ? p.items : p.heads), block(T);
@@ -71,7 +78,7 @@ void attn_launch(const LayerDev& L, const Shape& s, const AppendArgs& a, const u
 
 template <int D, int T>
 void attn_dispatch_t(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
-                     float* out, float* partials, const AttnPlan& p, hipStream_t st,
+                     float* out, uint64_t* partials, const AttnPlan& p, hipStream_t st,
                      hipEvent_t ev0, hipEvent_t ev1) {
     if (p.chunked)
         attn_launch<D, T, true, kAttnTpr>(L, s, a, q, out, partials, p, st, ev0, ev1);
@@ -87,7 +94,7 @@ void attn_dispatch_t(const LayerDev& L, const Shape& s, const AppendArgs& a, con
 
 template <int D>
 void attn_dispatch(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
-                   float* out, float* partials, const AttnPlan& p, hipStream_t st,
+                   float* out, uint64_t* partials, const AttnPlan& p, hipStream_t st,
                    hipEvent_t ev0, hipEvent_t ev1) {
     if (p.threads == 1024)
         attn_dispatch_t<D, 1024>(L, s, a, q, out, partials, p, st, ev0, ev1);
@@ -129,8 +136,15 @@ void layers_dispatch(const LayersArg& a, int layers, const MetaLayout& ml, const
         layers_launch<D, 256>(a, layers, ml, s, tpr, st);
 }
 
+int launch_zero_words(uint64_t* p, size_t n, void* stream) {
+    if (n == 0) return 0;
+    const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 1024);
+    hipLaunchKernelGGL(k_zero, dim3(blocks), dim3(256), 0, (hipStream_t)stream, p, n);
+    return last_error();
+}
+
 int launch_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
-                float* out, float* partials, const AttnPlan& p, void* stream, void* ev_start,
+                float* out, uint64_t* partials, const AttnPlan& p, void* stream, void* ev_start,
                 void* ev_stop) {
     hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
     if (s.d == 128)

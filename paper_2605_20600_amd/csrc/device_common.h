@@ -124,8 +124,8 @@ __device__ __forceinline__ void append_token(const LayerDev& L, int C, int d, in
 __device__ __forceinline__ int head_len(const LayerDev& L, int h) { return L.n[h] + L.dn; }
 
 // Step 1 for head h of the dense layout, by the nthreads threads of a block:
-// layer state reset (segment, capacity, length 0, labels, query sum, the
-// dense chunk table) and, for prefix rows [r0, r1), the copy of the
+// layer state reset (segment, capacity, length 0, labels, the dense chunk
+// table) and, for prefix rows [r0, r1), the copy of the
 // conditional keys and values into the head's first rows.
 __device__ inline void prefill_head(const LayerDev& L, int h, int nheads, int C, int d,
                                     const uint16_t* kc, const uint16_t* vc, int64_t seg_bytes,
@@ -144,7 +144,6 @@ __device__ inline void prefill_head(const LayerDev& L, int h, int nheads, int C,
             L.nstar[h] = 0;
             L.label[h] = 0;
             L.order[h] = h;
-            L.done[h] = 0;
         }
     }
     if (r1 <= r0) return;

@@ -63,6 +63,8 @@ struct headkv_ctx {
     int64_t dense_seg = 0;         // bytes per head segment before grouping
     size_t ws_bytes = 0;
     void* ws = nullptr;
+    bool ws_clear = false;         // the workspace has been zeroed (the chunked
+                                   // attention keeps it zero between launches)
     std::vector<Layer> layers;
     // timing of sampled launches: event pairs, kind and algorithmic bytes
     std::vector<hipEvent_t> events;
@@ -154,7 +156,7 @@ Plan make_plan(const headkv_config& c) {
     p.ml.compute(p.BH, c.head_dim, p.BH * per_head, std::min(c.period, c.num_visual),
                  c.score_mode == HEADKV_SCORE_ATTN_SUM ? 1 : 0);
     // partial (max, sum, weighted V) of every chunk table entry
-    p.ws_bytes = align_up((size_t)p.BH * per_head * (c.head_dim + 2) * sizeof(float), 256);
+    p.ws_bytes = align_up((size_t)p.BH * per_head * c.head_dim * sizeof(uint64_t), 256);
     return p;
 }
 
@@ -417,8 +419,8 @@ int resident_threads(int heads) {
 // The attention launches of one layer step (appended: the step's token is
 // attended from the input).  Returns their number (1 or 2).
 //  VARLEN, fewer heads than CUs: the layer's chunk table, chunks of one pass
-//    balanced across heads of unequal length, merged by the last chunk of
-//    each head to finish.
+//    balanced across heads of unequal length, merged in the same kernel
+//    (a tree of atomic exchanges over each head's chunks).
 //  VARLEN otherwise: one block per head over all its passes (no merge, the
 //    append fused), at the largest block size at which every head's block is
 //    resident at once (beyond that 256-thread blocks); longest heads first
@@ -481,7 +483,7 @@ int attn_plans(headkv_t h, const Layer& L, bool appended, AttnPlan* out) {
 // point's scratch); the event pair brackets the first kernel's start and the
 // last kernel's end.
 headkv_status launch_attention(headkv_t h, const Layer& L, const LayerDev& D, const AppendArgs& a,
-                               const uint16_t* q, float* out, float* partials, void* stream,
+                               const uint16_t* q, float* out, uint64_t* partials, void* stream,
                                void* e0, void* e1, const char* what) {
     AttnPlan plans[2];
     const int np = attn_plans(h, L, a.k != nullptr, plans);
@@ -490,6 +492,17 @@ headkv_status launch_attention(headkv_t h, const Layer& L, const LayerDev& D, co
             return fail(HEADKV_ERR_STATE,
                         "the handle has no workspace and this layer's attention is split into "
                         "chunks: use headkv_decode_attn_noalloc");
+    // the merge words of a chunked launch are zero until written; the static
+    // scratch starts zero, the caller's workspace is zeroed once
+    if (partials != nullptr && partials == h->ws && !h->ws_clear) {
+        for (int i = 0; i < np; ++i) {
+            if (!plans[i].chunked) continue;
+            const int e = launch_zero_words(partials, h->ws_bytes / sizeof(uint64_t), stream);
+            if (e) return hip_status(e, "workspace clear");
+            h->ws_clear = true;
+            break;
+        }
+    }
     for (int i = 0; i < np; ++i) {
         const int e = launch_attn(D, h->shape, a, q, out, partials, plans[i], stream,
                                   i == 0 ? e0 : nullptr, i == np - 1 ? e1 : nullptr);
@@ -614,13 +627,13 @@ headkv_status decode_step_impl(headkv_t h, int32_t layer, int32_t step, const ui
         if (st) return st;
         take_events(h, time_it, HEADKV_TIMED_ATTN, attn_bytes(h, L), &e0, &e1);
         // over the lengths the update wrote (D still counts the step's append)
-        return launch_attention(h, L, dev_of(h, L), none, q, out, static_cast<float*>(h->ws),
+        return launch_attention(h, L, dev_of(h, L), none, q, out, static_cast<uint64_t*>(h->ws),
                                 stream, e0, e1, "attention launch");
     }
     // the append is fused into the attention; the host counts it (dn)
     take_events(h, time_it, L.grouped ? HEADKV_TIMED_ATTN_APPEND : HEADKV_TIMED_ATTN_APPEND_DENSE,
                 fused_step_bytes(h, L), &e0, &e1);
-    st = launch_attention(h, L, D, a, q, out, static_cast<float*>(h->ws), stream, e0, e1,
+    st = launch_attention(h, L, D, a, q, out, static_cast<uint64_t*>(h->ws), stream, e0, e1,
                           "append + attention launch");
     if (st) return st;
     commit_append(h, L, step, update);
@@ -868,7 +881,7 @@ headkv_status headkv_decode_attn(headkv_t h, int32_t layer, const uint16_t* q, f
     if (st) return st;
     const Layer& L = h->layers[layer];
     AppendArgs none{};
-    return launch_attention(h, L, dev_of(h, L), none, q, out, static_cast<float*>(h->ws), stream,
+    return launch_attention(h, L, dev_of(h, L), none, q, out, static_cast<uint64_t*>(h->ws), stream,
                             nullptr, nullptr, "attention launch");
 }
 
@@ -883,7 +896,7 @@ headkv_status headkv_decode_attn_noalloc(headkv_t h, int32_t layer, const uint16
     for (int i = 0; i < np; ++i) {
         if (!plans[i].chunked) continue;
         chunked = true;
-        const size_t need = (size_t)plans[i].items * (h->cfg.head_dim + 2) * sizeof(float);
+        const size_t need = (size_t)plans[i].items * h->cfg.head_dim * sizeof(uint64_t);
         if (need > kScratchBytes)
             return fail(HEADKV_ERR_CAPACITY, "the layer's chunked attention needs " +
                                                  std::to_string(need) + " bytes of partials, more "
@@ -896,7 +909,7 @@ headkv_status headkv_decode_attn_noalloc(headkv_t h, int32_t layer, const uint16
         if (st) return st;
     }
     AppendArgs none{};
-    return launch_attention(h, L, dev_of(h, L), none, q, out, static_cast<float*>(scratch), stream,
+    return launch_attention(h, L, dev_of(h, L), none, q, out, static_cast<uint64_t*>(scratch), stream,
                             nullptr, nullptr, "attention launch");
 }
 

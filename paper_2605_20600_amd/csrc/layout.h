@@ -45,7 +45,7 @@ inline size_t segment_bytes(int C, int cap, int d) {
 }
 
 struct MetaLayout {
-    size_t seg_off, cap, n, budget, nstar, label, order, done, items, item_start, qring, total;
+    size_t seg_off, cap, n, budget, nstar, label, order, items, item_start, qring, total;
     int max_items, ring_len, attn_scores;
 
     // max_items: largest chunk table of a layer (every head at its largest
@@ -65,7 +65,6 @@ struct MetaLayout {
         nstar = take(sizeof(int32_t) * BH);
         label = take(sizeof(int32_t) * BH);
         order = take(sizeof(int32_t) * BH);
-        done = take(sizeof(int32_t) * BH);
         items = take(sizeof(uint32_t) * (size_t)max_items);
         item_start = take(sizeof(int32_t) * ((size_t)BH + 1));
         qring = take(sizeof(uint16_t) * (size_t)BH * ring_len * d);
@@ -84,8 +83,6 @@ struct LayerDev {
     int32_t* nstar;       // n* from grouping
     int32_t* label;       // 1 = local head
     int32_t* order;       // attention dispatch order of the heads (longest first)
-    int32_t* done;        // chunks of each head finished in the running chunked
-                          // launch (zero between launches)
     // chunk table: entry = head << 8 | chunk, the chunks of a head contiguous;
     // head h owns entries item_start[h] .. item_start[h+1]-1
     uint32_t* items;
@@ -112,7 +109,6 @@ inline LayerDev make_layer_dev(void* kv, void* meta, const MetaLayout& m) {
     L.nstar = reinterpret_cast<int32_t*>(b + m.nstar);
     L.label = reinterpret_cast<int32_t*>(b + m.label);
     L.order = reinterpret_cast<int32_t*>(b + m.order);
-    L.done = reinterpret_cast<int32_t*>(b + m.done);
     L.items = reinterpret_cast<uint32_t*>(b + m.items);
     L.item_start = reinterpret_cast<int32_t*>(b + m.item_start);
     L.qring = reinterpret_cast<uint16_t*>(b + m.qring);
@@ -176,8 +172,8 @@ constexpr size_t kUpdateLdsBudget = 156 * 1024;
 struct AttnPlan {
     int threads;     // 1024, 512 or 256
     int chunked;     // 0: one block per head, every pass; 1: one block per entry
-                     //    of the chunk table (chunks of one pass), merged by
-                     //    the last chunk of each head
+                     //    of the chunk table (chunks of one pass), merged in
+                     //    the kernel
     int items;       // entries of the chunk table (chunked)
     int heads;       // blocks of a launch with one block per head
     int use_order;   // one block per head: head = order[order_base + block]
@@ -201,12 +197,15 @@ struct LayersArg {
 // resident): heads of layer i are blocks i*BH .. i*BH + BH - 1.
 int launch_attn_layers(const LayersArg& a, int layers, const MetaLayout& ml, const Shape& s,
                        int threads, int tpr, void* stream);
-// a.k == nullptr: no append.  partials: (d + 2) floats per table entry.
+// a.k == nullptr: no append.  partials: d 64-bit words per table entry, zero
+// between launches (every word a chunked launch writes, it also clears).
 // ev_start / ev_stop (hipEvent_t or nullptr) receive the attention kernel's
 // own start and end timestamps.
 int launch_attn(const LayerDev& L, const Shape& s, const AppendArgs& a, const uint16_t* q,
-                float* out, float* partials, const AttnPlan& p, void* stream,
+                float* out, uint64_t* partials, const AttnPlan& p, void* stream,
                 void* ev_start = nullptr, void* ev_stop = nullptr);
+// Sets n 64-bit words at p to zero (a partial buffer before its first use).
+int launch_zero_words(uint64_t* p, size_t n, void* stream);
 int launch_export(const LayerDev& L, const Shape& s, uint8_t* mask, int32_t* count,
                   void* stream);
 

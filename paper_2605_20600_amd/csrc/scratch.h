@@ -1,6 +1,7 @@
 // The per-GPU static scratch array of the allocation-free attention entry
-// point (headkv_decode_attn_noalloc): room for the split-K partial results of
-// a chunked attention launch, so that the call needs no workspace.
+// point (headkv_decode_attn_noalloc): room for the merge words of a chunked
+// attention launch, so that the call needs no workspace.  It is zero when the
+// library loads, and every launch leaves the words it uses zero again.
 #pragma once
 
 #include <cstddef>

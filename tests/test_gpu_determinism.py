@@ -4,8 +4,8 @@ One flipped eviction changes every later step of a head, so the kernels must
 decide identically on identical inputs however their blocks are scheduled:
 the fp64 eviction scores and grouping mass are summed in a fixed order, the
 radix selection takes equal keys in position order, and the split-K merge of
-a chunked layer adds its partial results in chunk order whichever chunk
-arrives last.  Two fresh sessions over the same inputs must give bitwise-equal
+a chunked layer combines its partial results in a fixed tree over the chunk
+indices (left before right) whichever chunk arrives first.  Two fresh sessions over the same inputs must give bitwise-equal
 labels, n*, budgets, retained sets and attention outputs.
 """
 import pytest

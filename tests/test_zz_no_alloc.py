@@ -5,7 +5,7 @@ Both run the same attention kernels; the allocation-free call keeps the
 split-K partial results of a chunked layer (fewer batch x heads than compute
 units) in the library's static per-GPU scratch array instead of the handle's
 workspace.  Its outputs must equal the existing entry point's bit for bit (the
-chunks of a head are merged in chunk order either way), hence also lie within
+chunks of a head are merged in the same fixed tree either way), hence also lie within
 the 2e-2 parity bar of the oracle.  Two calls in a row, the second on a smaller
 layer, check that what the first left in the shared scratch does not leak into
 the second.
