@@ -251,6 +251,51 @@ __device__ void select_lowest(const double* sig, const uint16_t* order, uint8_t*
     }
 }
 
+// The same two selections as select_lowest on parts [0, n_long) and
+// [n_long, T), when T <= NT / 4: four threads (consecutive lanes) count the
+// entries of an entry's part that come before it by (score, rank), and the
+// entry leaves if fewer than its part's m do.  One pass over the part instead
+// of up to eight radix passes with their barriers; the count grows with the
+// part's size, so larger parts keep the radix select.  A part is ranked only
+// if it keeps some and loses some entries (the only parts whose scores exist).
+template <int NT>
+__device__ void select_small(double* sig, const uint16_t* order, uint8_t* evict, int n_long,
+                             int T, int m_long, int m_near, int tid) {
+    uint64_t* key = reinterpret_cast<uint64_t*>(sig);  // keys replace the scores in place
+    auto part_of = [&](int r, int& lo, int& hi, int& mq) {
+        const bool lng = r < n_long;
+        lo = lng ? 0 : n_long;
+        hi = lng ? n_long : T;
+        mq = lng ? m_long : m_near;
+    };
+    {
+        int lo, hi, mq;
+        part_of(tid, lo, hi, mq);
+        if (tid < T && mq > 0 && mq < hi - lo) key[tid] = score_key(sig[tid]);
+    }
+    __syncthreads();
+    const int r = tid >> 2, q = tid & 3;
+    int lo, hi, mq;
+    part_of(r, lo, hi, mq);
+    if (r >= T || mq <= 0) return;
+    if (mq >= hi - lo) {
+        if (q == 0) evict[order[r]] = 1;
+        return;
+    }
+    // entries before r count when not greater, those after when less
+    const uint64_t kr = key[r];
+    int c = 0;
+#pragma unroll 4
+    for (int j = lo + q; j < hi; j += 4) {
+        const uint64_t kj = key[j];
+        c += (j < r ? kj <= kr : kj < kr) ? 1 : 0;
+    }
+    // the four lanes of an entry are all here
+    c += __shfl_xor(c, 1);
+    c += __shfl_xor(c, 2);
+    if (q == 0 && c < mq) evict[order[r]] = 1;
+}
+
 // q . k of a cached row in fp64, the dims summed in order, without FMA.
 template <int D>
 __device__ __forceinline__ double dot_row(const double* qd, const uint16_t* row) {
@@ -503,16 +548,45 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
     char* src_seg = relayout ? const_cast<char*>(src_kv) + (int64_t)h * dense_seg_bytes
                              : L.kv + L.seg_off[h];
     SegPtrs S = seg_ptrs(src_seg, C, src_cap, D);
+    // With at most one slot per thread, thread s loads its slot's position
+    // now, and, for a global head that scores (NT >= 512: registers for a
+    // whole row), its K row right after the positions, so that their round
+    // trips overlap the ranking and the window sum.  The appended row is still
+    // being stored: its position comes from the step, its row is read when it
+    // is scored.
+    constexpr bool kRowAhead = NT >= 512 && !ATTN_SUM;
+    const bool one_slot = n <= NT;
+    const int n_ahead = app ? n0 : n;
+    const bool ahead = kRowAhead && window && one_slot;
+    int p_own = 0;
+    if (one_slot && tid < n) p_own = (app && tid == n0) ? a.step : S.pos[tid];
+    uint4 krow[kRowAhead ? kRow16 : 1];
 
     // rank every occupied slot by its position: bitmap + prefix popcount
     const int nw = UpdateLds::words(N);
     for (int i = tid; i < nw; i += NT) bm[i] = 0u;
     for (int i = tid; i < n; i += NT) evict[i] = 0;
     __syncthreads();
-    for (int s = tid; s < n; s += NT) {
-        const int p = (app && s == n0) ? a.step : S.pos[s];
-        pos[s] = p;
-        atomicOr(&bm[p >> 5], 1u << (p & 31));
+    if (one_slot) {
+        if (tid < n) {
+            pos[tid] = p_own;
+            atomicOr(&bm[p_own >> 5], 1u << (p_own & 31));
+        }
+    } else {
+        for (int s = tid; s < n; s += NT) {
+            const int p = (app && s == n0) ? a.step : S.pos[s];
+            pos[s] = p;
+            atomicOr(&bm[p >> 5], 1u << (p & 31));
+        }
+    }
+    // the K rows go out once the positions are in (a wait for a position
+    // would otherwise also wait for them); the empty asm completes the
+    // position's load on every path, so that no later wait counts the rows
+    asm volatile("" ::"v"(p_own));
+    if (ahead && tid < n_ahead) {
+        const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + tid) * D);
+#pragma unroll
+        for (int c = 0; c < (kRowAhead ? kRow16 : 1); ++c) krow[c] = kr[c];
     }
     __syncthreads();
     {
@@ -525,10 +599,12 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
         if (w0 + 1 < nw) wpre[w0 + 1] = ex + c0;
     }
     __syncthreads();
+    int r_own = -1;  // rank of this thread's slot (one slot per thread)
     for (int s = tid; s < n; s += NT) {
         const int p = pos[s];
         const int r = wpre[p >> 5] + __popc(bm[p >> 5] & ((1u << (p & 31)) - 1u));
         order[r] = (uint16_t)s;
+        r_own = r;
     }
     __syncthreads();
 
@@ -607,36 +683,62 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
                 if (tid < D) qs[tid] = qacc;
             }
             __syncthreads();
-            for (int r = r_lo + tid; r < r_hi; r += NT) {
-                const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + order[r]) * D);
-                double acc = 0.0;
-                // half a row in flight at a time keeps the kernel under 64
-                // VGPRs (eight blocks per CU), which pays more than one
-                // round trip per row
-                constexpr int HR = kRow16 / 2;
+            if (ahead) {
+                // thread s scores its own slot from the row it loaded
+                if (tid < n && r_own >= r_lo && r_own < r_hi) {
+                    if (tid >= n_ahead) {
+                        const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + tid) * D);
 #pragma unroll
-                for (int half = 0; half < 2; ++half) {
-                    uint4 v[HR];
+                        for (int c = 0; c < (kRowAhead ? kRow16 : 1); ++c) krow[c] = kr[c];
+                    }
+                    double acc = 0.0;
 #pragma unroll
-                    for (int c = 0; c < HR; ++c) v[c] = kr[half * HR + c];
-#pragma unroll
-                    for (int c = 0; c < HR; ++c) {
-                        const uint32_t wv[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
-                        const int i0 = 8 * (half * HR + c);
+                    for (int c = 0; c < (kRowAhead ? kRow16 : 1); ++c) {
+                        const uint32_t wv[4] = {krow[c].x, krow[c].y, krow[c].z, krow[c].w};
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
-                            acc = acc + qs[i0 + 2 * e] * (double)bf_lo(wv[e]);
-                            acc = acc + qs[i0 + 2 * e + 1] * (double)bf_hi(wv[e]);
+                            acc = acc + qs[8 * c + 2 * e] * (double)bf_lo(wv[e]);
+                            acc = acc + qs[8 * c + 2 * e + 1] * (double)bf_hi(wv[e]);
                         }
                     }
+                    sig[r_own] = acc;
                 }
-                sig[r] = acc;
+            } else {
+                for (int r = r_lo + tid; r < r_hi; r += NT) {
+                    const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + order[r]) * D);
+                    double acc = 0.0;
+                    // half a row in flight at a time keeps the kernel under 64
+                    // VGPRs (eight blocks per CU), which pays more than one
+                    // round trip per row
+                    constexpr int HR = kRow16 / 2;
+#pragma unroll
+                    for (int half = 0; half < 2; ++half) {
+                        uint4 v[HR];
+#pragma unroll
+                        for (int c = 0; c < HR; ++c) v[c] = kr[half * HR + c];
+#pragma unroll
+                        for (int c = 0; c < HR; ++c) {
+                            const uint32_t wv[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+                            const int i0 = 8 * (half * HR + c);
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                acc = acc + qs[i0 + 2 * e] * (double)bf_lo(wv[e]);
+                                acc = acc + qs[i0 + 2 * e + 1] * (double)bf_hi(wv[e]);
+                            }
+                        }
+                    }
+                    sig[r] = acc;
+                }
             }
             }
             __syncthreads();
             // per part, evict the m lowest by (score, position)
-            select_lowest<NT>(sig, order, evict, 0, n_long, m_long, tid);
-            select_lowest<NT>(sig, order, evict, n_long, T, m_near, tid);
+            if (NT >= 512 && T <= NT / 4) {  // (256-thread blocks keep eight per CU)
+                select_small<NT>(sig, order, evict, n_long, T, m_long, m_near, tid);
+            } else {
+                select_lowest<NT>(sig, order, evict, 0, n_long, m_long, tid);
+                select_lowest<NT>(sig, order, evict, n_long, T, m_near, tid);
+            }
         }
     }
     __syncthreads();
