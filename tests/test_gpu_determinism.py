@@ -52,3 +52,20 @@ def test_run_twice_bitwise(wl, n_steps):
         assert torch.equal(a["out"][(t, l)], b["out"][(t, l)]), ("out", t, l)
     print(f"{wl.name}: {len(steps)} steps x {len(inp.layers)} layers bitwise identical over two "
           f"runs", flush=True)
+
+
+def test_deep_merge_trees_run_twice_bitwise():
+    # chunk counts 1..24 per head (merge trees of up to five levels)
+    import numpy as np
+    from test_gpu_edges import DEEP_TREE_BUDGETS, DEEP_TREE_STEPS, DEEP_TREES
+    wl = DEEP_TREES
+    inp = DeviceInputs(wl, layers=[0])
+    inp.override[0] = torch.as_tensor(np.asarray(DEEP_TREE_BUDGETS, dtype=np.int32).reshape(-1),
+                                      device="cuda")
+    a = _run(wl, inp, DEEP_TREE_STEPS, wl.num_visual)
+    b = _run(wl, inp, DEEP_TREE_STEPS, wl.num_visual)
+    for (t, l) in a["out"]:
+        assert torch.equal(a["out"][(t, l)], b["out"][(t, l)]), ("out", t, l)
+    for (t, l) in a["snap"]:
+        for x, y in zip(a["snap"][(t, l)], b["snap"][(t, l)]):
+            assert torch.equal(x, y), ("retained", t, l)

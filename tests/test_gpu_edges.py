@@ -111,6 +111,22 @@ def test_few_long_heads_split_d64():
     _run(wl, budgets=[[1000, 900]], steps=[0, 300, 599, 600, 601, 800, 1023])
 
 
+# 2 heads of d = 128 that grow to 3,000 tokens before grouping and keep up to
+# 3,500 after it: before grouping the layer's chunk table cuts them into
+# 128-token chunks (every count from 1 to 24 as they grow: merge trees of up
+# to five levels, most of them not full), after it into 512-token chunks (up
+# to 8)
+DEEP_TREES = W.TINY.with_(heads=2, head_dim=128, grid_rows=64, grid_cols=64, period=64,
+                          group_threshold=3000, budget_mode=W.BUDGET_OVERRIDE)
+DEEP_TREE_BUDGETS = [[3500, 1800]]
+DEEP_TREE_STEPS = [0, 95, 96, 127, 223, 351, 500, 863, 1000, 1500, 2047, 2048, 2998, 2999, 3000,
+                   3001, 3063, 3064, 3065, 4095]
+
+
+def test_deep_merge_trees_d128():
+    _run(DEEP_TREES, budgets=DEEP_TREE_BUDGETS, steps=DEEP_TREE_STEPS)
+
+
 def test_large_logits():
     # amplitudes x4: a planted head's logit for its own position is ~600 nats
     # (exp overflows fp32 past ~88), so every merge of the softmax -- passes,
