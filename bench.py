@@ -20,6 +20,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -57,10 +58,12 @@ def parse():
                    help="approximate CPU work of the oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
     # every launch timed with events costs a few microseconds of the whole
-    # job's time; 64 is prime to the update periods of the workloads (24, 49,
-    # 65), so the sampled steps still include update steps and full-cache steps
-    p.add_argument("--timing-every", type=int, default=64,
-                   help="time the launches of every n-th step")
+    # job's time, so only every n-th step is timed; by default n is the
+    # smallest stride from 64 up that is prime to the workload's update period
+    # (64 at periods 49 and 65, 65 at period 24), so that the sampled steps
+    # include update steps as well as the others
+    p.add_argument("--timing-every", type=int, default=None,
+                   help="time the launches of every n-th step (default: see timing_stride)")
     p.add_argument("--copy-probe", action="store_true",
                    help="only run a plain 512 MiB device copy five times (calibrates the HBM "
                         "byte counters of a profiler run) and exit")
@@ -443,6 +446,19 @@ KIND_NAMES = ["k_attn<d, append> (headkv_decode_step, compressed cache)",
               "k_update_attn<d> (append + periodic update + attention, one launch)"]
 
 
+def timing_stride(requested, period: int) -> int:
+    """The stride of the timed steps: as requested, else the smallest from 64
+    up that is prime to the update period (a stride sharing a factor with it
+    can miss every update step: 64 and 24 at Janus and LlamaGen, whose update
+    steps are all odd)."""
+    if requested:
+        return requested
+    s = 64
+    while math.gcd(s, period) != 1:
+        s += 1
+    return s
+
+
 def launches_per_generation(wl, fused_update: bool):
     """Launches of each timed kind in one generation (all layers): the
     library times only every n-th step's launches, so the kinds' shares of a
@@ -488,7 +504,8 @@ def run_workload(wl, args, steps: int, warmup: int, labels_mode: str = "headkv",
     # timed region: whole generations, the step loop in the library.  Every
     # `timing_every`-th step's launches are timed with HIP events that take
     # the kernel's own start and end timestamps (every prefill launch too)
-    per_gen = ((wl.num_visual + args.timing_every - 1) // args.timing_every * 2 + 1) * wl.layers
+    te = timing_stride(args.timing_every, wl.period)
+    per_gen = ((wl.num_visual + te - 1) // te * 2 + 1) * wl.layers
     B.headkv_timing_reserve(sess.h, per_gen * steps)
     B.headkv_timing_collect(sess.h)              # discard warm-up records
     torch.cuda.synchronize()
@@ -498,7 +515,7 @@ def run_workload(wl, args, steps: int, warmup: int, labels_mode: str = "headkv",
     t_start = time.perf_counter()
     marks[0].record()
     for i in range(steps):
-        run_generation_native(sess, inp, outs, timing_every=args.timing_every,
+        run_generation_native(sess, inp, outs, timing_every=te,
                               label_override=labels, prefill_out=pre_out)
         marks[i + 1].record()
         say(f"# {wl.name} step {i + 1}/{steps} issued")
@@ -641,7 +658,7 @@ def main():
         "traffic": (measured_traffic() if headline and dominant == KIND_NAMES[0] else None),
         "kernel": dominant.replace("<d", f"<{wl.head_dim}"),
         "frac_events": achieved / HBM_PEAK_GBPS,
-        "timed_every_nth_step": args.timing_every,
+        "timed_every_nth_step": timing_stride(args.timing_every, wl.period),
         "launches": dom["launches_timed"],
         "avg_launch_us": dom["avg_us"],
         "alg_bytes_per_launch": dom["alg_bytes_per_launch"],

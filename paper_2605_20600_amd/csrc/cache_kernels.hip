@@ -252,12 +252,13 @@ __device__ void select_lowest(const double* sig, const uint16_t* order, uint8_t*
 }
 
 // The same two selections as select_lowest on parts [0, n_long) and
-// [n_long, T), when T <= NT / 4: four threads (consecutive lanes) count the
-// entries of an entry's part that come before it by (score, rank), and the
-// entry leaves if fewer than its part's m do.  One pass over the part instead
-// of up to eight radix passes with their barriers; the count grows with the
-// part's size, so larger parts keep the radix select.  A part is ranked only
-// if it keeps some and loses some entries (the only parts whose scores exist).
+// [n_long, T), when T <= NT / 2: Q = 4 (T <= NT / 4) or 2 consecutive lanes
+// count the entries of an entry's part that come before it by (score, rank),
+// and the entry leaves if fewer than its part's m do.  One pass over the part
+// instead of up to eight radix passes with their barriers; the count grows
+// with the part's size, so larger parts keep the radix select.  A part is
+// ranked only if it keeps some and loses some entries (the only parts whose
+// scores exist).
 template <int NT>
 __device__ void select_small(double* sig, const uint16_t* order, uint8_t* evict, int n_long,
                              int T, int m_long, int m_near, int tid) {
@@ -274,7 +275,10 @@ __device__ void select_small(double* sig, const uint16_t* order, uint8_t* evict,
         if (tid < T && mq > 0 && mq < hi - lo) key[tid] = score_key(sig[tid]);
     }
     __syncthreads();
-    const int r = tid >> 2, q = tid & 3;
+    const bool four = T <= NT / 4;
+    const int Q = four ? 4 : 2;
+    const int r = four ? tid >> 2 : tid >> 1;
+    const int q = four ? tid & 3 : tid & 1;
     int lo, hi, mq;
     part_of(r, lo, hi, mq);
     if (r >= T || mq <= 0) return;
@@ -282,17 +286,22 @@ __device__ void select_small(double* sig, const uint16_t* order, uint8_t* evict,
         if (q == 0) evict[order[r]] = 1;
         return;
     }
-    // entries before r count when not greater, those after when less
+    // entries before r come before it unless greater, those after only if
+    // less: count the greater ones before r and the lesser ones after it
     const uint64_t kr = key[r];
-    int c = 0;
-#pragma unroll 4
-    for (int j = lo + q; j < hi; j += 4) {
-        const uint64_t kj = key[j];
-        c += (j < r ? kj <= kr : kj < kr) ? 1 : 0;
+    int j = lo + q, before = 0, greater = 0;
+    for (; j < r; j += Q) {
+        greater += kr < key[j] ? 1 : 0;
+        ++before;
     }
-    // the four lanes of an entry are all here
+    if (j == r) j += Q;
+    int less = 0;
+#pragma unroll 4
+    for (; j < hi; j += Q) less += key[j] < kr ? 1 : 0;
+    int c = before - greater + less;
+    // the Q lanes of an entry are all here
     c += __shfl_xor(c, 1);
-    c += __shfl_xor(c, 2);
+    if (four) c += __shfl_xor(c, 2);
     if (q == 0 && c < mq) evict[order[r]] = 1;
 }
 
@@ -549,12 +558,12 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
                              : L.kv + L.seg_off[h];
     SegPtrs S = seg_ptrs(src_seg, C, src_cap, D);
     // With at most one slot per thread, thread s loads its slot's position
-    // now, and, for a global head that scores (NT >= 512: registers for a
-    // whole row), its K row right after the positions, so that their round
+    // now, and, for a global head that scores (with registers for a whole row:
+    // NT >= 512, or d = 64), its K row right after the positions, so that their round
     // trips overlap the ranking and the window sum.  The appended row is still
     // being stored: its position comes from the step, its row is read when it
     // is scored.
-    constexpr bool kRowAhead = NT >= 512 && !ATTN_SUM;
+    constexpr bool kRowAhead = (NT >= 512 || D <= 64) && !ATTN_SUM;
     const bool one_slot = n <= NT;
     const int n_ahead = app ? n0 : n;
     const bool ahead = kRowAhead && window && one_slot;
@@ -733,7 +742,7 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
             }
             __syncthreads();
             // per part, evict the m lowest by (score, position)
-            if (NT >= 512 && T <= NT / 4) {  // (256-thread blocks keep eight per CU)
+            if (T <= NT / 2) {
                 select_small<NT>(sig, order, evict, n_long, T, m_long, m_near, tid);
             } else {
                 select_lowest<NT>(sig, order, evict, 0, n_long, m_long, tid);
