@@ -252,16 +252,17 @@ __device__ void select_lowest(const double* sig, const uint16_t* order, uint8_t*
 }
 
 // The same two selections as select_lowest on parts [0, n_long) and
-// [n_long, T), when T <= NT / 2: Q = 4 (T <= NT / 4) or 2 consecutive lanes
-// count the entries of an entry's part that come before it by (score, rank),
+// [n_long, T), when T <= NT / Q: Q consecutive lanes (4 or 2) count the
+// entries of an entry's part that come before it by (score, rank),
 // and the entry leaves if fewer than its part's m do.  One pass over the part
 // instead of up to eight radix passes with their barriers; the count grows
 // with the part's size, so larger parts keep the radix select.  A part is
 // ranked only if it keeps some and loses some entries (the only parts whose
 // scores exist).
-template <int NT>
+template <int NT, int Q>
 __device__ void select_small(double* sig, const uint16_t* order, uint8_t* evict, int n_long,
                              int T, int m_long, int m_near, int tid) {
+    static_assert(Q == 2 || Q == 4, "two or four lanes per entry");
     uint64_t* key = reinterpret_cast<uint64_t*>(sig);  // keys replace the scores in place
     auto part_of = [&](int r, int& lo, int& hi, int& mq) {
         const bool lng = r < n_long;
@@ -275,10 +276,7 @@ __device__ void select_small(double* sig, const uint16_t* order, uint8_t* evict,
         if (tid < T && mq > 0 && mq < hi - lo) key[tid] = score_key(sig[tid]);
     }
     __syncthreads();
-    const bool four = T <= NT / 4;
-    const int Q = four ? 4 : 2;
-    const int r = four ? tid >> 2 : tid >> 1;
-    const int q = four ? tid & 3 : tid & 1;
+    const int r = tid / Q, q = tid % Q;
     int lo, hi, mq;
     part_of(r, lo, hi, mq);
     if (r >= T || mq <= 0) return;
@@ -286,22 +284,17 @@ __device__ void select_small(double* sig, const uint16_t* order, uint8_t* evict,
         if (q == 0) evict[order[r]] = 1;
         return;
     }
-    // entries before r come before it unless greater, those after only if
-    // less: count the greater ones before r and the lesser ones after it
+    // entries before r count when not greater, those after when less
     const uint64_t kr = key[r];
-    int j = lo + q, before = 0, greater = 0;
-    for (; j < r; j += Q) {
-        greater += kr < key[j] ? 1 : 0;
-        ++before;
-    }
-    if (j == r) j += Q;
-    int less = 0;
+    int c = 0;
 #pragma unroll 4
-    for (; j < hi; j += Q) less += key[j] < kr ? 1 : 0;
-    int c = before - greater + less;
+    for (int j = lo + q; j < hi; j += Q) {
+        const uint64_t kj = key[j];
+        c += (j < r ? kj <= kr : kj < kr) ? 1 : 0;
+    }
     // the Q lanes of an entry are all here
     c += __shfl_xor(c, 1);
-    if (four) c += __shfl_xor(c, 2);
+    if (Q == 4) c += __shfl_xor(c, 2);
     if (q == 0 && c < mq) evict[order[r]] = 1;
 }
 
@@ -742,8 +735,10 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
             }
             __syncthreads();
             // per part, evict the m lowest by (score, position)
-            if (T <= NT / 2) {
-                select_small<NT>(sig, order, evict, n_long, T, m_long, m_near, tid);
+            if (T <= NT / 4) {
+                select_small<NT, 4>(sig, order, evict, n_long, T, m_long, m_near, tid);
+            } else if (T <= NT / 2) {
+                select_small<NT, 2>(sig, order, evict, n_long, T, m_long, m_near, tid);
             } else {
                 select_lowest<NT>(sig, order, evict, 0, n_long, m_long, tid);
                 select_lowest<NT>(sig, order, evict, n_long, T, m_near, tid);
