@@ -3,21 +3,27 @@
 // j <= i) V for the C prefix tokens of every (b, h), on the MFMA units of
 // gfx950.
 //
-// One wavefront per 32 queries, with no LDS and no block barrier.  For each
-// tile of 32 keys:
-//   S^T = K_tile Q^T   32x32x16 bf16 MFMAs over d (A = key rows, B = the
-//                      wavefront's query rows, held in registers), so that a
-//                      lane holds 16 of the 32 scores of one query and the
-//                      other 16 sit in lane l ^ 32;
+// A block of 4 wavefronts takes 128 queries of one head, one wavefront per 32
+// of them.  The keys arrive in blocks of 128: the block's threads load one
+// into LDS together (K and V rows, padded by 16 bytes against bank conflicts)
+// with every load issued at once, so the head's keys cost one memory round
+// trip per 128 rather than one per 32-key tile and wavefront.  For each tile
+// of 32 keys at or before its queries, a wavefront computes
+//   S^T = K_tile Q^T   32x32x16 bf16 MFMAs over d (A = key rows from LDS,
+//                      B = the wavefront's query rows, held in registers), so
+//                      that a lane holds 16 of the 32 scores of one query and
+//                      the other 16 sit in lane l ^ 32;
 //   online softmax     per query in fp32 (exp2 of pre-scaled scores), the
 //                      running max shared by the lane pair;
 //   O^T += V^T P^T     32x32x8 bf16 MFMAs: the score accumulators, rounded to
-//                      bf16, are exactly the B operand of this shape; the V
-//                      tile is loaded with 16-byte loads (issued before the
-//                      score MFMAs) into the wavefront's own LDS rows, from
-//                      which each lane reads its 4 keys of one dim.
+//                      bf16, are exactly the B operand of this shape; each
+//                      lane reads its 4 keys of one dim from the LDS V rows.
 // The normaliser sums the bf16-rounded weights that multiply V.  The same
-// launch stores the prefix keys and values into the cache (headkv_prefill).
+// launch stores the prefix keys and values into the cache (headkv_prefill):
+// the block of query tile t writes key block t from the registers it loaded
+// it into.  Prefixes shorter than 128 tokens, where most of a key block would
+// be clamped rows, take k_prefill_attn_tiles instead: each wavefront loads its
+// own 32-key tiles (the same MFMA steps).
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -48,6 +54,168 @@ __device__ __forceinline__ bf16x8_t load8(const uint16_t* p) {
     return __builtin_bit_cast(bf16x8_t, w);
 }
 
+// grid: ceil(C / 128) x B*H blocks, the query tiles of a head adjacent;
+// block: 256 threads = 4 wavefronts of 32 queries
+// Each block also does Step 1's cache work for its head: the block of the
+// first query tile resets the head's layer state, and every block stores the
+// keys and values of its own 128 prefix rows into the cache.
+template <int D>
+__global__ __launch_bounds__(256) void k_prefill_attn_keys(LayerDev L, int nheads,
+                                                      const uint16_t* __restrict__ qc,
+                                                      const uint16_t* __restrict__ kc,
+                                                      const uint16_t* __restrict__ vc,
+                                                      float* __restrict__ out, int C,
+                                                      float qscale, int64_t seg_bytes,
+                                                      int dense_cap, int dense_chunks) {
+    constexpr int KS = D / 16;            // 32x32x16 steps over d
+    constexpr int MB = D / 32;            // 32-dim blocks of the output
+    constexpr int CH = D / 8;             // 16-byte pieces of a row
+    constexpr int PER = 128 * CH / 256;   // pieces of a 128-key block per thread (K or V)
+    constexpr int PITCH = D + 8;          // LDS row pitch in bf16
+    __shared__ __align__(16) uint16_t ks[128 * PITCH];
+    __shared__ __align__(16) uint16_t vs[128 * PITCH];
+    const int tiles = (C + 127) / 128;
+    const int bh = blockIdx.x / tiles;
+    const int tile = blockIdx.x - bh * tiles;
+    prefill_head(L, bh, nheads, C, D, kc, vc, seg_bytes, dense_cap, dense_chunks, 0, 0, tile == 0,
+                 threadIdx.x, 256);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int q0 = tile * 128 + wave * 32;
+    const bool active = q0 < C;  // a wavefront past C still loads and meets the barriers
+    const int half = lane >> 5, j = lane & 31;  // j: this lane's query (and key row of a tile)
+    const size_t base = (size_t)bh * C * D;
+    const uint16_t* Q = qc + base;
+    const uint4* K4 = reinterpret_cast<const uint4*>(kc + base);
+    const uint4* V4 = reinterpret_cast<const uint4*>(vc + base);
+    const int qrow = min(q0 + j, C - 1);
+    bf16x8_t qb[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) qb[s] = load8(Q + (size_t)qrow * D + 16 * s + 8 * half);
+
+    f32x16_t acc[MB];
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[mb][r] = 0.f;
+    float m = -INFINITY, lsum = 0.f;
+    const int q = q0 + j;  // this lane's query
+    const SegPtrs cache = seg_ptrs(L.kv + (int64_t)bh * seg_bytes, C, dense_cap, D);
+    uint4* cK = reinterpret_cast<uint4*>(cache.K);
+    uint4* cV = reinterpret_cast<uint4*>(cache.V);
+    for (int kb = 0; kb <= tile; ++kb) {
+        // keys kb*128 .. kb*128 + 127 (rows past C clamped to C - 1: finite,
+        // and masked by the causal mask since every query is below C).  The
+        // barrier comes first, and every row is loaded and written: otherwise
+        // the compiler keeps the loaded rows in scratch memory, or sinks each
+        // load into the branch that uses it and waits for them one at a time.
+        if (kb > 0) __syncthreads();  // every wavefront is done with the previous block
+        uint4 kr[PER], vr[PER];
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int c = tid + 256 * i, row = c / CH, col = c % CH;
+            const size_t key = (size_t)min(kb * 128 + row, C - 1);
+            kr[i] = K4[key * CH + col];
+            vr[i] = V4[key * CH + col];
+        }
+        // every load out before the first write: the empty asm makes the
+        // loaded values opaque, so that the register allocator cannot reload
+        // them one at a time next to their writes
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            asm volatile("" : "+v"(kr[i].x), "+v"(kr[i].y), "+v"(kr[i].z), "+v"(kr[i].w));
+            asm volatile("" : "+v"(vr[i].x), "+v"(vr[i].y), "+v"(vr[i].z), "+v"(vr[i].w));
+        }
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int c = tid + 256 * i, row = c / CH, col = c % CH;
+            *reinterpret_cast<uint4*>(ks + row * PITCH + col * 8) = kr[i];
+            *reinterpret_cast<uint4*>(vs + row * PITCH + col * 8) = vr[i];
+        }
+        if (kb == tile) {  // this block's own prefix rows into the cache
+#pragma unroll
+            for (int i = 0; i < PER; ++i) {
+                const int c = tid + 256 * i, row = c / CH, col = c % CH;
+                const int key = kb * 128 + row;
+                if (key < C) {
+                    cK[(size_t)key * CH + col] = kr[i];
+                    cV[(size_t)key * CH + col] = vr[i];
+                }
+            }
+        }
+        __syncthreads();
+        if (!active) continue;
+        for (int t = 0; t < 4; ++t) {
+            const int k0 = kb * 128 + 32 * t;
+            if (k0 > q0 + 31 || k0 >= C) break;  // causal: tiles at or before the queries
+            const uint16_t* kt = ks + (32 * t) * PITCH;
+            const uint16_t* vt = vs + (32 * t) * PITCH;
+            // S^T[key i][query j] for keys k0 .. k0 + 31
+            f32x16_t st;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) st[r] = 0.f;
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                st = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    *reinterpret_cast<const bf16x8_t*>(kt + j * PITCH + 16 * s + 8 * half), qb[s],
+                    st, 0, 0, 0);
+            // keys of accumulator r: k0 + 8 (r / 4) + 4 half + r % 4; causal mask
+            float mx = m;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = k0 + 8 * (r / 4) + 4 * half + (r & 3);
+                st[r] = key <= q ? st[r] * qscale : -INFINITY;
+                mx = fmaxf(mx, st[r]);
+            }
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float f = __builtin_amdgcn_exp2f(m - mx);  // m = -inf gives 0
+            m = mx;
+            lsum *= f;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[mb][r] *= f;
+            // weights, rounded to bf16: B operands of the four 32x32x8 steps
+            bf16x4_t pb[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint16_t w = bf16_rne(__builtin_amdgcn_exp2f(st[4 * g + e] - mx));
+                    lsum += __uint_as_float((uint32_t)w << 16);
+                    pb[g][e] = (short)w;
+                }
+            // O^T[dim][query] += V^T[dim][key] P^T[key][query]
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    bf16x4_t va;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        va[e] = (short)vt[(8 * g + 4 * half + e) * PITCH + 32 * mb + j];
+                    acc[mb] = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(va, pb[g], acc[mb], 0, 0, 0);
+                }
+        }
+    }
+    if (!active) return;
+    lsum += __shfl_xor(lsum, 32);
+    if (q >= C) return;
+    const float inv = 1.f / lsum;
+    float* o = out + base + (size_t)q * D;
+    // accumulator r of block mb: dim 32 mb + 8 (r / 4) + 4 half + r % 4
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            float4 v;
+            v.x = acc[mb][4 * g] * inv;
+            v.y = acc[mb][4 * g + 1] * inv;
+            v.z = acc[mb][4 * g + 2] * inv;
+            v.w = acc[mb][4 * g + 3] * inv;
+            *reinterpret_cast<float4*>(o + 32 * mb + 8 * g + 4 * half) = v;
+        }
+}
+
 // A tile of 32 keys: the A operands of S^T (key row j, 16 dims per step, this
 // half's 8 of them) and 16-byte pieces of the V rows.
 template <int D>
@@ -72,13 +240,12 @@ __device__ __forceinline__ KeyTile<D> load_tile(const uint16_t* K, const uint16_
     return t;
 }
 
-// grid: ceil(C / 128) x B*H blocks, the query tiles of a head adjacent;
-// block: 256 threads = 4 wavefronts of 32 queries
-// Each block also does Step 1's cache work for its head: the block of the
-// first query tile resets the head's layer state, and every block copies the
-// keys and values of its own 128 prefix rows into the cache.
+// Prefixes shorter than 128 tokens (one query tile per head; most of a key
+// block would be clamped rows): each wavefront loads its own key tiles, one
+// at a time, the V tile through its own LDS rows.  Grid and block as for
+// k_prefill_attn_keys; the block copies its head's prefix rows into the cache.
 template <int D>
-__global__ __launch_bounds__(256) void k_prefill_attn(LayerDev L, int nheads,
+__global__ __launch_bounds__(256) void k_prefill_attn_tiles(LayerDev L, int nheads,
                                                       const uint16_t* __restrict__ qc,
                                                       const uint16_t* __restrict__ kc,
                                                       const uint16_t* __restrict__ vc,
@@ -199,12 +366,17 @@ int launch_prefill_attn(const LayerDev& L, const Shape& s, const uint16_t* qc, c
     const float qscale = (float)(1.4426950408889634 / std::sqrt((double)s.d));
     hipStream_t st = (hipStream_t)stream;
     hipEvent_t e0 = static_cast<hipEvent_t>(ev_start), e1 = static_cast<hipEvent_t>(ev_stop);
-    if (s.d == 128)
-        hipExtLaunchKernelGGL(k_prefill_attn<128>, grid, block, 0, st, e0, e1, 0, L, s.BH, qc, kc,
-                              vc, out, s.C, qscale, dense_seg_bytes, dense_cap, dense_chunks);
-    else
-        hipExtLaunchKernelGGL(k_prefill_attn<64>, grid, block, 0, st, e0, e1, 0, L, s.BH, qc, kc,
-                              vc, out, s.C, qscale, dense_seg_bytes, dense_cap, dense_chunks);
+#define HEADKV_PREFILL_LAUNCH(KERNEL)                                                        \
+    hipExtLaunchKernelGGL(KERNEL, grid, block, 0, st, e0, e1, 0, L, s.BH, qc, kc, vc, out, s.C, \
+                          qscale, dense_seg_bytes, dense_cap, dense_chunks)
+    if (s.C >= 128) {
+        if (s.d == 128) HEADKV_PREFILL_LAUNCH(k_prefill_attn_keys<128>);
+        else HEADKV_PREFILL_LAUNCH(k_prefill_attn_keys<64>);
+    } else {
+        if (s.d == 128) HEADKV_PREFILL_LAUNCH(k_prefill_attn_tiles<128>);
+        else HEADKV_PREFILL_LAUNCH(k_prefill_attn_tiles<64>);
+    }
+#undef HEADKV_PREFILL_LAUNCH
     return last_error();
 }
 
