@@ -22,6 +22,12 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 
+# per source: the attention kernels take the arguments their first loads need
+# as leading plain arguments, preloaded into scalar registers at wave launch
+# (and so do the probe's kernels, which bound them)
+PRELOAD = ["-mllvm", "-amdgpu-kernarg-preload-count=16"]
+SOURCE_FLAGS = {"attn_kernels.hip": PRELOAD, "stream_probe.hip": PRELOAD}
+
 
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
@@ -37,7 +43,8 @@ def build(verbose: bool = False) -> str:
     objs = []
     for src in SOURCES:
         obj = os.path.join(out_dir, src + ".o")
-        cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-c",
+        cmd = [hipcc(), *HIPCC_FLAGS, *SOURCE_FLAGS.get(src, []), "-I",
+               os.path.join(ROOT, "include"), "-c",
                os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
@@ -50,7 +57,8 @@ def build(verbose: bool = False) -> str:
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
     tmp = PROBE + f".tmp{os.getpid()}"
-    cmd = [hipcc(), *HIPCC_FLAGS, os.path.join(CSRC, "stream_probe.hip"), "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, *SOURCE_FLAGS["stream_probe.hip"],
+           os.path.join(CSRC, "stream_probe.hip"), "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

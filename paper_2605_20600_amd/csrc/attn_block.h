@@ -179,7 +179,16 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
         h = (int)(it >> 8);
         t_begin = (int)(it & 255u) * TP;
     } else {
-        h = use_order ? L.order[order_base + item] : item;
+        // through a vector load: a scalar one would leave its wait at the
+        // join of the two paths, where it also waits for the kernel arguments
+        // still in flight, and the block's first metadata loads would follow
+        // them on the path without the order as well
+        h = item;
+        if (use_order) {
+            int lane0 = 0;
+            asm("" : "+v"(lane0));
+            h = __builtin_amdgcn_readfirstlane(L.order[order_base + item + lane0]);
+        }
         t_begin = 0;
     }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -191,12 +200,13 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     // just changed it), else the one in memory
     const int n = n_given >= 0 ? n_given : head_len(L, h);
     const int i0 = CHUNKED ? L.item_start[h] : 0;  // the head's first chunk slot
-    // Everything the first K/V load waits for comes in two rounds of scalar
-    // loads: the kernel arguments, then the metadata with the rest of them.
-    // Left to itself, the compiler fetches arguments late, each behind the
-    // previous wait (up to four rounds); an empty asm statement that takes
-    // these values pins them before any load that follows.  (Placed before the
-    // metadata loads, it would make them vector loads.)
+    // Everything the first K/V load waits for comes in one round of scalar
+    // loads when the kernel preloads its leading arguments (the metadata, with
+    // the rest of the arguments), else two (the arguments first).  Left to
+    // itself, the compiler fetches arguments late, each behind the previous
+    // wait (up to four rounds); an empty asm statement that takes these values
+    // pins them before any load that follows.  (Placed before the metadata
+    // loads, it would make them vector loads.)
     asm volatile("" ::"s"(q), "s"(seg), "s"(cap), "s"(n), "s"(C), "s"(pad_len), "s"(qscale));
     if (CHUNKED) asm volatile("" ::"s"(i0), "s"(part));
     if (APPEND) asm volatile("" ::"s"(a.k), "s"(a.v), "s"(L.qring), "s"(L.ring_len));

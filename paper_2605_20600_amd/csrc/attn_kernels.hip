@@ -31,11 +31,28 @@ namespace {
 using namespace dev;
 
 // 4 wavefronts per SIMD (16 per CU) at every block size: at most 128 VGPRs.
+// The arguments that the block's first loads need lead the list, as plain
+// pointers and an integer, so that they are preloaded into scalar registers
+// at wave launch: the first metadata loads then go out without waiting for
+// the kernel-argument fetch.  `sel` is the chunk table (chunked launches),
+// else the dispatch order from the launch's first head, or null for block i =
+// head i.  The same fields of L are not read.
 template <int D, bool APPEND, int T, bool CHUNKED, int TPR>
 __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_attn(
-    LayerDev L, int C, AppendArgs a, const uint16_t* __restrict__ q, float* __restrict__ out,
-    uint64_t* __restrict__ part, int use_order, int order_base, int pad_len, float qscale) {
-    attn_block<D, APPEND, T, CHUNKED, TPR>(L, C, a, q, out, part, use_order, order_base, pad_len,
+    char* kv, int64_t* seg_off, int32_t* len_n, int32_t* cap, const uint16_t* q, int32_t* sel,
+    int dn, LayerDev L, int C, AppendArgs a, float* __restrict__ out,
+    uint64_t* __restrict__ part, int pad_len, float qscale) {
+    LayerDev M = L;
+    M.kv = kv;
+    M.seg_off = seg_off;
+    M.n = len_n;
+    M.cap = cap;
+    M.dn = dn;
+    if (CHUNKED)
+        M.items = reinterpret_cast<uint32_t*>(sel);
+    else
+        M.order = sel;
+    attn_block<D, APPEND, T, CHUNKED, TPR>(M, C, a, q, out, part, sel != nullptr, 0, pad_len,
                                            qscale, (int)blockIdx.x);
 }
 
@@ -65,15 +82,17 @@ void attn_launch(const LayerDev& L, const Shape& s, const AppendArgs& a, const u
                  hipEvent_t ev1) {
     const float qscale = (float)(1.4426950408889634 / std::sqrt((double)D));
     const dim3 grid(CHUNKED ? p.items : p.heads), block(T);
+    int32_t* sel = CHUNKED ? reinterpret_cast<int32_t*>(L.items)
+                           : (p.use_order ? L.order + p.order_base : nullptr);
     // with events, they take the kernel's own start and end timestamps
     if (a.k != nullptr)
-        hipExtLaunchKernelGGL((k_attn<D, true, T, CHUNKED, TPR>), grid, block, 0, st, ev0, ev1, 0, L,
-                              s.C, a, q, out, partials, p.use_order, p.order_base, p.pad_len,
-                              qscale);
+        hipExtLaunchKernelGGL((k_attn<D, true, T, CHUNKED, TPR>), grid, block, 0, st, ev0, ev1, 0,
+                              L.kv, L.seg_off, L.n, L.cap, q, sel, L.dn, L, s.C, a, out, partials,
+                              p.pad_len, qscale);
     else
-        hipExtLaunchKernelGGL((k_attn<D, false, T, CHUNKED, TPR>), grid, block, 0, st, ev0, ev1, 0, L,
-                              s.C, a, q, out, partials, p.use_order, p.order_base, p.pad_len,
-                              qscale);
+        hipExtLaunchKernelGGL((k_attn<D, false, T, CHUNKED, TPR>), grid, block, 0, st, ev0, ev1, 0,
+                              L.kv, L.seg_off, L.n, L.cap, q, sel, L.dn, L, s.C, a, out, partials,
+                              p.pad_len, qscale);
 }
 
 template <int D, int T>
