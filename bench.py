@@ -99,12 +99,13 @@ def parse():
     return p.parse_args()
 
 
-# sources of the attention kernel: the profiler's byte counters stay valid
-# while these are unchanged
+# sources of the attention kernel and the script that holds its build flags:
+# the profiler's records stay valid while these are unchanged
 ATTN_SOURCES = ("paper_2605_20600_amd/csrc/attn_kernels.hip",
                 "paper_2605_20600_amd/csrc/attn_block.h",
                 "paper_2605_20600_amd/csrc/device_common.h",
-                "paper_2605_20600_amd/csrc/layout.h")
+                "paper_2605_20600_amd/csrc/layout.h",
+                "paper_2605_20600_amd/build.py")
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_attn_lumina768_b8_rho1-8_traffic.json")
 
 
