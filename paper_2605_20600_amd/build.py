@@ -22,11 +22,13 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
 
-# per source: the attention kernels take the arguments their first loads need
-# as leading plain arguments, preloaded into scalar registers at wave launch
-# (and so do the probe's kernels, which bound them)
+# per source: the attention kernels and the fused update + attention kernel
+# take the arguments their first loads need as leading plain arguments,
+# preloaded into scalar registers at wave launch (and so do the probe's
+# kernels, which bound them)
 PRELOAD = ["-mllvm", "-amdgpu-kernarg-preload-count=16"]
-SOURCE_FLAGS = {"attn_kernels.hip": PRELOAD, "stream_probe.hip": PRELOAD}
+SOURCE_FLAGS = {"attn_kernels.hip": PRELOAD, "cache_kernels.hip": PRELOAD,
+                "stream_probe.hip": PRELOAD}
 
 
 def hipcc() -> str:

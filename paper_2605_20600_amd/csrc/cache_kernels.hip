@@ -484,7 +484,10 @@ __device__ void attention_sum_scores(const LayerDev& L, const SegPtrs& S, int C,
 // (the Eq. 6 kernel stays under 64 VGPRs: eight 256-thread blocks per CU).
 // The update of head h by the block's NT threads (body of k_update and of the
 // fused update + attention kernel); returns the head's length afterwards.
-template <int D, bool ATTN_SUM, int G, int NT = kBlock>
+// FUSED: the block goes on to the attention, so it has the attention's 128
+// VGPRs: where no K row was loaded ahead, a whole row is scored per round
+// trip instead of half of one.
+template <int D, bool ATTN_SUM, int G, int NT = kBlock, bool FUSED = false>
 __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, const AppendArgs& a,
                                             const char* src_kv, int relayout,
                                             int64_t dense_seg_bytes, int dense_cap,
@@ -506,6 +509,10 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
     const int n0 = head_len(L, h);
     const int B = L.budget[h];
     const int local = L.label[h];
+    // the segment's metadata too, before the append's stores (after them, the
+    // compiler can no longer read it through the scalar cache)
+    const int cap_h = L.cap[h];
+    const int64_t seg_h = L.seg_off[h];
     // the step's append, then the update that follows it; the update takes the
     // new token's position and query from the append's own values rather than
     // reading them back from memory
@@ -529,26 +536,14 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
     }
     // Eq. 6 window of a global head that evicts: steps w0..step of the query
     // ring (the step's own query, when this kernel appends it, from the
-    // append's values).  The first kRingChunk rows are loaded now, so that
-    // their round trip overlaps the ranking below.
-    constexpr int PER = (kRingChunk * kRow16 + NT - 1) / NT;
+    // append's values)
     const int w0 = step - L.ring_len + 1 > 0 ? step - L.ring_len + 1 : 0;
     const int wlast = app ? step - 1 : step;  // last step read from the ring
     const bool window = !ATTN_SUM && !local && M > 0;
-    uint4 wbuf[PER];
-    if (window) {
-        const int cn = wlast + 1 - w0 < kRingChunk ? wlast + 1 - w0 : kRingChunk;
-#pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int v = tid + k * NT;
-            if (v < cn * kRow16)
-                wbuf[k] = reinterpret_cast<const uint4*>(ring_slot(L, D, h, w0 + v / kRow16))[v % kRow16];
-        }
-    }
 
-    const int src_cap = relayout ? dense_cap : L.cap[h];
+    const int src_cap = relayout ? dense_cap : cap_h;
     char* src_seg = relayout ? const_cast<char*>(src_kv) + (int64_t)h * dense_seg_bytes
-                             : L.kv + L.seg_off[h];
+                             : L.kv + seg_h;
     SegPtrs S = seg_ptrs(src_seg, C, src_cap, D);
     // With at most one slot per thread, thread s loads its slot's position
     // now, and, for a global head that scores (with registers for a whole row:
@@ -562,6 +557,25 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
     const bool ahead = kRowAhead && window && one_slot;
     int p_own = 0;
     if (one_slot && tid < n) p_own = (app && tid == n0) ? a.step : S.pos[tid];
+    // The window's first kRingChunk ring rows, loaded now so that their round
+    // trip overlaps the ranking.  Every thread loads (past the window's rows,
+    // and for a head without a window, the window's first piece again), so
+    // that no branch holds a load: the wait for the position before them
+    // then leaves them in flight.  16-byte pieces as a vector type: copies of
+    // the struct type were kept in scratch memory.
+    typedef unsigned int piece_t __attribute__((ext_vector_type(4)));
+    constexpr int PER = (kRingChunk * kRow16 + NT - 1) / NT;
+    piece_t wbuf[PER];
+    {
+        const int cw = wlast + 1 - w0 < kRingChunk ? wlast + 1 - w0 : kRingChunk;
+        const int cn = window ? cw : 0;
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int v0 = tid + k * NT;
+            const int v = v0 < cn * kRow16 ? v0 : 0;
+            wbuf[k] = reinterpret_cast<const piece_t*>(ring_slot(L, D, h, w0 + v / kRow16))[v % kRow16];
+        }
+    }
     uint4 krow[kRowAhead ? kRow16 : 1];
 
     // rank every occupied slot by its position: bitmap + prefix popcount
@@ -575,10 +589,25 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
             atomicOr(&bm[p_own >> 5], 1u << (p_own & 31));
         }
     } else {
-        for (int s = tid; s < n; s += NT) {
-            const int p = (app && s == n0) ? a.step : S.pos[s];
-            pos[s] = p;
-            atomicOr(&bm[p >> 5], 1u << (p & 31));
+        // PB positions per thread in flight at a time (slot 0 stands in for the
+        // slots past n, so that no branch holds a load)
+        constexpr int PB = 4;
+        for (int s0 = 0; s0 < n; s0 += PB * NT) {
+            int pv[PB];
+#pragma unroll
+            for (int k = 0; k < PB; ++k) {
+                const int s = s0 + tid + k * NT;
+                pv[k] = S.pos[s < n ? s : 0];
+            }
+#pragma unroll
+            for (int k = 0; k < PB; ++k) {
+                const int s = s0 + tid + k * NT;
+                if (s < n) {
+                    const int p = (app && s == n0) ? a.step : pv[k];
+                    pos[s] = p;
+                    atomicOr(&bm[p >> 5], 1u << (p & 31));
+                }
+            }
         }
     }
     // the K rows go out once the positions are in (a wait for a position
@@ -657,14 +686,14 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
                         for (int k = 0; k < PER; ++k) {
                             const int v = tid + k * NT;
                             if (v < cn * kRow16)
-                                wbuf[k] = reinterpret_cast<const uint4*>(
+                                wbuf[k] = reinterpret_cast<const piece_t*>(
                                     ring_slot(L, D, h, c0 + v / kRow16))[v % kRow16];
                         }
                     }
 #pragma unroll
                     for (int k = 0; k < PER; ++k) {
                         const int v = tid + k * NT;
-                        if (v < cn * kRow16) reinterpret_cast<uint4*>(stage)[v] = wbuf[k];
+                        if (v < cn * kRow16) reinterpret_cast<piece_t*>(stage)[v] = wbuf[k];
                     }
                     __syncthreads();
                     // eight LDS reads in flight ahead of the in-order adds (the
@@ -709,12 +738,14 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
                 for (int r = r_lo + tid; r < r_hi; r += NT) {
                     const uint4* kr = reinterpret_cast<const uint4*>(S.K + (size_t)(C + order[r]) * D);
                     double acc = 0.0;
-                    // half a row in flight at a time keeps the kernel under 64
-                    // VGPRs (eight blocks per CU), which pays more than one
-                    // round trip per row
-                    constexpr int HR = kRow16 / 2;
+                    // half a row in flight at a time keeps the update kernel
+                    // under 64 VGPRs (eight blocks per CU), which pays more
+                    // than one round trip per row; the fused kernel takes the
+                    // whole row unless the row loaded ahead holds registers
+                    constexpr int NH = (FUSED && !kRowAhead) ? 1 : 2;
+                    constexpr int HR = kRow16 / NH;
 #pragma unroll
-                    for (int half = 0; half < 2; ++half) {
+                    for (int half = 0; half < NH; ++half) {
                         uint4 v[HR];
 #pragma unroll
                         for (int c = 0; c < HR; ++c) v[c] = kr[half * HR + c];
@@ -830,19 +861,36 @@ __global__ __launch_bounds__(NT) void k_update(LayerDev L, int C, int N, AppendA
 // whose attention runs one T-thread block per head: the block updates its
 // head (Eq. 6 scores) with all its threads, then attends over the updated
 // cache with the length it has just computed.  The head comes from the
-// dispatch order when use_order.  At most 128 VGPRs, as the attention
-// kernels: 1024 / T blocks per CU.
+// dispatch order when `order` is not null.  At most 128 VGPRs, as the
+// attention kernels: 1024 / T blocks per CU.  The metadata tables the first
+// loads need, the order and the appended count lead the argument list as
+// plain pointers and an integer, preloaded into scalar registers at wave
+// launch (the same fields of L are not read); the order is read by a vector
+// load, whose wait stays on its own path.
 template <int D, int T, int TPR>
 __global__ __launch_bounds__(T) __attribute__((amdgpu_waves_per_eu(4))) void k_update_attn(
-    LayerDev L, int C, int N, AppendArgs a, int recent_len, int rs_num, int rs_den, int u,
-    int step, int lds_cap, double sqrt_d, const uint16_t* __restrict__ q,
-    float* __restrict__ out, int use_order, int pad_len, float qscale) {
-    const int h = use_order ? L.order[blockIdx.x] : (int)blockIdx.x;
-    const int n = update_block<D, false, 1, T>(L, C, N, a, nullptr, 0, 0, 0, recent_len,
+    int32_t* len_n, int32_t* budget, int32_t* label, int64_t* seg_off, int32_t* cap,
+    const int32_t* order, int dn, LayerDev L, int C, int N, AppendArgs a, int recent_len,
+    int rs_num, int rs_den, int u, int step, int lds_cap, double sqrt_d,
+    const uint16_t* __restrict__ q, float* __restrict__ out, int pad_len, float qscale) {
+    LayerDev M = L;
+    M.n = len_n;
+    M.budget = budget;
+    M.label = label;
+    M.seg_off = seg_off;
+    M.cap = cap;
+    M.dn = dn;
+    int h = (int)blockIdx.x;
+    if (order != nullptr) {
+        int lane0 = 0;
+        asm("" : "+v"(lane0));
+        h = __builtin_amdgcn_readfirstlane(order[(int)blockIdx.x + lane0]);
+    }
+    const int n = update_block<D, false, 1, T, true>(M, C, N, a, nullptr, 0, 0, 0, recent_len,
                                                rs_num, rs_den, u, step, lds_cap, sqrt_d, h);
     __syncthreads();  // the rows the update moved are read by other threads
     const AppendArgs none{};
-    attn_block<D, false, T, false, TPR>(L, C, none, q, out, nullptr, 0, 0, pad_len, qscale, h,
+    attn_block<D, false, T, false, TPR>(M, C, none, q, out, nullptr, 0, 0, pad_len, qscale, h,
                                         n);
 }
 
@@ -966,9 +1014,11 @@ void update_attn_launch(const LayerDev& L, const Shape& s, const AppendArgs& a, 
     }();
     (void)lds_ok;
     const float qscale = (float)(1.4426950408889634 / sqrt_d);
-    hipExtLaunchKernelGGL((k_update_attn<D, T, TPR>), dim3(s.BH), dim3(T), lds, st, e0, e1, 0, L,
-                          s.C, s.N, a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q,
-                          out, use_order, pad_len, qscale);
+    hipExtLaunchKernelGGL((k_update_attn<D, T, TPR>), dim3(s.BH), dim3(T), lds, st, e0, e1, 0,
+                          L.n, L.budget, L.label, L.seg_off, L.cap,
+                          use_order ? L.order : static_cast<int32_t*>(nullptr), L.dn, L, s.C, s.N,
+                          a, recent_len, rs_num, rs_den, u, step, lds_cap, sqrt_d, q, out,
+                          pad_len, qscale);
 }
 
 template <int D, int T>
