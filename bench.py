@@ -99,22 +99,24 @@ def parse():
     return p.parse_args()
 
 
-# sources of the attention kernel and the script that holds its build flags:
-# the profiler's records stay valid while these are unchanged
+# sources of the attention kernel: the profiler's records stay valid while
+# these and the flags they are compiled with are unchanged
 ATTN_SOURCES = ("paper_2605_20600_amd/csrc/attn_kernels.hip",
                 "paper_2605_20600_amd/csrc/attn_block.h",
                 "paper_2605_20600_amd/csrc/device_common.h",
-                "paper_2605_20600_amd/csrc/layout.h",
-                "paper_2605_20600_amd/build.py")
+                "paper_2605_20600_amd/csrc/layout.h")
 TRAFFIC_RECORD = os.path.join(ROOT, "profiles", "k_attn_lumina768_b8_rho1-8_traffic.json")
 
 
 def attn_source_sha256() -> str:
     import hashlib
+    from paper_2605_20600_amd import build as lib_build
     h = hashlib.sha256()
     for rel in ATTN_SOURCES:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
+    flags = lib_build.HIPCC_FLAGS + lib_build.SOURCE_FLAGS.get("attn_kernels.hip", [])
+    h.update(" ".join(flags).encode())
     return h.hexdigest()
 
 
