@@ -12,9 +12,13 @@
 // Launches rotate over 32 buffers of S bytes, so that (as in a decode step
 // over 32 layers) the data is not in the 256 MB Infinity Cache when it is read.
 // Usage: stream_probe [MB per launch, default 48] [launches per case, 640].
-// Run it under rocprofv3 --kernel-trace --stats for the kernels' own
-// durations; it also prints the wall time per launch of each back-to-back
-// series from events around it.
+// For each case it prints the wall time per launch of a back-to-back series
+// (events around the series), then the mean duration of each launch of a
+// second series from its own start and stop events (hipExtLaunchKernelGGL,
+// the kernel's own timestamps, as the library's benchmark times its
+// kernels).  Run it under rocprofv3 --kernel-trace --stats for the
+// profiler's durations of the same kernels.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -88,37 +92,58 @@ int main(int argc, char** argv) {
     hipEvent_t a, b;
     CHECK(hipEventCreate(&a));
     CHECK(hipEventCreate(&b));
+    std::vector<hipEvent_t> e0(n), e1(n);
+    for (int i = 0; i < n; ++i) {
+        CHECK(hipEventCreate(&e0[i]));
+        CHECK(hipEventCreate(&e1[i]));
+    }
+    // launch(i, start, stop): null events for a plain launch
     auto series = [&](const char* name, auto launch) {
-        for (int i = 0; i < 64; ++i) launch(i);  // warm-up
+        for (int i = 0; i < 64; ++i) launch(i, nullptr, nullptr);  // warm-up
         CHECK(hipDeviceSynchronize());
         CHECK(hipEventRecord(a, nullptr));
-        for (int i = 0; i < n; ++i) launch(i);
+        for (int i = 0; i < n; ++i) launch(i, nullptr, nullptr);
         CHECK(hipEventRecord(b, nullptr));
         CHECK(hipEventSynchronize(b));
         CHECK(hipGetLastError());
         float ms = 0.f;
         CHECK(hipEventElapsedTime(&ms, a, b));
-        std::printf("%-44s %8.2f us per launch back to back\n", name, ms * 1e3 / n);
+        for (int i = 0; i < n; ++i) launch(i, e0[i], e1[i]);
+        CHECK(hipDeviceSynchronize());
+        CHECK(hipGetLastError());
+        double own = 0.0;
+        for (int i = 0; i < n; ++i) {
+            float t = 0.f;
+            CHECK(hipEventElapsedTime(&t, e0[i], e1[i]));
+            own += t;
+        }
+        std::printf("%-44s %8.2f us per launch back to back, %8.2f us per launch from its own events\n",
+                    name, ms * 1e3 / n, own * 1e3 / n);
         std::fflush(stdout);
     };
-    series("empty, 256 x 1024 threads", [&](int) {
-        hipLaunchKernelGGL(probe_empty<1024>, dim3(256), dim3(1024), 0, nullptr, out, 0);
+    series("empty, 256 x 1024 threads", [&](int, hipEvent_t s0, hipEvent_t s1) {
+        hipExtLaunchKernelGGL(probe_empty<1024>, dim3(256), dim3(1024), 0, nullptr, s0, s1, 0,
+                              out, 0);
     });
     for (size_t bytes : {mb << 20, 2 * (mb << 20)}) {
         const size_t units = bytes / 16;
         char name[96];
         const size_t pb1 = (units + 255) / 256;
         std::snprintf(name, sizeof name, "read %zu MB, 256 x 1024 threads", bytes >> 20);
-        series(name, [&](int i) {
-            hipLaunchKernelGGL((probe_read<1024, 12>), dim3(256), dim3(1024), 0, nullptr,
-                               buf[i % L], units, pb1, out);
+        series(name, [&](int i, hipEvent_t s0, hipEvent_t s1) {
+            hipExtLaunchKernelGGL((probe_read<1024, 12>), dim3(256), dim3(1024), 0, nullptr, s0,
+                                  s1, 0, buf[i % L], units, pb1, out);
         });
         const size_t pb8 = (units + max_blocks - 1) / max_blocks;
         std::snprintf(name, sizeof name, "read %zu MB, 2048 x 256 threads", bytes >> 20);
-        series(name, [&](int i) {
-            hipLaunchKernelGGL((probe_read<256, 12>), dim3(max_blocks), dim3(256), 0, nullptr,
-                               buf[i % L], units, pb8, out);
+        series(name, [&](int i, hipEvent_t s0, hipEvent_t s1) {
+            hipExtLaunchKernelGGL((probe_read<256, 12>), dim3(max_blocks), dim3(256), 0, nullptr,
+                                  s0, s1, 0, buf[i % L], units, pb8, out);
         });
+    }
+    for (int i = 0; i < n; ++i) {
+        CHECK(hipEventDestroy(e0[i]));
+        CHECK(hipEventDestroy(e1[i]));
     }
     for (auto p : buf) CHECK(hipFree(p));
     CHECK(hipFree(out));
