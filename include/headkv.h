@@ -53,7 +53,7 @@ typedef int32_t headkv_status;
 #define HEADKV_ERR_CAPACITY (-2)    /* a caller buffer is too small */
 #define HEADKV_ERR_STATE (-3)       /* call out of the documented order */
 #define HEADKV_ERR_HIP (-4)         /* a HIP runtime call or launch failed */
-#define HEADKV_ERR_UNSUPPORTED (-5) /* a shape this build does not handle */
+#define HEADKV_ERR_UNSUPPORTED (-5) /* a shape this library does not handle */
 
 /* Budget modes (Sec. 5.1, Implementation Details: global heads keep rho*N
  * tokens, local heads a small set of neighbouring tokens). */
@@ -85,7 +85,7 @@ typedef int32_t headkv_status;
                                      over the queries; keeps the last P queries
                                      of every head in the metadata buffer */
 
-/* Limits of this build. */
+/* Limits of this library. */
 #define HEADKV_MAX_VISUAL 16384  /* num_visual */
 #define HEADKV_MAX_PREFIX 2048   /* prefix_len */
 #define HEADKV_MAX_CAPACITY 4608 /* visual tokens one head can hold */
