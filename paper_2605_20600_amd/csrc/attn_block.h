@@ -109,6 +109,19 @@ __device__ __forceinline__ void chunk_merge(int h, int nch, int c, int i0, float
     }
 }
 
+// Partial logit of one lane: its NW words of q and of a K row, bf16 pairs,
+// multiplied and summed in fp32 (the products of bf16 values are exact in fp32)
+template <int NW>
+__device__ __forceinline__ float lane_dot(const uint32_t* qw, const Words<NW>& k) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    float dp = 0.f;
+#pragma unroll
+    for (int e = 0; e < NW; ++e)
+        dp = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, qw[e]),
+                                             __builtin_bit_cast(bf16x2_t, k.w[e]), dp, false);
+    return dp;
+}
+
 // Online-softmax update of one row's state with NT tokens t0 + j * ROWS + row
 // (those at or past t_end masked); k/v hold their d/16 elements of the lane.
 // The running max is the wavefront's (the same in all its rows), taken over
@@ -117,7 +130,8 @@ __device__ __forceinline__ void chunk_merge(int h, int nch, int c, int i0, float
 template <int D, int NT, int ROWS>
 __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec (&kk)[NT],
                                                 const typename AttnRegs<D>::Vec (&vv)[NT],
-                                                int t0, int row, int t_end, const float* qf,
+                                                int t0, int row, int t_end,
+                                                const uint32_t* qw, float qscale,
                                                 float& m, float& l, float* acc) {
     constexpr int NW = AttnRegs<D>::NW;
     constexpr int VPL = AttnRegs<D>::VPL;
@@ -125,13 +139,7 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
     float mx = m;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-        float dp = 0.f;
-#pragma unroll
-        for (int e = 0; e < NW; ++e) {
-            dp += qf[2 * e] * bf_lo(kk[j].w[e]);
-            dp += qf[2 * e + 1] * bf_hi(kk[j].w[e]);
-        }
-        dp = lanes_sum<AttnRegs<D>::LPR>(dp);
+        const float dp = lanes_sum<AttnRegs<D>::LPR>(lane_dot<NW>(qw, kk[j])) * qscale;
         s[j] = (t0 + j * ROWS + row < t_end) ? dp : -INFINITY;
         mx = fmaxf(mx, s[j]);
     }
@@ -247,32 +255,23 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     float acc[VPL];
 #pragma unroll
     for (int e = 0; e < VPL; ++e) acc[e] = 0.f;
-    float qf[VPL];
-    // q in fp32, pre-scaled; then the append's stores, and the new token as the
-    // first token of the softmax: every row of wavefront 0 holds its K/V row,
-    // so each computes its logit and takes it as the starting max; row 0
-    // counts it and writes its K/V row, its position and q's row of the query
-    // ring
+    uint32_t qw[NW];
+    // q's bf16 pairs (the logits are scaled after the dot products); then the
+    // append's stores, and the new token as the first token of the softmax:
+    // every row of wavefront 0 holds its K/V row, so each computes its logit
+    // and takes it as the starting max; row 0 counts it and writes its K/V
+    // row, its position and q's row of the query ring
     auto begin = [&]() {
-        // an opaque copy of q, so that its conversion (common to both
-        // branches below) is not hoisted in front of the K/V loads, where it
-        // would wait for q
+        // an opaque copy of q, so that its use (common to both branches
+        // below) is not hoisted in front of the K/V loads, where it would
+        // wait for q
         Vec qv = qraw;
         static_assert(NW == 4, "four words per lane");
         asm volatile("" : "+v"(qv.w[0]), "+v"(qv.w[1]), "+v"(qv.w[2]), "+v"(qv.w[3]));
 #pragma unroll
-        for (int e = 0; e < NW; ++e) {
-            qf[2 * e] = bf_lo(qv.w[e]) * qscale;
-            qf[2 * e + 1] = bf_hi(qv.w[e]) * qscale;
-        }
+        for (int e = 0; e < NW; ++e) qw[e] = qv.w[e];
         if (newtok) {
-            float dp = 0.f;
-#pragma unroll
-            for (int e = 0; e < NW; ++e) {
-                dp += qf[2 * e] * bf_lo(kn.w[e]);
-                dp += qf[2 * e + 1] * bf_hi(kn.w[e]);
-            }
-            m = lanes_sum<LPR>(dp);
+            m = lanes_sum<LPR>(lane_dot<NW>(qw, kn)) * qscale;
             if (row == 0) {
                 *reinterpret_cast<Vec*>(K + (size_t)len_c * D + col * VPL) = kn;
                 *reinterpret_cast<Vec*>(V + (size_t)len_c * D + col * VPL) = vn;
@@ -303,7 +302,7 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
         // keep every load of the pass ahead of its first use
         __builtin_amdgcn_sched_barrier(0);
         begin();
-        attn_accumulate<D, TPR, ROWS>(kk, vv, t_begin, row, s_end, qf, m, l, acc);
+        attn_accumulate<D, TPR, ROWS>(kk, vv, t_begin, row, s_end, qw, qscale, m, l, acc);
     } else {
         begin();
     }
@@ -316,7 +315,7 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
         for (int j = 0; j < TPR; ++j)
             vv[j] = nt_load<NW>(V + (size_t)min(t0 + j * ROWS + row, s_stop - 1) * D + col * VPL);
         __builtin_amdgcn_sched_barrier(0);
-        attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, s_end, qf, m, l, acc);
+        attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, s_end, qw, qscale, m, l, acc);
     }
     // merge the rows of each wavefront: they share its max, so by sums; every
     // exchange of a step is issued before the first is used
