@@ -143,8 +143,17 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
         s[j] = (t0 + j * ROWS + row < t_end) ? dp : -INFINITY;
         mx = fmaxf(mx, s[j]);
     }
+    // the wavefront's max: the row sums leave the same value in every lane of
+    // a row (each of their steps adds a symmetric pair of lanes), so one lane
+    // per row is read directly instead of exchanging through LDS
+    {
+        constexpr int LPR = AttnRegs<D>::LPR;
+        float wm = mx;
 #pragma unroll
-    for (int off = AttnRegs<D>::LPR; off <= 32; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        for (int r = 0; r < 64 / LPR; ++r)
+            wm = fmaxf(wm, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mx), r * LPR)));
+        mx = wm;
+    }
     if (mx != -INFINITY) {
         const float f = __builtin_amdgcn_exp2f(m - mx);  // m = -inf gives 0
         l *= f;
