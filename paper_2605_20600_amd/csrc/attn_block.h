@@ -122,6 +122,17 @@ __device__ __forceinline__ float lane_dot(const uint32_t* qw, const Words<NW>& k
     return dp;
 }
 
+// Row padding (floats) of the end-of-block merge buffer: lane g of a column
+// reads row g * wpg + k, so rows wpg apart must start 64 / g_lanes banks
+// apart (64 banks of 4 bytes) for the g_lanes lanes of a column to read
+// without conflicts
+constexpr int merge_pad(int wpg, int d, int g_lanes) {
+    if (g_lanes == 1) return 0;
+    for (int pad = 0; pad < 64; ++pad)
+        if ((wpg * (d + pad)) % 64 == 64 / g_lanes) return pad;
+    return -1;
+}
+
 // Online-softmax update of one row's state with NT tokens t0 + j * ROWS + row
 // (those at or past t_end masked); k/v hold their d/16 elements of the lane.
 // The running max is the wavefront's (the same in all its rows), taken over
@@ -339,8 +350,19 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
 #pragma unroll
         for (int e = 0; e < VPL; ++e) acc[e] += ao[e];
     }
+    // G adjacent lanes per output column merge the wavefronts' partials
+    // below: 4 in a 1024-thread block that owns its CU, where the tail of the
+    // merge is the launch's; 1 elsewhere (in 512-thread blocks, two to a CU,
+    // and with the chunk merge's atomics after it, spreading it measured
+    // slower).  The rows of sacc are padded so that the G lanes of a column,
+    // which read different rows, fall in different LDS banks.
+    constexpr int G = (!CHUNKED && T == 1024 && T / D >= 4) ? 4 : 1;
+    constexpr int WPG = WAVES / G;
+    static_assert(WAVES % G == 0 && G * D <= T, "merge groups");
+    constexpr int PAD = merge_pad(WPG, D, G);
+    static_assert(PAD >= 0, "no conflict-free padding");
     __shared__ float sm[WAVES], sl[WAVES];
-    __shared__ float sacc[WAVES][D];
+    __shared__ float sacc[WAVES][D + PAD];
     if (lane < LPR) {
 #pragma unroll
         for (int e = 0; e < VPL; ++e) sacc[wave][col * VPL + e] = acc[e];
@@ -350,32 +372,51 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
         }
     }
     __syncthreads();
-    if (tid < D) {
-        // all LDS reads first: the merge runs on two wavefronts at the very end
-        // of the block, where each serial LDS latency adds to the launch
-        float mw[WAVES], lw[WAVES], xw[WAVES];
+    // each of a column's G lanes merges WAVES / G of the wavefronts'
+    // partials, then the G lanes are combined with DPP steps: the merge at
+    // the very end of the block, where every serial step adds to the launch,
+    // is spread over G times the lanes.  All LDS reads are issued first.
+    if (tid < G * D) {
+        const int c = tid / G, g = tid % G;
+        float mw[WPG], lw[WPG], xw[WPG];
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) {
-            mw[w] = sm[w];
-            lw[w] = sl[w];
-            xw[w] = sacc[w][tid];
+        for (int k = 0; k < WPG; ++k) {
+            mw[k] = sm[g * WPG + k];
+            lw[k] = sl[g * WPG + k];
+            xw[k] = sacc[g * WPG + k][c];
         }
         __builtin_amdgcn_sched_barrier(0);
         float mx = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) mx = fmaxf(mx, mw[w]);
+        for (int k = 0; k < WPG; ++k) mx = fmaxf(mx, mw[k]);
+        // the column's max over its G lanes (symmetric pairs: the same value
+        // in all of them)
+        if (G >= 2)
+            mx = fmaxf(mx, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(mx), 0xB1, 0xF, 0xF, false)));
+        if (G >= 4)
+            mx = fmaxf(mx, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(mx), 0x4E, 0xF, 0xF, false)));
         float o = 0.f, z = 0.f;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) {
-            const float f = (mw[w] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mw[w] - mx);
-            o += f * xw[w];
-            z += f * lw[w];
+        for (int k = 0; k < WPG; ++k) {
+            const float f = (mw[k] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mw[k] - mx);
+            o += f * xw[k];
+            z += f * lw[k];
         }
-        if (!CHUNKED || nch == 1)
-            out[(size_t)h * D + tid] = o / z;
-        else
-            chunk_merge<D>(h, nch, t_begin / TP, i0, o / z, mx + __builtin_amdgcn_logf(z), out,
-                           part, tid);
+        if (G >= 2) {
+            o += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(o), 0xB1, 0xF, 0xF, false));
+            z += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(z), 0xB1, 0xF, 0xF, false));
+        }
+        if (G >= 4) {
+            o += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(o), 0x4E, 0xF, 0xF, false));
+            z += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(z), 0x4E, 0xF, 0xF, false));
+        }
+        if (g == 0) {
+            if (!CHUNKED || nch == 1)
+                out[(size_t)h * D + c] = o / z;
+            else
+                chunk_merge<D>(h, nch, t_begin / TP, i0, o / z, mx + __builtin_amdgcn_logf(z),
+                               out, part, c);
+        }
     }
 }
 
