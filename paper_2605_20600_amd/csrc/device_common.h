@@ -37,18 +37,29 @@ __device__ __forceinline__ float lanes_sum(float v) {
     return v;
 }
 
+// Inclusive prefix sum over the 64 lanes of a wavefront (all active): within
+// each row of 16 lanes by DPP row shifts (lanes whose source lies outside
+// the row add 0), then the totals of the rows before, read from lanes 15, 31
+// and 47 (no exchange through LDS)
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+    int v = x;
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+    const int r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31),
+              r2 = __builtin_amdgcn_readlane(v, 47);
+    const int row = (threadIdx.x & 63) >> 4;
+    return v + (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
+}
+
 // Exclusive prefix sum over a block of NT threads (256 by default);
 // *total receives the sum.  Every thread of the block must call it.
 template <int NT = kBlock>
 __device__ inline int block_exclusive_scan(int x, int* total) {
     __shared__ int wsum[NT / 64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    int inc = x;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int y = __shfl_up(inc, o);
-        if (lane >= o) inc += y;
-    }
+    const int inc = wave_inclusive_scan(x);
     if (lane == 63) wsum[wave] = inc;
     __syncthreads();
     int off = 0, tot = 0;
