@@ -292,9 +292,10 @@ __device__ void select_small(double* sig, const uint16_t* order, uint8_t* evict,
         const uint64_t kj = key[j];
         c += (j < r ? kj <= kr : kj < kr) ? 1 : 0;
     }
-    // the Q lanes of an entry are all here
-    c += __shfl_xor(c, 1);
-    if (Q == 4) c += __shfl_xor(c, 2);
+    // the Q lanes of an entry (an aligned pair or quad) are all here: summed
+    // within the quad by DPP
+    c += __builtin_amdgcn_update_dpp(0, c, 0xB1, 0xF, 0xF, false);  // lane ^ 1
+    if (Q == 4) c += __builtin_amdgcn_update_dpp(0, c, 0x4E, 0xF, 0xF, false);  // lane ^ 2
     if (q == 0 && c < mq) evict[order[r]] = 1;
 }
 
@@ -829,6 +830,9 @@ __device__ __forceinline__ int update_block(const LayerDev& L, int C, int N, con
             nf += tf;
         }
         __syncthreads();
+        // the two lists have the same length when exactly M slots were
+        // selected; the moves never read past either list
+        nh = nh < nf ? nh : nf;
         uint4* k4 = reinterpret_cast<uint4*>(S.K);
         uint4* v4 = reinterpret_cast<uint4*>(S.V);
         for (int i = tid; i < nh * kRow16; i += NT) {
