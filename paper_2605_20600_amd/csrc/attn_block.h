@@ -134,7 +134,7 @@ constexpr int merge_pad(int wpg, int d, int g_lanes) {
 }
 
 // Online-softmax update of one row's state with NT tokens t0 + j * ROWS + row
-// (those at or past t_end masked); k/v hold their d/16 elements of the lane.
+// (those at or past t_end masked); k/v hold the lane's 8 elements of each row.
 // The running max is the wavefront's (the same in all its rows), taken over
 // the logits before the V rows are used, so that the rows of a wavefront
 // merge at the end by plain sums.
