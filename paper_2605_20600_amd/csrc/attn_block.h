@@ -201,11 +201,11 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     constexpr int ROWS = T / LPR;
     constexpr int TP = ROWS * TPR;  // tokens per pass
     constexpr int WAVES = T / 64;
-    int h, t_begin;
+    int h, chunk = 0;
     if (CHUNKED) {
         const uint32_t it = L.items[item];
         h = (int)(it >> 8);
-        t_begin = (int)(it & 255u) * TP;
+        chunk = (int)(it & 255u);
     } else {
         // through a vector load: a scalar one would leave its wait at the
         // join of the two paths, where it also waits for the kernel arguments
@@ -217,7 +217,6 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
             asm("" : "+v"(lane0));
             h = __builtin_amdgcn_readfirstlane(L.order[order_base + item + lane0]);
         }
-        t_begin = 0;
     }
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = tid / LPR, col = tid % LPR;
@@ -243,12 +242,15 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     // attended as token len_c, from the input
     const int len_c = C + n;
     const int len = len_c + (APPEND ? 1 : 0);
-    // chunked: only the chunks that hold tokens take part (a chunk past the
-    // head's length has nothing to do), and the only chunk of a head that
-    // fits in one writes the output itself, without partials
+    // chunked: the fewest chunks of at most one pass that hold the head's
+    // tokens take part, with equal shares of them (the later table entries of
+    // the head have nothing to do), and the only chunk of a head that fits in
+    // one writes the output itself, without partials
     const int nch = len > TP ? (len + TP - 1) / TP : 1;
-    if (CHUNKED && t_begin >= nch * TP) return;
-    const int t_end = CHUNKED ? min(len, t_begin + TP) : len;
+    const int per = (len + nch - 1) / nch;  // at most TP
+    if (CHUNKED && chunk >= nch) return;
+    const int t_begin = CHUNKED ? chunk * per : 0;
+    const int t_end = CHUNKED ? min(len, t_begin + per) : len;
     // cache rows this block streams: [t_begin, s_end); the padding strategy
     // reads the rows of the layer's longest head (pad_len attended tokens, the
     // appended one included, which comes from the input), those past s_end
@@ -414,7 +416,7 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
             if (!CHUNKED || nch == 1)
                 out[(size_t)h * D + c] = o / z;
             else
-                chunk_merge<D>(h, nch, t_begin / TP, i0, o / z, mx + __builtin_amdgcn_logf(z),
+                chunk_merge<D>(h, nch, chunk, i0, o / z, mx + __builtin_amdgcn_logf(z),
                                out, part, c);
         }
     }
