@@ -128,8 +128,8 @@ typedef struct headkv_ctx* headkv_t;
  *                   attention chunk table;
  *   workspace_bytes: one buffer shared by all layers: the merge words of the
  *                   attention of layers with fewer heads than compute units,
- *                   which cut each head into chunks of one pass and merge
- *                   them in the same kernel.  The library zeroes it before
+ *                   which cut each head into chunks of at most one pass
+ *                   and merge them in the same kernel.  The library zeroes it before
  *                   its first use and every launch leaves it zero; callers
  *                   must not write it while a handle uses it. */
 headkv_status headkv_plan(const headkv_config* cfg, size_t* dense_kv_bytes,

@@ -418,9 +418,10 @@ int resident_threads(int heads) {
 
 // The attention launches of one layer step (appended: the step's token is
 // attended from the input).  Returns their number (1 or 2).
-//  VARLEN, fewer heads than CUs: the layer's chunk table, chunks of one pass
-//    balanced across heads of unequal length, merged in the same kernel
-//    (a tree of atomic exchanges over each head's chunks).
+//  VARLEN, fewer heads than CUs: the layer's chunk table, chunks of at most
+//    one pass (at each launch the fewest that hold a head's length, sharing
+//    its tokens evenly), balanced across heads of unequal length, merged in
+//    the same kernel (a tree of atomic exchanges over each head's chunks).
 //  VARLEN otherwise: one block per head over all its passes (no merge, the
 //    append fused), at the largest block size at which every head's block is
 //    resident at once (beyond that 256-thread blocks); longest heads first
