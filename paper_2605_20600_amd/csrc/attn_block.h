@@ -137,16 +137,13 @@ constexpr int merge_pad(int wpg, int d, int g_lanes) {
 // (those at or past t_end masked); k/v hold the lane's 8 elements of each row.
 // The running max is the wavefront's (the same in all its rows), taken over
 // the logits before the V rows are used, so that the rows of a wavefront
-// merge at the end by plain sums.
+// merge at the end by plain sums.  In two halves: the logits and the new
+// running max from the K rows, then the weights and their V rows.
 template <int D, int NT, int ROWS>
-__device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec (&kk)[NT],
-                                                const typename AttnRegs<D>::Vec (&vv)[NT],
-                                                int t0, int row, int t_end,
-                                                const uint32_t* qw, float qscale,
-                                                float& m, float& l, float* acc) {
+__device__ __forceinline__ float attn_logits(const typename AttnRegs<D>::Vec (&kk)[NT], int t0,
+                                             int row, int t_end, const uint32_t* qw, float qscale,
+                                             float m, float (&s)[NT]) {
     constexpr int NW = AttnRegs<D>::NW;
-    constexpr int VPL = AttnRegs<D>::VPL;
-    float s[NT];
     float mx = m;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
@@ -157,14 +154,20 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
     // the wavefront's max: the row sums leave the same value in every lane of
     // a row (each of their steps adds a symmetric pair of lanes), so one lane
     // per row is read directly instead of exchanging through LDS
-    {
-        constexpr int LPR = AttnRegs<D>::LPR;
-        float wm = mx;
+    constexpr int LPR = AttnRegs<D>::LPR;
+    float wm = mx;
 #pragma unroll
-        for (int r = 0; r < 64 / LPR; ++r)
-            wm = fmaxf(wm, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mx), r * LPR)));
-        mx = wm;
-    }
+    for (int r = 0; r < 64 / LPR; ++r)
+        wm = fmaxf(wm, __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mx), r * LPR)));
+    return wm;
+}
+
+template <int D, int NT>
+__device__ __forceinline__ void attn_weigh(const typename AttnRegs<D>::Vec (&vv)[NT],
+                                           const float (&s)[NT], float mx, float& m, float& l,
+                                           float* acc) {
+    constexpr int NW = AttnRegs<D>::NW;
+    constexpr int VPL = AttnRegs<D>::VPL;
     if (mx != -INFINITY) {
         const float f = __builtin_amdgcn_exp2f(m - mx);  // m = -inf gives 0
         l *= f;
@@ -182,6 +185,17 @@ __device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec 
         }
         m = mx;
     }
+}
+
+template <int D, int NT, int ROWS>
+__device__ __forceinline__ void attn_accumulate(const typename AttnRegs<D>::Vec (&kk)[NT],
+                                                const typename AttnRegs<D>::Vec (&vv)[NT],
+                                                int t0, int row, int t_end,
+                                                const uint32_t* qw, float qscale,
+                                                float& m, float& l, float* acc) {
+    float s[NT];
+    const float mx = attn_logits<D, NT, ROWS>(kk, t0, row, t_end, qw, qscale, m, s);
+    attn_weigh<D, NT>(vv, s, mx, m, l, acc);
 }
 
 // The work of one attention block; `item` is its index among the blocks of
@@ -314,30 +328,52 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
     // V rows are still arriving.  A chunk past the head's cached length reads
     // nothing.
     Vec kk[TPR], vv[TPR];
-    if (t_begin < s_stop) {
-#pragma unroll
-        for (int j = 0; j < TPR; ++j)
-            kk[j] = nt_load<NW>(K + (size_t)min(t_begin + j * ROWS + row, s_stop - 1) * D + col * VPL);
-#pragma unroll
-        for (int j = 0; j < TPR; ++j)
-            vv[j] = nt_load<NW>(V + (size_t)min(t_begin + j * ROWS + row, s_stop - 1) * D + col * VPL);
-        // keep every load of the pass ahead of its first use
-        __builtin_amdgcn_sched_barrier(0);
-        begin();
-        attn_accumulate<D, TPR, ROWS>(kk, vv, t_begin, row, s_end, qw, qscale, m, l, acc);
-    } else {
-        begin();
-    }
-    // further passes of a head longer than one pass
-    for (int t0 = t_begin + TP; t0 < s_stop; t0 += TP) {
+    auto load_k = [&](int t0) {
 #pragma unroll
         for (int j = 0; j < TPR; ++j)
             kk[j] = nt_load<NW>(K + (size_t)min(t0 + j * ROWS + row, s_stop - 1) * D + col * VPL);
+    };
+    auto load_v = [&](int t0) {
 #pragma unroll
         for (int j = 0; j < TPR; ++j)
             vv[j] = nt_load<NW>(V + (size_t)min(t0 + j * ROWS + row, s_stop - 1) * D + col * VPL);
+    };
+    // a head longer than one pass (only at the full pass of 8 tokens per row:
+    // the other widths are picked when every head fits in one pass, and a
+    // chunk holds at most one) requests the next pass's K rows as soon as
+    // this pass's logits are taken, and its V rows once this pass's are
+    // accumulated, so that the stream runs on across passes; every request
+    // is unconditional, so that no join makes the compiler wait for all
+    constexpr bool kPipe = TPR == kAttnTpr && !CHUNKED;
+    int t0 = t_begin;
+    if (t_begin < s_stop) {
+        load_k(t_begin);
+        load_v(t_begin);
+        // keep every load of the pass ahead of its first use
         __builtin_amdgcn_sched_barrier(0);
+        begin();
+        if constexpr (kPipe) {
+            for (; t0 + TP < s_stop; t0 += TP) {
+                float s[TPR];
+                const float mx = attn_logits<D, TPR, ROWS>(kk, t0, row, s_end, qw, qscale, m, s);
+                load_k(t0 + TP);
+                __builtin_amdgcn_sched_barrier(0);
+                attn_weigh<D, TPR>(vv, s, mx, m, l, acc);
+                load_v(t0 + TP);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
         attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, s_end, qw, qscale, m, l, acc);
+    } else {
+        begin();
+    }
+    if constexpr (!kPipe) {
+        for (t0 += TP; t0 < s_stop; t0 += TP) {
+            load_k(t0);
+            load_v(t0);
+            __builtin_amdgcn_sched_barrier(0);
+            attn_accumulate<D, TPR, ROWS>(kk, vv, t0, row, s_end, qw, qscale, m, l, acc);
+        }
     }
     // merge the rows of each wavefront: they share its max, so by sums; every
     // exchange of a step is issued before the first is used
