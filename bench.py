@@ -14,7 +14,9 @@ kernel (the dominant one) against MI355X's 8 TB/s HBM peak with algorithmic
 bytes; `cpu_baseline` times the fp64 CPU oracle on a bounded sample;
 `all_layer_launch` (layouts of 256 to 1024 heads) times, outside the timed
 region, the last step's attention as one launch per layer and as one launch
-for all layers, which shows the per-launch share of the roofline gap.
+for all layers, which shows the per-launch share of the roofline gap;
+`roofline.plain_read` is the same-size plain read in one launch on the same
+box (the ceiling for one launch per layer) and the kernel's share of it.
 """
 from __future__ import annotations
 
@@ -290,6 +292,37 @@ def rocprof_roofline(alg_bytes: float):
     return {"frac_rocprof": alg_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS,
             "avg_launch_us_rocprof": us, "launches_rocprof": c["calls"],
             "rocprof_record": os.path.relpath(KTRACE_RECORD, ROOT)}
+
+
+# The headline attention launch reads 48.5 MB of algorithmic bytes: 46 MiB.
+PLAIN_READ_MIB = 46
+
+
+def plain_read_ceiling(mib: int):
+    """The one-launch streaming ceiling on this machine: the stream probe (built
+    with the library) reads `mib` MiB in one launch of 256 x 1024 threads,
+    640 times, each launch timed by its own start/stop events as the
+    attention's are.  Run as a child process before this process touches the
+    GPU; the kernel's share of the ceiling is added once the attention is
+    measured."""
+    import re
+    import subprocess
+    probe = os.path.join(ROOT, "paper_2605_20600_amd", "stream_probe")
+    if not os.path.exists(probe):
+        return None
+    try:
+        res = subprocess.run([probe, str(mib), "640"], capture_output=True, text=True,
+                             timeout=120, check=True)
+    except (subprocess.SubprocessError, OSError) as e:
+        return {"error": str(e)[:200]}
+    m = re.search(rf"read {mib} MB, 256 x 1024 threads\s+([0-9.]+) us per launch back to back,"
+                  r"\s+([0-9.]+) us per launch from its own events", res.stdout)
+    if not m:
+        return {"error": "unexpected probe output"}
+    b2b, own = float(m.group(1)), float(m.group(2))
+    frac = mib * 2**20 / (own * 1e-6) / 1e9 / HBM_PEAK_GBPS
+    return {"probe": f"stream_probe {mib} 640", "bytes": mib * 2**20,
+            "us_events": own, "us_back_to_back": b2b, "frac_events": frac}
 
 
 def cpu_baseline(wl, seconds_target: float):
@@ -606,6 +639,14 @@ def main():
     if args.kernel_trace_record:
         write_kernel_trace_record(args.kernel_trace_record)
         return
+    # the headline run measures the plain-read ceiling first, as a child
+    # process, before this one touches the GPU
+    ceiling = None
+    if (args.workload == "lumina_mgpt_768" and args.rho in (None, "1/8") and not args.copy_probe
+            and args.method == "headkv" and args.attn_strategy == "varlen"
+            and args.score_mode == "mean_logit" and not args.label_stability
+            and not args.all_layer_launch):
+        ceiling = plain_read_ceiling(PLAIN_READ_MIB)
     import torch
     if args.copy_probe:
         src = torch.empty(512 << 20, dtype=torch.uint8, device="cuda").fill_(1)
@@ -668,6 +709,9 @@ def main():
     }
     if headline and dominant == KIND_NAMES[0]:
         roof.update(rocprof_roofline(dom["alg_bytes_per_launch"]))
+        if ceiling and "frac_events" in ceiling:
+            ceiling["kernel_share"] = roof["frac_events"] / ceiling["frac_events"]
+        roof["plain_read"] = ceiling
     line = {
         "metric": METRIC,
         "value": r["tokens_per_s"],
