@@ -144,6 +144,20 @@ def test_large_logits_many_heads_several_passes():
     _run(wl, budgets=bud, slices=((0, 0), (0, 7)), steps=[0, 511, 599, 600, 601, 900, 1023])
 
 
+def test_pass_boundaries_d128():
+    # 8 x 32 = 256 heads of d = 128: one 1024-thread block per head.  Before
+    # grouping every head caches C + t tokens at step t and attends one more,
+    # so these steps stream 575 cached rows (one wide pass of 9 tokens per
+    # row), then 576, 1024, 1025, 1536 and 1537 rows in passes of 512: two,
+    # two full, three with one row in the last, three full, four.  From the second
+    # pass on, each pass's rows are requested while the previous one finishes.
+    wl = W.TINY.with_(batch=8, heads=32, head_dim=128, grid_rows=40, grid_cols=41, period=41,
+                      group_threshold=1600)
+    C = wl.prefix_len
+    steps = [n - C for n in (575, 576, 1024, 1025, 1536, 1537)] + [1600, 1639]
+    _run(wl, slices=((0, 0), (0, 7)), steps=steps)
+
+
 def test_limits_prefix_capacity_and_length():
     # the documented limits at once: a 2048-token prefix, 16384 visual tokens
     # and heads holding HEADKV_MAX_CAPACITY = 4608 visual tokens (budget 4480 +
