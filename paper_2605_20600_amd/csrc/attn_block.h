@@ -338,13 +338,13 @@ __device__ __forceinline__ void attn_block(const LayerDev& L, int C, const Appen
         for (int j = 0; j < TPR; ++j)
             vv[j] = nt_load<NW>(V + (size_t)min(t0 + j * ROWS + row, s_stop - 1) * D + col * VPL);
     };
-    // a head longer than one pass (only at the full pass of 8 tokens per row:
-    // the other widths are picked when every head fits in one pass, and a
-    // chunk holds at most one) requests the next pass's K rows as soon as
+    // a head longer than one pass (only at 8 or 6 tokens per row: the other
+    // widths are picked when every head fits in one pass, and a chunk holds
+    // at most one) requests the next pass's K rows as soon as
     // this pass's logits are taken, and its V rows once this pass's are
     // accumulated, so that the stream runs on across passes; every request
     // is unconditional, so that no join makes the compiler wait for all
-    constexpr bool kPipe = TPR == kAttnTpr && !CHUNKED;
+    constexpr bool kPipe = (TPR == kAttnTpr || TPR == kAttnTprShort) && !CHUNKED;
     int t0 = t_begin;
     if (t_begin < s_stop) {
         load_k(t_begin);
