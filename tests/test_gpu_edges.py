@@ -146,15 +146,18 @@ def test_large_logits_many_heads_several_passes():
 
 def test_pass_boundaries_d128():
     # 8 x 32 = 256 heads of d = 128: one 1024-thread block per head.  Before
-    # grouping every head caches C + t tokens at step t and attends one more,
-    # so these steps stream 575 cached rows (one wide pass of 9 tokens per
-    # row), then 576, 1024, 1025, 1536 and 1537 rows in passes of 512: two,
-    # two full, three with one row in the last, three full, four.  From the second
-    # pass on, each pass's rows are requested while the previous one finishes.
+    # grouping every head caches C + t tokens at step t and attends one more;
+    # a launch whose heads need more than one pass takes passes of 512 or 384
+    # tokens, whichever loads fewer rows in all, each pass's rows requested
+    # while the previous one finishes.  Cached rows at the steps below: 575
+    # (one wide pass of 576), 576 and 767 (two of 384: the second with 192 and
+    # 383 rows), 768 and 1023 (two of 512), 1024 (three of 384), 1535 (three of
+    # 512, the last with 511 rows), 1536 (four of 384, all full)
     wl = W.TINY.with_(batch=8, heads=32, head_dim=128, grid_rows=40, grid_cols=41, period=41,
                       group_threshold=1600)
     C = wl.prefix_len
-    steps = [n - C for n in (575, 576, 1024, 1025, 1536, 1537)] + [1600, 1639]
+    rows = (575, 576, 767, 768, 1023, 1024, 1535, 1536)
+    steps = [n - C for n in rows] + [1600, 1639]
     _run(wl, slices=((0, 0), (0, 7)), steps=steps)
 
 
